@@ -1,0 +1,155 @@
+"""Seeded synthetic inputs shared by the oracle-side tests and the GPU path.
+
+This module only draws random numbers and rounds them to the storage dtypes
+(float32 weights, bfloat16 / float16 activation bit patterns).  It holds none
+of the CubicQuant arithmetic: no packing, no level function, no fitting, no
+quantizer.  Every generator uses numpy's PCG64 with its own seed, draws in
+float64 and rounds once.
+
+The workloads are the layer shapes and value laws of the benchmark
+configurations:
+  * ``gemv_4k``    M=1, K=N=4096; x ~ N(0,1) (seed 0), W ~ N(0, 0.02^2) (seed 1).
+  * ``llama8b``    Llama-3-8B-shaped decode layers (K, N) in
+    {(4096, 6144) QKV, (4096, 4096) O, (4096, 28672) gate+up, (14336, 4096) down},
+    M in {1, 4, 16}; W ~ Laplace(0, 0.014) with ceil(0.01 K) input channels
+    scaled x8; x ~ N(0,1) times a per-token factor ~ U[0.5, 4].
+  * ``sweep``      M=1, K=N=8192, W ~ N(0, 0.015^2), every B x G.
+  * ``crossover``  K=8192, N=28672, M in {1 .. 8192}; W ~ Student-t(5) scaled to
+    std 0.02; x ~ N(0,1) with 0.5% of entries scaled x20.
+  * ``prefill70b`` M in {2048, 8192}, (K, N) in {(8192, 28672), (28672, 8192),
+    (8192, 10240)}; W ~ Laplace(0, 0.01) times a per-row factor log-uniform in
+    [0.5, 2]; x ~ N(0,1).
+Seeds: for workload number c (1..5) tensor t uses 1000*c + t, except the first
+workload whose x uses seed 0 and W seed 1.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+LLAMA8B_LAYERS = (("qkv", 4096, 6144), ("o_proj", 4096, 4096),
+                  ("gate_up", 4096, 28672), ("down", 14336, 4096))
+PREFILL70B_SHAPES = ((8192, 28672), (28672, 8192), (8192, 10240))
+CROSSOVER_M = (1, 2, 8, 32, 128, 512, 2048, 8192)
+
+
+def rng(seed: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(seed))
+
+
+def to_f32(x) -> np.ndarray:
+    return np.asarray(x, dtype=np.float64).astype(np.float32)
+
+
+def to_bf16_bits(x) -> np.ndarray:
+    """Round float64 -> float32 -> bfloat16 (nearest even), return uint16 bits."""
+    f = np.ascontiguousarray(np.asarray(x, dtype=np.float64).astype(np.float32))
+    u = f.view(np.uint32).astype(np.uint64)
+    lsb = (u >> 16) & 1
+    r = ((u + 0x7FFF + lsb) >> 16).astype(np.uint16)
+    nan = np.isnan(f)
+    if np.any(nan):
+        r = np.where(nan, np.uint16(0x7FC0), r)
+    return r
+
+
+def to_f16_bits(x) -> np.ndarray:
+    return np.asarray(x, dtype=np.float64).astype(np.float16).view(np.uint16)
+
+
+def bf16_bits_to_f32(bits) -> np.ndarray:
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16
+    return b.view(np.float32)
+
+
+# ---------------------------------------------------------------- value laws
+
+
+def normal(seed: int, shape, std: float = 1.0) -> np.ndarray:
+    return rng(seed).standard_normal(shape) * std
+
+
+def laplace(seed: int, shape, b: float) -> np.ndarray:
+    return rng(seed).laplace(0.0, b, shape)
+
+
+def student_t(seed: int, shape, nu: float, std: float) -> np.ndarray:
+    return rng(seed).standard_t(nu, shape) * (std / math.sqrt(nu / (nu - 2.0)))
+
+
+# ---------------------------------------------------------------- workloads
+
+
+def gemv_4k():
+    """(x bf16 bits [1, 4096], W float32 [4096, 4096])."""
+    x = to_bf16_bits(normal(0, (1, 4096)))
+    w = to_f32(normal(1, (4096, 4096), 0.02))
+    return x, w
+
+
+def llama8b_weight(layer: int, k: int, n: int) -> np.ndarray:
+    """Laplace(0, 0.014) weights [N, K], ceil(0.01 K) input channels x8."""
+    w = laplace(2000 + 2 * layer, (n, k), 0.014)
+    cols = rng(2001 + 2 * layer).choice(k, size=math.ceil(0.01 * k), replace=False)
+    w[:, cols] *= 8.0
+    return to_f32(w)
+
+
+def llama8b_act(m: int, k: int, seed_offset: int = 0) -> np.ndarray:
+    """bf16 bits [M, K]: N(0,1) rows times a per-token factor ~ U[0.5, 4]."""
+    x = normal(2100 + seed_offset, (m, k))
+    u = rng(2101 + seed_offset).uniform(0.5, 4.0, (m, 1))
+    return to_bf16_bits(x * u)
+
+
+def sweep_weight(k: int = 8192, n: int = 8192) -> np.ndarray:
+    return to_f32(normal(3001, (n, k), 0.015))
+
+
+def sweep_act(k: int = 8192) -> np.ndarray:
+    return to_bf16_bits(normal(3002, (1, k)))
+
+
+def crossover_weight(k: int = 8192, n: int = 28672) -> np.ndarray:
+    return to_f32(student_t(4001, (n, k), 5.0, 0.02))
+
+
+def crossover_act(m: int, k: int = 8192) -> np.ndarray:
+    x = normal(4002, (m, k))
+    mask = rng(4003).random((m, k)) < 0.005
+    x[mask] *= 20.0
+    return to_bf16_bits(x)
+
+
+def prefill70b_weight(k: int, n: int, seed_offset: int = 0) -> np.ndarray:
+    w = laplace(5001 + seed_offset, (n, k), 0.01)
+    mult = np.exp(rng(5002 + seed_offset).uniform(math.log(0.5), math.log(2.0), (n, 1)))
+    return to_f32(w * mult)
+
+
+def prefill70b_act(m: int, k: int) -> np.ndarray:
+    return to_bf16_bits(normal(5003, (m, k)))
+
+
+def small_weight(seed: int, n: int, k: int, law: str = "laplace") -> np.ndarray:
+    """Small test matrices with the same laws as the workloads."""
+    if law == "laplace":
+        w = laplace(seed, (n, k), 0.014)
+        cols = rng(seed + 1).choice(k, size=max(1, math.ceil(0.01 * k)), replace=False)
+        w[:, cols] *= 8.0
+    elif law == "normal":
+        w = normal(seed, (n, k), 0.02)
+    elif law == "student":
+        w = student_t(seed, (n, k), 5.0, 0.02)
+    else:
+        raise ValueError(law)
+    return to_f32(w)
+
+
+def small_act(seed: int, m: int, k: int, outliers: bool = True) -> np.ndarray:
+    x = normal(seed, (m, k)) * rng(seed + 1).uniform(0.5, 4.0, (m, 1))
+    if outliers:
+        mask = rng(seed + 2).random((m, k)) < 0.005
+        x[mask] *= 20.0
+    return to_bf16_bits(x)
