@@ -1,0 +1,179 @@
+/*
+ * cq.h -- C ABI of the CubicQuant hot path on AMD Instinct MI355X (gfx950).
+ *
+ * CubicQuant (arXiv 2608.06763) stores a weight matrix W of logical shape
+ * N x K (output rows x input channels) as:
+ *   - a packed B-bit code stream, B in 1..8 (Sec. 2.1, eq. codes): codes
+ *     k in [-M, M] with M = 2^(B-1) - 1, stored as two's-complement B-bit
+ *     fields; the pattern -2^(B-1) is reserved and decodes to zero; W1 stores
+ *     one bit per weight, 1 meaning +1 and 0 meaning -1.  Fields are laid out
+ *     row-major as one continuous bitstream per row, least significant bit
+ *     first: field j of a row occupies stream bits [jB, jB+B), and stream bit
+ *     p is bit (p mod 8) of byte floor(p/8) (Sec. 2.1, Sec. 5.2
+ *     eq. gpu-packed-extraction).  Fields may straddle bytes (W3, W5..W7).
+ *   - per [1, G] group along K (Sec. 2.3): one FP32 scale s and two FP16
+ *     shape values a, b, as three row-major N x (K/G) tensors.  c = 1 - a - b
+ *     is derived.  64 bits of metadata per group, B + 64/G bits per weight
+ *     (eq. effective-bits).
+ * A code k of a group decodes to w = sign(k) s q(|k|/M) with
+ * q(t) = t [a + t (b + c t)] (Sec. 2.2, eq. cubic); W1 decodes to k s.
+ *
+ * Conventions for every call:
+ *   - All pointers marked "device" are HIP device pointers; the caller owns
+ *     every buffer and keeps it alive until the stream has finished the call.
+ *     The library allocates no memory in any call declared here and keeps no
+ *     state besides a per-device property cache.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Device calls are asynchronous and stream ordered; they validate their
+ *     arguments on the host in O(1) and return a status synchronously.  A
+ *     launch failure is reported as CQ_ERR_HIP.  A fault inside a kernel
+ *     surfaces at the caller's next synchronisation.
+ *   - Device pointers must be 16-byte aligned (CQ_ERR_ALIGN otherwise).
+ *   - Row strides are dense: codes rows are K*B/8 bytes, metadata rows K/G
+ *     entries, activations rows K elements, outputs rows N elements.
+ *   - Hot calls assume metadata validated by cq_pack_groups (finite,
+ *     admissible shapes); they never read outside the described buffers for
+ *     any metadata values.
+ *   - All calls are thread safe.
+ */
+#ifndef CQ_H
+#define CQ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CQ_OK = 0,
+    CQ_ERR_ARG = 1,          /* null pointer, bad width, bad group, m or k <= 0  */
+    CQ_ERR_SHAPE = 2,        /* K % G != 0, K*B % 128 != 0, size overflow        */
+    CQ_ERR_ALIGN = 3,        /* a device pointer is not 16-byte aligned          */
+    CQ_ERR_META = 4,         /* scale or shape values rejected by cq_pack_groups */
+    CQ_ERR_CODE = 5,         /* code outside [-M, M] (W1: outside {-1, +1})      */
+    CQ_ERR_DTYPE = 6,        /* unsupported activation / output dtype            */
+    CQ_ERR_HIP = 7,          /* a HIP runtime call or a kernel launch failed     */
+    CQ_ERR_UNSUPPORTED = 8   /* valid request this build has no kernel for       */
+} cq_status;
+
+typedef enum { CQ_BF16 = 0, CQ_FP16 = 1, CQ_FP32 = 2 } cq_dtype;
+
+/* Borrowed description of one packed weight matrix (never retained). */
+typedef struct {
+    int32_t bits;            /* B in 1..8                                        */
+    int32_t group;           /* G: multiple of 32, 32 <= G <= 512                */
+    int64_t n;               /* N output rows                                    */
+    int64_t k;               /* K input channels; K % G == 0, K*B % 128 == 0     */
+    const uint8_t *codes;    /* device, N x (K*B/8) bytes                        */
+    const float *scale;      /* device, N x (K/G) FP32                           */
+    const uint16_t *a;       /* device, N x (K/G) FP16 bit patterns              */
+    const uint16_t *b;       /* device, N x (K/G) FP16 bit patterns              */
+} cq_weight;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char *cq_status_str(cq_status s);
+
+/*
+ * cq_pack_groups -- validate one quantized matrix and pack its codes (host).
+ *
+ * Implements the storage format of Sec. 2.1-2.3 and Appendix A.  Every
+ * pointer is a HOST pointer.
+ *   codes      N x K signed codes, row-major: [-M, M] for B >= 2 (the reserved
+ *              pattern is never emitted), {-1, +1} for B = 1.
+ *   scale      N x (K/G) FP32; finite and >= 0; 0 only for a group whose codes
+ *              are all zero (B >= 2).
+ *   a, b       N x (K/G) FP16 bit patterns; finite.  For B >= 3 the curve must
+ *              be strictly monotone: m(a, b) > 0 evaluated in float64 on the
+ *              FP16 values (Sec. 3.1, eq. shape-domain; Appendix A item 5).
+ *   packed_out N x (K*B/8) bytes, written only when the call succeeds.
+ *   bad_index  optional; on CQ_ERR_CODE receives the flat index of the first
+ *              bad code, on CQ_ERR_META the flat index of the first bad group.
+ * Group constraints: G*B % 8 == 0, K % G == 0 (CQ_ERR_SHAPE otherwise).  The
+ * host packer accepts any G >= 1 with those properties; device calls further
+ * require G % 32 == 0, G <= 512 and K*B % 128 == 0.
+ * Integer-only and bit exact; O(N K); runs on the calling thread.
+ */
+cq_status cq_pack_groups(int32_t bits, int32_t group, int64_t n, int64_t k,
+                         const int8_t *codes, const float *scale,
+                         const uint16_t *a, const uint16_t *b,
+                         uint8_t *packed_out, int64_t *bad_index);
+
+/*
+ * cq_decode_ref -- materialising decode of a packed matrix (device).
+ *
+ * Unpacks every field with the byte/shift rule of eq. gpu-packed-extraction,
+ * sign-extends it and maps the reserved pattern to 0 (W1: 2u - 1), and
+ * reconstructs w = sign(k) s q(|k|/M) in FP32 (Sec. 5.2, Horner form
+ * eq. gpu-horner).  This is the test reference for the fused kernels and the
+ * "expand, then multiply" baseline; the hot calls never use it.
+ *   codes_out  optional device int8 [N, K]: the signed codes (bit exact).
+ *   w_out      optional device float [N, K]: the FP32 reconstruction.
+ * At least one output must be non-NULL.
+ */
+cq_status cq_decode_ref(const cq_weight *w, int8_t *codes_out, float *w_out, void *stream);
+
+/*
+ * cq_gemm_model_dtype -- y = x W_hat^T with BF16/FP16 activations (device).
+ *
+ * Model-dtype execution of Sec. 5.3: the packed payload and group metadata
+ * are decoded inside the kernel and consumed immediately; no expanded weight
+ * is written.  Narrow row counts use a weight-streaming GEMV; many rows use a
+ * tiled matrix-core GEMM that forms s*q as a BF16/FP16 operand (the dense
+ * rounding point of Sec. 5.3).  Accumulation is FP32.
+ *   x        device [M, K] in x_dtype (CQ_BF16 or CQ_FP16), row-major.
+ *   m        rows of x, >= 1.
+ *   y        device [M, N] in y_dtype: x_dtype, or CQ_FP32 (diagnostics).
+ * The result is deterministic for a given device, shape and dtype.
+ */
+cq_status cq_gemm_model_dtype(const cq_weight *w, const void *x, cq_dtype x_dtype, int64_t m,
+                              void *y, cq_dtype y_dtype, void *stream);
+
+/*
+ * cq_quantize_act_a8 -- dynamic per-row INT8 activation carrier (device).
+ *
+ * Sec. 5.4, eq. a8-activation-scale and eq. a8-activation-quantization:
+ *   xbar = max(max_j |x_j|, eps), eps = 1e-10 rounded to FP32,
+ *   d_x = xbar / 127 (IEEE FP32 division),
+ *   x8_j = clip(round_half_away(x_j / d_x), -127, 127) (IEEE FP32 division).
+ *   x    device [M, K] in x_dtype (CQ_BF16 or CQ_FP16).
+ *   x8   device int8 [M, K];  dx  device float [M].
+ * Bit exact.  An all-zero row yields zero carriers and d_x = eps/127.
+ */
+cq_status cq_quantize_act_a8(const void *x, cq_dtype x_dtype, int64_t m, int64_t k,
+                             int8_t *x8, float *dx, void *stream);
+
+/*
+ * cq_gemm_a8 -- Dynamic-A8 product from INT8 activation carriers (device).
+ *
+ * Sec. 5.4, eq. a8-output: every weight maps to the INT8 carrier
+ * r(k) = sign(k) RNE(127 q(|k|/M)) (Sec. 4.3 eq. carrier; round to nearest
+ * even of the exact value from the FP16 shapes, Appendix A item 7; W1 +-127),
+ * each group forms the exact INT32 partial P_g = sum_j x8_j r(k_j)
+ * (|P_g| <= G 127^2, eq. a8-int32-bound), and
+ *   y = sum_g (d_x s_g / 127) P_g
+ * with the rescale and the cross-group sum in FP32.
+ *   x8, dx        outputs of cq_quantize_act_a8 for the same M and K.
+ *   y             device [M, N] in y_dtype (CQ_BF16, CQ_FP16 or CQ_FP32).
+ *   partials_dbg  optional device int32 [M, N, K/G] receiving every P_g
+ *                 (a debugging output; it slows the call down).
+ */
+cq_status cq_gemm_a8(const cq_weight *w, const int8_t *x8, const float *dx, int64_t m,
+                     void *y, cq_dtype y_dtype, int32_t *partials_dbg, void *stream);
+
+/*
+ * Row-regime kernel selection (Sec. 5.5-5.6).  Each path picks the GEMV
+ * family for m <= its threshold and the tiled GEMM family above it.  The
+ * defaults come from measurements on MI355X.  cq_set_gemv_max_rows
+ * overrides the threshold for one path (0 = model dtype, 1 = Dynamic A8);
+ * a negative value restores the default.  Intended for tests and
+ * benchmarks; process wide.
+ */
+cq_status cq_set_gemv_max_rows(int32_t path, int64_t max_rows);
+int64_t cq_get_gemv_max_rows(int32_t path);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CQ_H */

@@ -1,0 +1,223 @@
+"""MI355X-native CubicQuant hot path: Python binding of ``libcq.so``.
+
+The binding only marshals arguments: every step of the hot path runs in the
+HIP kernels behind the C ABI declared in ``include/cq.h``.  PyTorch provides
+device memory and the current stream.  Importing this package does not need a
+GPU; calling a device entry point does, and a missing library raises.
+
+Entry points (same names as the C ABI):
+  cq_pack_groups, cq_decode_ref, cq_gemm_model_dtype, cq_quantize_act_a8,
+  cq_gemm_a8, cq_set_gemv_max_rows, cq_get_gemv_max_rows
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libcq.so")
+
+CQ_BF16, CQ_FP16, CQ_FP32 = 0, 1, 2
+STATUS = {0: "CQ_OK", 1: "CQ_ERR_ARG", 2: "CQ_ERR_SHAPE", 3: "CQ_ERR_ALIGN", 4: "CQ_ERR_META",
+          5: "CQ_ERR_CODE", 6: "CQ_ERR_DTYPE", 7: "CQ_ERR_HIP", 8: "CQ_ERR_UNSUPPORTED"}
+
+EXPORTS = ("cq_status_str", "cq_pack_groups", "cq_decode_ref", "cq_gemm_model_dtype", "cq_quantize_act_a8",
+           "cq_gemm_a8", "cq_set_gemv_max_rows", "cq_get_gemv_max_rows")
+
+
+class CQError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)}")
+
+
+class cq_weight(ctypes.Structure):
+    _fields_ = [("bits", ctypes.c_int32), ("group", ctypes.c_int32), ("n", ctypes.c_int64),
+                ("k", ctypes.c_int64), ("codes", ctypes.c_void_p), ("scale", ctypes.c_void_p),
+                ("a", ctypes.c_void_p), ("b", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libcq.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_06763_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    L.cq_status_str.restype = ctypes.c_char_p
+    L.cq_status_str.argtypes = [ctypes.c_int]
+    L.cq_pack_groups.restype = ctypes.c_int
+    L.cq_pack_groups.argtypes = [i32, i32, i64, i64, vp, vp, vp, vp, vp, vp]
+    L.cq_decode_ref.restype = ctypes.c_int
+    L.cq_decode_ref.argtypes = [ctypes.POINTER(cq_weight), vp, vp, vp]
+    L.cq_gemm_model_dtype.restype = ctypes.c_int
+    L.cq_gemm_model_dtype.argtypes = [ctypes.POINTER(cq_weight), vp, ctypes.c_int, i64, vp, ctypes.c_int, vp]
+    L.cq_quantize_act_a8.restype = ctypes.c_int
+    L.cq_quantize_act_a8.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp, vp]
+    L.cq_gemm_a8.restype = ctypes.c_int
+    L.cq_gemm_a8.argtypes = [ctypes.POINTER(cq_weight), vp, vp, i64, vp, ctypes.c_int, vp, vp]
+    L.cq_set_gemv_max_rows.restype = ctypes.c_int
+    L.cq_set_gemv_max_rows.argtypes = [i32, i64]
+    L.cq_get_gemv_max_rows.restype = i64
+    L.cq_get_gemv_max_rows.argtypes = [i32]
+    _lib = L
+    return L
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        raise CQError(status, where)
+
+
+def _np_ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+# ---------------------------------------------------------------- host packer
+
+
+def cq_pack_groups(codes, scale, a_bits, b_bits, bits: int, group: int) -> np.ndarray:
+    """Validate and pack host arrays; returns uint8 [N, K*B/8]."""
+    codes = np.ascontiguousarray(codes, dtype=np.int8)
+    n, k = codes.shape
+    scale = np.ascontiguousarray(scale, dtype=np.float32)
+    a_bits = np.ascontiguousarray(a_bits, dtype=np.uint16)
+    b_bits = np.ascontiguousarray(b_bits, dtype=np.uint16)
+    out = np.zeros((n, (k * bits + 7) // 8), np.uint8)
+    bad = ctypes.c_int64(-1)
+    st = lib().cq_pack_groups(bits, group, n, k, _np_ptr(codes), _np_ptr(scale), _np_ptr(a_bits),
+                              _np_ptr(b_bits), _np_ptr(out), ctypes.byref(bad))
+    if st != 0:
+        err = CQError(st, "cq_pack_groups")
+        err.bad_index = bad.value
+        raise err
+    return out
+
+
+# ---------------------------------------------------------------- device weights
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_ptr(stream=None):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class CQWeight:
+    """Device copy of one packed matrix plus its C descriptor."""
+
+    def __init__(self, packed, scale, a_bits, b_bits, bits: int, group: int, n: int, k: int,
+                 device="cuda"):
+        torch = _torch()
+
+        def dev(arr, dtype):
+            if isinstance(arr, torch.Tensor):
+                return arr.to(device=device).contiguous().view(dtype)
+            return torch.from_numpy(np.ascontiguousarray(arr)).to(device).view(dtype)
+
+        self.codes = dev(packed, torch.uint8)
+        self.scale = dev(scale, torch.float32)
+        self.a = dev(np.asarray(a_bits, np.uint16).view(np.int16) if not isinstance(a_bits, torch.Tensor)
+                     else a_bits, torch.int16)
+        self.b = dev(np.asarray(b_bits, np.uint16).view(np.int16) if not isinstance(b_bits, torch.Tensor)
+                     else b_bits, torch.int16)
+        self.bits, self.group, self.n, self.k = int(bits), int(group), int(n), int(k)
+        self.desc = cq_weight(self.bits, self.group, self.n, self.k, self.codes.data_ptr(),
+                              self.scale.data_ptr(), self.a.data_ptr(), self.b.data_ptr())
+
+    @classmethod
+    def from_codes(cls, codes, scale, a_bits, b_bits, bits: int, group: int, device="cuda"):
+        packed = cq_pack_groups(codes, scale, a_bits, b_bits, bits, group)
+        n, k = np.asarray(codes).shape
+        return cls(packed, scale, a_bits, b_bits, bits, group, n, k, device)
+
+    def clone(self) -> "CQWeight":
+        """Same bytes at new device addresses."""
+        return CQWeight(self.codes.clone(), self.scale.clone(), self.a.clone(), self.b.clone(),
+                        self.bits, self.group, self.n, self.k, self.codes.device)
+
+    @property
+    def nbytes(self) -> int:
+        return (self.codes.numel() + self.scale.numel() * 4 + self.a.numel() * 2 + self.b.numel() * 2)
+
+
+def _dt(t) -> int:
+    torch = _torch()
+    if t == torch.bfloat16:
+        return CQ_BF16
+    if t == torch.float16:
+        return CQ_FP16
+    if t == torch.float32:
+        return CQ_FP32
+    raise ValueError(f"unsupported dtype {t}")
+
+
+def cq_decode_ref(w: CQWeight, want_codes=True, want_values=True, stream=None):
+    torch = _torch()
+    codes = torch.empty((w.n, w.k), dtype=torch.int8, device=w.codes.device) if want_codes else None
+    vals = torch.empty((w.n, w.k), dtype=torch.float32, device=w.codes.device) if want_values else None
+    st = lib().cq_decode_ref(ctypes.byref(w.desc), codes.data_ptr() if codes is not None else None,
+                             vals.data_ptr() if vals is not None else None, _stream_ptr(stream))
+    _check(st, "cq_decode_ref")
+    return codes, vals
+
+
+def cq_gemm_model_dtype(w: CQWeight, x, y_dtype=None, out=None, stream=None):
+    """y = x W_hat^T; x is a [M, K] bf16/fp16 device tensor."""
+    torch = _torch()
+    assert x.dim() == 2 and x.shape[1] == w.k and x.is_contiguous()
+    y_dtype = y_dtype or x.dtype
+    if out is None:
+        out = torch.empty((x.shape[0], w.n), dtype=y_dtype, device=x.device)
+    st = lib().cq_gemm_model_dtype(ctypes.byref(w.desc), x.data_ptr(), _dt(x.dtype), x.shape[0],
+                                   out.data_ptr(), _dt(out.dtype), _stream_ptr(stream))
+    _check(st, "cq_gemm_model_dtype")
+    return out
+
+
+def cq_quantize_act_a8(x, x8=None, dx=None, stream=None):
+    torch = _torch()
+    assert x.dim() == 2 and x.is_contiguous()
+    m, k = x.shape
+    if x8 is None:
+        x8 = torch.empty((m, k), dtype=torch.int8, device=x.device)
+    if dx is None:
+        dx = torch.empty((m,), dtype=torch.float32, device=x.device)
+    st = lib().cq_quantize_act_a8(x.data_ptr(), _dt(x.dtype), m, k, x8.data_ptr(), dx.data_ptr(),
+                                  _stream_ptr(stream))
+    _check(st, "cq_quantize_act_a8")
+    return x8, dx
+
+
+def cq_gemm_a8(w: CQWeight, x8, dx, y_dtype=None, want_partials=False, out=None, stream=None):
+    torch = _torch()
+    assert x8.dim() == 2 and x8.shape[1] == w.k and x8.is_contiguous()
+    m = x8.shape[0]
+    y_dtype = y_dtype or torch.bfloat16
+    if out is None:
+        out = torch.empty((m, w.n), dtype=y_dtype, device=x8.device)
+    parts = torch.empty((m, w.n, w.k // w.group), dtype=torch.int32, device=x8.device) if want_partials else None
+    st = lib().cq_gemm_a8(ctypes.byref(w.desc), x8.data_ptr(), dx.data_ptr(), m, out.data_ptr(), _dt(out.dtype),
+                          parts.data_ptr() if parts is not None else None, _stream_ptr(stream))
+    _check(st, "cq_gemm_a8")
+    return (out, parts) if want_partials else out
+
+
+def cq_set_gemv_max_rows(path: int, max_rows: int):
+    _check(lib().cq_set_gemv_max_rows(path, max_rows), "cq_set_gemv_max_rows")
+
+
+def cq_get_gemv_max_rows(path: int) -> int:
+    return int(lib().cq_get_gemv_max_rows(path))

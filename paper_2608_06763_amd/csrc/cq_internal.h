@@ -1,0 +1,38 @@
+// Internal launcher declarations shared by the host API and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/cq.h"
+
+namespace cq {
+
+// Dtype codes used as template arguments: 0 = bf16, 1 = fp16, 2 = fp32.
+
+hipError_t launch_decode_ref(const cq_weight &w, int8_t *codes_out, float *w_out, hipStream_t stream);
+
+// Model-dtype narrow-row GEMV family (m <= 16).
+hipError_t launch_gemv_a16(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                           hipStream_t stream);
+
+// Model-dtype tiled matrix-core GEMM family.
+hipError_t launch_gemm_a16(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                           hipStream_t stream);
+
+// Dynamic-A8 activation quantizer.
+hipError_t launch_quant_a8(const void *x, int x_dt, int64_t m, int64_t k, int8_t *x8, float *dx,
+                           hipStream_t stream);
+
+// Dynamic-A8 narrow-row GEMV family (m <= 16).
+hipError_t launch_gemv_a8(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
+                          int32_t *partials, hipStream_t stream);
+
+// Dynamic-A8 tiled int8 matrix-core GEMM family.
+hipError_t launch_gemm_a8(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
+                          int32_t *partials, hipStream_t stream);
+
+// Largest row count each GEMV family accepts.
+constexpr int64_t kGemvMaxRows = 16;
+
+}  // namespace cq

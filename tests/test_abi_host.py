@@ -1,0 +1,174 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+The library must load and export every function ``include/cq.h`` declares;
+``cq_pack_groups`` must equal the oracle's packer byte for byte and reject
+every invalid input the format forbids; device entry points must reject bad
+arguments on the host before touching a device.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2608_06763_amd as cq
+from oracle import fit as FIT
+from oracle import format as F
+from workloads import small_weight
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "cq.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cq_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) >= 8
+    L = cq.lib()
+    for name in names:
+        assert hasattr(L, name), name
+    assert set(names) == set(cq.EXPORTS)
+
+
+def test_status_strings():
+    L = cq.lib()
+    for s in range(9):
+        assert L.cq_status_str(s).decode().startswith(cq.STATUS[s])
+
+
+@pytest.mark.parametrize("bits", range(1, 9))
+@pytest.mark.parametrize("group", [8, 16, 32, 64, 128, 256])
+def test_pack_matches_oracle(bits, group):
+    if (group * bits) % 8:
+        pytest.skip("G*B not byte aligned")
+    rng = np.random.default_rng(bits * 1000 + group)
+    n, k = 5, group * 3
+    codes = rng.choice(F.valid_codes(bits), size=(n, k)).astype(np.int8)
+    s = rng.uniform(0.1, 1.0, (n, k // group)).astype(np.float32)
+    a = np.full((n, k // group), F.f64_to_f16_bits(0.8), np.uint16)
+    b = np.full((n, k // group), F.f64_to_f16_bits(-0.2), np.uint16)
+    assert np.array_equal(cq.cq_pack_groups(codes, s, a, b, bits, group), F.pack(codes, bits))
+
+
+def test_pack_fitted_weights_matches_oracle():
+    w = small_weight(5, 16, 512, "laplace")
+    for bits in (2, 3, 4, 5, 8):
+        r = FIT.fit(w, bits, 128)
+        got = cq.cq_pack_groups(r.codes, r.scale, r.a_bits, r.b_bits, bits, 128)
+        assert np.array_equal(got, F.pack(r.codes, bits))
+
+
+def _meta(n, ng, a=1.0, b=0.0, s=1.0):
+    return (np.full((n, ng), s, np.float32), np.full((n, ng), F.f64_to_f16_bits(a), np.uint16),
+            np.full((n, ng), F.f64_to_f16_bits(b), np.uint16))
+
+
+def _pack_err(codes, s, a, b, bits, group):
+    with pytest.raises(cq.CQError) as ei:
+        cq.cq_pack_groups(codes, s, a, b, bits, group)
+    return ei.value
+
+
+def test_pack_rejects_out_of_range_codes():
+    codes = np.zeros((2, 64), np.int8)
+    codes[1, 5] = -8  # reserved pattern at W4
+    e = _pack_err(codes, *_meta(2, 2), 4, 32)
+    assert e.status == 5 and e.bad_index == 64 + 5
+    codes[1, 5] = 8
+    assert _pack_err(codes, *_meta(2, 2), 4, 32).status == 5
+    w1 = np.ones((1, 32), np.int8)
+    w1[0, 3] = 0  # W1 has no zero code
+    e = _pack_err(w1, *_meta(1, 1), 1, 32)
+    assert e.status == 5 and e.bad_index == 3
+
+
+def test_pack_rejects_bad_metadata():
+    codes = np.ones((1, 64), np.int8)
+    s, a, b = _meta(1, 2, a=2.0, b=0.0)  # q'(1) = -1: not monotone
+    e = _pack_err(codes, s, a, b, 4, 32)
+    assert e.status == 4 and e.bad_index == 0
+    s, a, b = _meta(1, 2, a=0.0, b=0.0)  # q = t^3: closure, not strict
+    assert _pack_err(codes, s, a, b, 3, 32).status == 4
+    s, a, b = _meta(1, 2)
+    s[0, 1] = np.nan
+    e = _pack_err(codes, s, a, b, 4, 32)
+    assert e.status == 4 and e.bad_index == 1
+    s, a, b = _meta(1, 2)
+    s[0, 0] = -1.0
+    assert _pack_err(codes, s, a, b, 4, 32).status == 4
+    s, a, b = _meta(1, 2)
+    s[0, 0] = 0.0  # zero scale with nonzero codes
+    assert _pack_err(codes, s, a, b, 4, 32).status == 4
+    s, a, b = _meta(1, 2)
+    a[0, 0] = 0x7C00  # +inf fp16
+    assert _pack_err(codes, s, a, b, 4, 32).status == 4
+    # non-monotone shapes are irrelevant at W2 (no interior level)
+    s, a, b = _meta(1, 2, a=2.0, b=0.0)
+    cq.cq_pack_groups(codes, s, a, b, 2, 32)
+
+
+def test_pack_zero_group_with_zero_scale_is_valid():
+    codes = np.zeros((1, 64), np.int8)
+    s, a, b = _meta(1, 2, s=0.0)
+    assert np.all(cq.cq_pack_groups(codes, s, a, b, 4, 32) == 0)
+
+
+def test_pack_rejects_bad_shapes():
+    codes = np.zeros((1, 60), np.int8)
+    assert _pack_err(codes, *_meta(1, 2), 4, 32).status == 2     # K % G
+    codes = np.zeros((1, 12), np.int8)
+    assert _pack_err(codes, *_meta(1, 3), 3, 4).status == 2      # G*B % 8
+    L = cq.lib()
+    z = np.zeros(4, np.uint8)
+    p = z.ctypes.data_as(ctypes.c_void_p)
+    assert L.cq_pack_groups(9, 32, 1, 32, p, p, p, p, p, None) == 1
+    assert L.cq_pack_groups(4, 32, 1, 32, None, p, p, p, p, None) == 1
+
+
+def _desc(bits=4, group=128, n=64, k=256, ptr=4096):
+    return cq.cq_weight(bits, group, n, k, ptr, ptr, ptr, ptr)
+
+
+def test_device_calls_validate_on_host():
+    # every case below must be rejected before any device work is issued
+    L = cq.lib()
+    P = ctypes.c_void_p
+    ok = 4096
+    bad_align = 4100
+    w = _desc()
+    cases = [
+        (_desc(bits=0), 1), (_desc(bits=9), 1), (_desc(group=48), 1), (_desc(group=1024), 1),
+        (_desc(group=16), 1), (_desc(k=320), 2), (_desc(bits=3, group=32, k=96), 2),
+        (_desc(n=0), 1), (_desc(ptr=bad_align), 3),
+    ]
+    for d, want in cases:
+        assert L.cq_gemm_model_dtype(ctypes.byref(d), P(ok), 0, 1, P(ok), 0, None) == want
+        assert L.cq_gemm_a8(ctypes.byref(d), P(ok), P(ok), 1, P(ok), 0, None, None) == want
+        assert L.cq_decode_ref(ctypes.byref(d), P(ok), None, None) == want
+    assert L.cq_gemm_model_dtype(None, P(ok), 0, 1, P(ok), 0, None) == 1
+    assert L.cq_gemm_model_dtype(ctypes.byref(w), P(ok), 0, 0, P(ok), 0, None) == 1        # m = 0
+    assert L.cq_gemm_model_dtype(ctypes.byref(w), P(ok), 2, 1, P(ok), 2, None) == 6        # fp32 x
+    assert L.cq_gemm_model_dtype(ctypes.byref(w), P(ok), 0, 1, P(ok), 1, None) == 6        # bf16 -> fp16
+    assert L.cq_gemm_model_dtype(ctypes.byref(w), P(bad_align), 0, 1, P(ok), 0, None) == 3
+    assert L.cq_gemm_a8(ctypes.byref(w), P(ok), P(ok), 1, P(ok), 7, None, None) == 6
+    assert L.cq_gemm_a8(ctypes.byref(w), P(ok), P(ok), 1, P(ok), 0, P(bad_align), None) == 3
+    assert L.cq_decode_ref(ctypes.byref(w), None, None, None) == 1
+    assert L.cq_quantize_act_a8(P(ok), 0, 1, 48, P(ok), P(ok), None) == 2                 # k % 32
+    assert L.cq_quantize_act_a8(P(ok), 2, 1, 64, P(ok), P(ok), None) == 6
+    assert L.cq_quantize_act_a8(P(ok), 0, 0, 64, P(ok), P(ok), None) == 1
+    assert L.cq_quantize_act_a8(P(ok), 0, 1, 64, P(bad_align), P(ok), None) == 3
+
+
+def test_gemv_threshold_override():
+    assert cq.cq_get_gemv_max_rows(0) >= 1
+    cq.cq_set_gemv_max_rows(0, 0)
+    assert cq.cq_get_gemv_max_rows(0) == 0
+    cq.cq_set_gemv_max_rows(0, -1)
+    assert cq.cq_get_gemv_max_rows(0) >= 1
+    with pytest.raises(cq.CQError):
+        cq.cq_set_gemv_max_rows(2, 1)

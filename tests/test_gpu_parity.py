@@ -1,0 +1,298 @@
+"""GPU parity: every entry point of the C ABI against the CPU oracle.
+
+Integer stages (unpacked codes, INT8 activation carriers, their scales, INT32
+group partials) must match bit for bit.  Floating-point outputs must satisfy
+eps_comp <= 2e-3 (bf16/fp16 outputs; the final output rounding is excused
+once, see oracle/ref.py) and tighter bounds for FP32 outputs of paths that
+multiply in FP32.
+"""
+import numpy as np
+import pytest
+
+from oracle import a8 as A8
+from oracle import format as F
+from oracle import ref as R
+from tests._cases import act, fitted, ref_a8, ref_model_dtype, say
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-3
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    import paper_2608_06763_amd as cq
+    cq.lib()
+    return torch
+
+
+def _cq():
+    import paper_2608_06763_amd as cq
+    return cq
+
+
+def _weight(r, bits, group):
+    return _cq().CQWeight.from_codes(r.codes, r.scale, r.a_bits, r.b_bits, bits, group)
+
+
+def _x(torch, bits_np, dtype):
+    t = torch.from_numpy(bits_np.view(np.int16)).cuda()
+    return t.view(torch.bfloat16 if dtype == "bf16" else torch.float16)
+
+
+def _np(t):
+    import torch
+    if t.dtype in (torch.bfloat16, torch.float16):
+        return t.float().cpu().numpy().astype(np.float64)
+    return t.cpu().numpy()
+
+
+WIDTHS = list(range(1, 9))
+GROUPS = [32, 64, 128, 256]
+
+
+# ---------------------------------------------------------------- decode
+
+
+@pytest.mark.parametrize("bits", WIDTHS)
+@pytest.mark.parametrize("group", GROUPS)
+def test_decode_ref(torch_dev, bits, group):
+    r = fitted(1, 40, 512, bits, group)
+    say("decode_ref", bits, group)
+    w = _weight(r, bits, group)
+    codes, vals = _cq().cq_decode_ref(w)
+    torch_dev.cuda.synchronize()
+    assert np.array_equal(codes.cpu().numpy(), r.codes)
+    want = F.decode(r.codes, bits, group, r.scale, r.a_bits, r.b_bits)
+    got = vals.cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(got - want) <= 2e-6 * np.abs(want) + 1e-30)
+
+
+@pytest.mark.parametrize("bits,raw", [(4, 0x88), (3, None), (2, 0xAA), (8, 0x80)])
+def test_decode_reserved_pattern(torch_dev, bits, raw):
+    # a stream made only of the reserved pattern (bypassing the packer)
+    k = 128
+    n = 2
+    if bits == 3:
+        row = bytes([0x24, 0x49, 0x92]) * (k * 3 // 24)
+    else:
+        row = bytes([raw]) * (k * bits // 8)
+    packed = np.frombuffer(row * n, np.uint8).reshape(n, -1).copy()
+    s = np.ones((n, 1), np.float32)
+    a = np.full((n, 1), F.f64_to_f16_bits(0.7), np.uint16)
+    b = np.full((n, 1), F.f64_to_f16_bits(-0.1), np.uint16)
+    assert np.all(F.unpack(packed, bits, k) == 0)
+    say("decode_reserved", bits)
+    w = _cq().CQWeight(packed, s, a, b, bits, 128, n, k)
+    codes, vals = _cq().cq_decode_ref(w)
+    assert np.all(codes.cpu().numpy() == 0) and np.all(vals.cpu().numpy() == 0)
+    x = torch_dev.ones((1, k), dtype=torch_dev.bfloat16, device="cuda")
+    y = _cq().cq_gemm_model_dtype(w, x, y_dtype=torch_dev.float32)
+    assert np.all(y.cpu().numpy() == 0)
+
+
+# ---------------------------------------------------------------- model dtype
+
+
+@pytest.mark.parametrize("bits", WIDTHS)
+@pytest.mark.parametrize("group", GROUPS)
+@pytest.mark.parametrize("m", [1, 5, 16])
+def test_gemv_model_dtype(torch_dev, bits, group, m):
+    r = fitted(2, 72, 768, bits, group)
+    xb, xv = act(3 + m, m, 768)
+    y_ref = ref_model_dtype(xv, r, bits, group)
+    say("gemv_a16", bits, group, m)
+    w = _weight(r, bits, group)
+    x = _x(torch_dev, xb, "bf16")
+    y16 = _cq().cq_gemm_model_dtype(w, x)
+    y32 = _cq().cq_gemm_model_dtype(w, x, y_dtype=torch_dev.float32)
+    assert R.eps_comp(_np(y16), y_ref, "bf16") <= TOL
+    # FP32 output of the FP32-multiply GEMV: rounding-order differences only
+    assert R.eps_comp(_np(y32), y_ref, "fp32") <= 1e-5
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4, 8])
+@pytest.mark.parametrize("m", [1, 16])
+def test_gemv_model_dtype_fp16(torch_dev, bits, m):
+    r = fitted(4, 40, 512, bits, 128)
+    xb, xv = act(5, m, 512, "fp16")
+    y_ref = ref_model_dtype(xv, r, bits, 128)
+    say("gemv_a16_fp16", bits, m)
+    w = _weight(r, bits, 128)
+    y = _cq().cq_gemm_model_dtype(w, _x(torch_dev, xb, "fp16"))
+    assert y.dtype == torch_dev.float16
+    assert R.eps_comp(_np(y), y_ref, "fp16") <= TOL
+
+
+@pytest.mark.parametrize("bits", WIDTHS)
+@pytest.mark.parametrize("group", [32, 128])
+@pytest.mark.parametrize("m", [1, 37, 130])
+def test_gemm_model_dtype_tiled(torch_dev, bits, group, m):
+    cq = _cq()
+    r = fitted(6, 136, 768, bits, group)
+    xb, xv = act(7 + m, m, 768)
+    y_ref = ref_model_dtype(xv, r, bits, group)
+    say("gemm_a16", bits, group, m)
+    w = _weight(r, bits, group)
+    x = _x(torch_dev, xb, "bf16")
+    cq.cq_set_gemv_max_rows(0, 0)
+    try:
+        y = cq.cq_gemm_model_dtype(w, x)
+        y32 = cq.cq_gemm_model_dtype(w, x, y_dtype=torch_dev.float32)
+    finally:
+        cq.cq_set_gemv_max_rows(0, -1)
+    assert R.eps_comp(_np(y), y_ref, "bf16") <= TOL
+    # bf16 output is the RNE of the fp32 output of the same kernel
+    assert np.array_equal(_np(y), _np(y32.to(torch_dev.bfloat16)))
+
+
+@pytest.mark.parametrize("m", [1, 64])
+def test_gemm_model_dtype_fp16_tiled(torch_dev, m):
+    cq = _cq()
+    r = fitted(8, 72, 512, 4, 128)
+    xb, xv = act(9, m, 512, "fp16")
+    y_ref = ref_model_dtype(xv, r, 4, 128)
+    say("gemm_a16_fp16", m)
+    w = _weight(r, 4, 128)
+    cq.cq_set_gemv_max_rows(0, 0)
+    try:
+        y = cq.cq_gemm_model_dtype(w, _x(torch_dev, xb, "fp16"))
+    finally:
+        cq.cq_set_gemv_max_rows(0, -1)
+    assert R.eps_comp(_np(y), y_ref, "fp16") <= TOL
+
+
+def test_model_dtype_deterministic(torch_dev):
+    r = fitted(10, 64, 1024, 4, 128)
+    xb, _ = act(11, 3, 1024)
+    say("determinism_a16")
+    w = _weight(r, 4, 128)
+    x = _x(torch_dev, xb, "bf16")
+    y1 = _cq().cq_gemm_model_dtype(w, x, y_dtype=torch_dev.float32)
+    y2 = _cq().cq_gemm_model_dtype(w, x, y_dtype=torch_dev.float32)
+    assert torch_dev.equal(y1, y2)
+
+
+# ---------------------------------------------------------------- Dynamic A8
+
+
+@pytest.mark.parametrize("m,k", [(1, 32), (7, 4096), (64, 768)])
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+def test_quantize_act_a8_bitexact(torch_dev, m, k, dtype):
+    xb, xv = act(12 + m, m, k, dtype)
+    if m >= 7:
+        xv = xv.copy()
+        xb = xb.copy()
+        xb[1] = 0            # an all-zero row
+        xv[1] = 0
+    x8_ref, d_ref = A8.quantize_act(xv)
+    say("quant_a8", m, k, dtype)
+    x8, dx = _cq().cq_quantize_act_a8(_x(torch_dev, xb, dtype))
+    assert np.array_equal(x8.cpu().numpy(), x8_ref)
+    assert np.array_equal(dx.cpu().numpy().view(np.uint32), d_ref.view(np.uint32))
+
+
+def test_quantize_act_a8_halfway_cases(torch_dev):
+    vals = np.array([[127.0, 2.5, -2.5, 0.5, -0.5, 1.5, 126.5, -127.0] * 4])
+    from workloads import to_bf16_bits
+    xb = to_bf16_bits(vals)
+    x8_ref, _ = A8.quantize_act(vals)
+    say("quant_a8_halfway")
+    x8, dx = _cq().cq_quantize_act_a8(_x(torch_dev, xb, "bf16"))
+    assert dx.item() == 1.0
+    assert np.array_equal(x8.cpu().numpy(), x8_ref)
+
+
+@pytest.mark.parametrize("bits", WIDTHS)
+@pytest.mark.parametrize("group", GROUPS)
+@pytest.mark.parametrize("m,family", [(1, "gemv"), (16, "gemv"), (3, "gemm"), (70, "gemm")])
+def test_gemm_a8_partials_bitexact(torch_dev, bits, group, m, family):
+    cq = _cq()
+    r = fitted(13, 72, 768, bits, group)
+    xb, xv = act(14 + m, m, 768)
+    x8_ref, d_ref, y_ref, p_ref = ref_a8(xv, r, bits, group)
+    say("gemm_a8", bits, group, m, family)
+    w = _weight(r, bits, group)
+    x8 = torch_dev.from_numpy(x8_ref).cuda()
+    dx = torch_dev.from_numpy(d_ref).cuda()
+    if family == "gemm":
+        cq.cq_set_gemv_max_rows(1, 0)
+    try:
+        y, parts = cq.cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32, want_partials=True)
+        y16 = cq.cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.bfloat16)
+    finally:
+        cq.cq_set_gemv_max_rows(1, -1)
+    assert np.array_equal(parts.cpu().numpy(), p_ref)
+    assert R.eps_comp(_np(y), y_ref, "fp32") <= 1e-5
+    assert R.eps_comp(_np(y16), y_ref, "bf16") <= TOL
+
+
+def test_a8_carrier_tie_rounds_to_even(torch_dev):
+    # W8, a = 2^-7, b = 127/128, code 64: 127 q = 32.5 exactly -> carrier 32
+    n, k, g = 16, 128, 128
+    codes = np.zeros((n, k), np.int8)
+    codes[:, 0] = 64
+    codes[:, 1] = -64
+    s = np.ones((n, 1), np.float32)
+    a = np.full((n, 1), F.f64_to_f16_bits(2.0 ** -7), np.uint16)
+    b = np.full((n, 1), F.f64_to_f16_bits(127 / 128), np.uint16)
+    x8 = np.zeros((1, k), np.int8)
+    x8[0, 0] = 1
+    x8[0, 1] = 3
+    dx = np.ones(1, np.float32)
+    cq = _cq()
+    say("a8_tie")
+    w = cq.CQWeight.from_codes(codes, s, a, b, 8, g)
+    for thr in (-1, 0):
+        cq.cq_set_gemv_max_rows(1, thr)
+        try:
+            _, parts = cq.cq_gemm_a8(w, torch_dev.from_numpy(x8).cuda(), torch_dev.from_numpy(dx).cuda(),
+                                     y_dtype=torch_dev.float32, want_partials=True)
+        finally:
+            cq.cq_set_gemv_max_rows(1, -1)
+        assert np.all(parts.cpu().numpy() == 32 * 1 - 32 * 3)
+
+
+def test_a8_operator_end_to_end(torch_dev):
+    # quantizer + GEMM through the device, against the oracle's A8 semantics
+    r = fitted(15, 96, 1024, 4, 128)
+    xb, xv = act(16, 9, 1024)
+    _, _, y_ref, _ = ref_a8(xv, r, 4, 128)
+    say("a8_operator")
+    w = _weight(r, 4, 128)
+    x8, dx = _cq().cq_quantize_act_a8(_x(torch_dev, xb, "bf16"))
+    y = _cq().cq_gemm_a8(w, x8, dx)
+    assert R.eps_comp(_np(y), y_ref, "bf16") <= TOL
+
+
+def test_a8_deterministic(torch_dev):
+    r = fitted(17, 64, 1024, 5, 64)
+    xb, _ = act(18, 33, 1024)
+    say("determinism_a8")
+    w = _weight(r, 5, 64)
+    x8, dx = _cq().cq_quantize_act_a8(_x(torch_dev, xb, "bf16"))
+    y1 = _cq().cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32)
+    y2 = _cq().cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32)
+    assert torch_dev.equal(y1, y2)
+
+
+# ---------------------------------------------------------------- edge shapes
+
+
+@pytest.mark.parametrize("n,k,g,m", [(1, 128, 128, 1), (1, 128, 128, 16), (3, 512, 512, 2), (257, 256, 32, 17)])
+def test_edge_shapes(torch_dev, n, k, g, m):
+    r = fitted(19, n, k, 4, g)
+    xb, xv = act(20, m, k)
+    y_ref = ref_model_dtype(xv, r, 4, g)
+    _, _, ya_ref, p_ref = ref_a8(xv, r, 4, g)
+    say("edge", n, k, g, m)
+    w = _weight(r, 4, g)
+    x = _x(torch_dev, xb, "bf16")
+    y = _cq().cq_gemm_model_dtype(w, x)
+    assert R.eps_comp(_np(y), y_ref, "bf16") <= TOL
+    x8, dx = _cq().cq_quantize_act_a8(x)
+    ya, parts = _cq().cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32, want_partials=True)
+    assert np.array_equal(parts.cpu().numpy(), p_ref)
+    assert R.eps_comp(_np(ya), ya_ref, "fp32") <= 1e-5
