@@ -2,9 +2,15 @@
 //
 // A workgroup owns a BM x BN tile of y.  For every K step it decodes the packed
 // weight tile once: s_g q(t_k) is formed in FP32 from the FP32 scale and the
-// FP16 shapes, rounded to the activation dtype (the dense-path rounding point
-// of Sec. 5.3) and staged in LDS next to the activation tile; the MFMA
+// FP16 shapes and converted to the activation dtype (the dense-path rounding
+// point of Sec. 5.3), then staged in LDS next to the activation tile; the MFMA
 // accumulates in FP32.  Decoded weights never leave the workgroup.
+//
+// With BF16 activations a single BF16 operand (8 significant bits) costs up to
+// about 2e-3 of max|y| in the worst output, so the FP32 value is carried as an
+// unevaluated sum hi + lo of two BF16 numbers (hi = bf16(v), lo = bf16(v - hi),
+// 16 significant bits) and both halves go through the MFMA into the same FP32
+// accumulator.  FP16 activations use one FP16 operand (11 significant bits).
 //
 // MFMA operand layout (v_mfma_f32_16x16x32_{bf16,f16}): lane l supplies row
 // (l % 16) of A and column (l % 16) of B, each with the 8 consecutive K slots
@@ -49,6 +55,8 @@ __global__ void __launch_bounds__(256) gemm_a16_tiled(
     constexpr int M = max_code(B);
     __shared__ __attribute__((aligned(16))) uint16_t As[BM * LDS_STRIDE];
     __shared__ __attribute__((aligned(16))) uint16_t Bs[BN * LDS_STRIDE];
+    constexpr bool kSplit = (XDT == 0);
+    __shared__ __attribute__((aligned(16))) uint16_t Bl[kSplit ? BN * LDS_STRIDE : 8];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -77,6 +85,7 @@ __global__ void __launch_bounds__(256) gemm_a16_tiled(
         }
         {
             uint32_t packed[4] = {0, 0, 0, 0};
+            uint32_t packed_lo[4] = {0, 0, 0, 0};
             const int64_t row = n0 + br;
             if (row < n) {
                 const uint32_t *wp = reinterpret_cast<const uint32_t *>(codes) + row * row_words + (k0 >> 5) * B;
@@ -95,10 +104,16 @@ __global__ void __launch_bounds__(256) gemm_a16_tiled(
                 for (int e = 0; e < 8; ++e) {
                     const int code = unit_code<B>(w, bc + e);
                     const float lv = (B == 1) ? float(code) : signed_level(code, M, a, b, c);
-                    packed[e >> 1] |= uint32_t(to_act<XDT>(s * lv)) << (16 * (e & 1));
+                    const float v = s * lv;
+                    const uint16_t hi = to_act<XDT>(v);
+                    packed[e >> 1] |= uint32_t(hi) << (16 * (e & 1));
+                    if constexpr (kSplit) packed_lo[e >> 1] |= uint32_t(f32_to_bf16(v - bf16_to_f32(hi))) << (16 * (e & 1));
                 }
             }
             *reinterpret_cast<uint4 *>(&Bs[br * LDS_STRIDE + bc]) = make_uint4(packed[0], packed[1], packed[2], packed[3]);
+            if constexpr (kSplit)
+                *reinterpret_cast<uint4 *>(&Bl[br * LDS_STRIDE + bc]) =
+                    make_uint4(packed_lo[0], packed_lo[1], packed_lo[2], packed_lo[3]);
         }
         __syncthreads();
         uint4 af[2], bfr[2];
@@ -112,6 +127,15 @@ __global__ void __launch_bounds__(256) gemm_a16_tiled(
         for (int i = 0; i < 2; ++i)
 #pragma unroll
             for (int j = 0; j < 2; ++j) acc[i][j] = mfma16<XDT>(af[i], bfr[j], acc[i][j]);
+        if constexpr (kSplit) {
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                bfr[j] = *reinterpret_cast<const uint4 *>(&Bl[(wn + j * 16 + (lane & 15)) * LDS_STRIDE + 8 * (lane >> 4)]);
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) acc[i][j] = mfma16<XDT>(af[i], bfr[j], acc[i][j]);
+        }
         __syncthreads();
     }
 #pragma unroll
