@@ -153,3 +153,32 @@ def small_act(seed: int, m: int, k: int, outliers: bool = True) -> np.ndarray:
         mask = rng(seed + 2).random((m, k)) < 0.005
         x[mask] *= 20.0
     return to_bf16_bits(x)
+
+
+# ---------------------------------------------------------------- packed-representation stand-in
+#
+# Shape pairs printed in the paper's population tables (Gaussian / Laplace
+# optima, Sec. 3.3), used as fixed, known-monotone curve shapes.
+PRINTED_SHAPES = ((1.0, 0.0), (0.7932, -0.3847), (0.5203, -0.2936), (0.8517, -0.1852),
+                  (0.6216, -0.1495), (0.7510, -0.5253), (0.4603, -0.3881))
+
+
+def synthetic_representation(seed: int, n: int, k: int, bits: int, group: int, scale_center: float = 0.05):
+    """Random stand-in for a quantized matrix: codes drawn from a rounded
+    Laplace law clipped to [-M, M], lognormal FP32 scales and shapes taken from
+    PRINTED_SHAPES.  Kernel timing does not depend on the values, only on the
+    layout, so this serves timing runs that must not call the oracle."""
+    g = rng(seed)
+    m = 1 if bits == 1 else (1 << (bits - 1)) - 1
+    if bits == 1:
+        codes = np.where(g.random((n, k)) < 0.5, -1, 1).astype(np.int8)
+    else:
+        raw = np.rint(g.laplace(0.0, max(m / 3.0, 0.5), (n, k)))
+        codes = np.clip(raw, -m, m).astype(np.int8)
+    ng = k // group
+    scale = (scale_center * np.exp(0.3 * g.standard_normal((n, ng)))).astype(np.float32)
+    pick = g.integers(0, len(PRINTED_SHAPES), (n, ng))
+    shapes = np.array(PRINTED_SHAPES)
+    a_bits = to_f16_bits(shapes[pick, 0])
+    b_bits = to_f16_bits(shapes[pick, 1])
+    return codes, scale, a_bits, b_bits
