@@ -130,4 +130,17 @@ __device__ __forceinline__ int exact_carrier(int i, int m, double a, double b) {
     return int(r);
 }
 
+// Compute units of the current device (cached per device id).
+inline int device_cu_count() {
+    static int cus[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cus[dev] == 0) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+        cus[dev] = v;
+    }
+    return cus[dev];
+}
+
 }  // namespace cq

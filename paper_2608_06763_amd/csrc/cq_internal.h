@@ -16,6 +16,19 @@ hipError_t launch_decode_ref(const cq_weight &w, int8_t *codes_out, float *w_out
 hipError_t launch_gemv_a16(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                            hipStream_t stream);
 
+// Conservative model-dtype GEMV (every B and G, m <= 16).
+hipError_t launch_gemv_a16_generic(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                                   hipStream_t stream);
+
+// Model-dtype single-row streaming GEMV (m == 1, every B, G <= 512).
+hipError_t launch_gemv_a16_stream(const cq_weight &w, const void *x, int x_dt, void *y, int y_dt,
+                                  hipStream_t stream);
+
+// Model-dtype table-decode GEMV (m <= 4); see gemv_a16_lut.hip.
+bool gemv_a16_lut_supported(const cq_weight &w, int64_t m);
+hipError_t launch_gemv_a16_lut(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                               hipStream_t stream);
+
 // Model-dtype tiled matrix-core GEMM family.
 hipError_t launch_gemm_a16(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                            hipStream_t stream);

@@ -113,6 +113,16 @@ static hipError_t dispatch_bits(const cq_weight &w, const void *x, int64_t m, vo
 
 hipError_t launch_gemv_a16(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                            hipStream_t stream) {
+    if (m == 1) return launch_gemv_a16_stream(w, x, x_dt, y, y_dt, stream);
+    if (gemv_a16_lut_supported(w, m)) {
+        const hipError_t e = launch_gemv_a16_lut(w, x, x_dt, m, y, y_dt, stream);
+        if (e != hipErrorNotSupported) return e;
+    }
+    return launch_gemv_a16_generic(w, x, x_dt, m, y, y_dt, stream);
+}
+
+hipError_t launch_gemv_a16_generic(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                                   hipStream_t stream) {
     if (x_dt == 0) {
         if (y_dt == 0) return dispatch_bits<0, 0>(w, x, m, y, stream);
         return dispatch_bits<0, 2>(w, x, m, y, stream);

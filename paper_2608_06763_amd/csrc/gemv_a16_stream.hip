@@ -1,0 +1,343 @@
+// Model-dtype single-row GEMV, streaming table-decode family (Sec. 5.2
+// strategy 2 and Sec. 5.3 narrow-row tactic) for m == 1.
+//
+// Numerics follow the paper's narrow-row GEMV: the activation and the
+// normalised level are multiplied in FP32; the FP32 group scale multiplies
+// each 32-code sub-reduction of the group (a regrouping of the group
+// reduction, identical up to rounding order).
+//
+// Work mapping (coalescing first).  K is cut into column blocks of 64 units of
+// 32 codes (2048 codes; a unit is exactly B 32-bit words of the row).  Lane l
+// of a wave always owns unit l of its column block, so one wavefront load of a
+// row reads 64 * 4B contiguous bytes.  A workgroup owns RW rows; its waves take
+// different column blocks of those rows and are reduced through LDS at the
+// end.  A wave requests the codes and metadata of all RW rows of a column
+// block before it decodes any of them, and the activations of its column block
+// stay in registers (FP32) for all RW rows.
+//
+// Decode.  The UPG = G/32 lanes that share a group share its level table:
+// every lane writes some of the 2^B signed normalised levels (0 for the
+// reserved pattern) into the table columns of all lanes of its group with
+// 128-bit LDS stores, then reads one entry per weight from its own column at
+// byte (field << 8) + lane * 4 + wave base, which is free of bank conflicts.
+// For W4 the address is assembled by one byte permute per weight.  B >= 6
+// evaluates the cubic in registers instead of keeping a 64..256-entry table.
+#include "cq_device.h"
+#include "cq_internal.h"
+
+namespace cq {
+
+namespace {
+
+typedef __attribute__((address_space(3))) float lds_f;
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) f32x4_t lds_f4;
+
+__device__ __forceinline__ float lds_ld(uint32_t a) { return *reinterpret_cast<const lds_f *>(uintptr_t(a)); }
+__device__ __forceinline__ void lds_st4(uint32_t a, float v) {
+    *reinterpret_cast<lds_f4 *>(uintptr_t(a)) = f32x4_t{v, v, v, v};
+}
+__device__ __forceinline__ void lds_st(uint32_t a, float v) { *reinterpret_cast<lds_f *>(uintptr_t(a)) = v; }
+
+__device__ __forceinline__ void wave_lds_fence() {
+    // LDS instructions of one wavefront execute in issue order, so ordering the
+    // compiler's memory operations is enough for cross-lane LDS visibility within
+    // a wavefront; no hardware wait (which would also drain pending HBM loads).
+    __asm__ __volatile__("" ::: "memory");
+    __builtin_amdgcn_wave_barrier();
+}
+
+}  // namespace
+
+template <int B, int UPG, int RW, int XDT, int YDT>
+__global__ void __launch_bounds__(512) gemv_a16_stream(
+    const uint8_t *__restrict__ codes, const float *__restrict__ scale,
+    const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
+    int64_t n, int64_t k, const uint16_t *__restrict__ x, void *__restrict__ y) {
+    constexpr int G = UPG * 32;
+    constexpr int M = max_code(B);
+    constexpr bool LUT = (B <= 5);
+    constexpr int NT = LUT ? (1 << B) : 1;
+    // LDS (dynamic, starting at address 0): one NT x 256-byte table per wave,
+    // then the cross-wave partial sums.  The W4 address build relies on bits
+    // 8..15 of the table base being zero.
+    extern __shared__ __attribute__((aligned(16))) float tab[];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int nwaves = blockDim.x >> 6;
+    float *red = tab + nwaves * NT * 64;
+    const int64_t ntiles = (n + RW - 1) / RW;
+    const int64_t units = k >> 5;
+    const int64_t ncb = (units + 63) >> 6;
+    const int64_t ng = k / G;
+    const int64_t row_words = (k * B) >> 5;
+    const uint32_t tbase = uint32_t(uintptr_t((lds_f *)tab));
+    const uint32_t col = tbase + uint32_t(wave) * (NT * 256u) + uint32_t(lane) * 4u;
+    // first column of this lane's group inside the wave (the group's UPG lanes are adjacent)
+    const uint32_t gcol = tbase + uint32_t(wave) * (NT * 256u) + uint32_t(lane - lane % UPG) * 4u;
+    const uint32_t wtag = uint32_t(wave) * 0x10101010u;
+
+    // magnitudes this lane evaluates for its group's table, and their t = i/M
+    constexpr int MPL = (B == 1) ? 1 : (M + 1 + UPG - 1) / UPG;
+    int mag[MPL];
+    float tq[MPL];
+#pragma unroll
+    for (int t = 0; t < MPL; ++t) {
+        mag[t] = (B == 1) ? (lane % UPG == 0 ? 1 : M + 1) : lane % UPG + UPG * t;
+        tq[t] = float(mag[t]) * (1.0f / float(M));
+    }
+
+    // Persistent grid: a workgroup walks row tiles blockIdx.x, + gridDim.x, ...
+    // and every wave walks its column blocks of each tile.  The codes and
+    // metadata of the next (tile, column block) item are requested before the
+    // current item is decoded, so HBM reads always overlap decoding.
+    const int64_t my_tiles = blockIdx.x < ntiles ? (ntiles - 1 - blockIdx.x) / gridDim.x + 1 : 0;
+    const int64_t cbw = (ncb - wave + nwaves - 1) / nwaves;  // column blocks of this wave per tile
+    const int64_t items = my_tiles * cbw;
+
+    uint32_t wn[RW][B];
+    float sn[RW];
+    uint32_t an[RW], bn[RW];
+    auto fetch = [&](int64_t it) {
+        const int64_t tile = blockIdx.x + (it / cbw) * gridDim.x;
+        const int64_t cb = wave + (it % cbw) * nwaves;
+        const int64_t u_raw = cb * 64 + lane;
+        const int64_t u = u_raw < units ? u_raw : units - 1;  // clamped: loads stay valid
+        const int64_t g = u / UPG;
+#pragma unroll
+        for (int r = 0; r < RW; ++r) {
+            const int64_t row_raw = tile * RW + r;
+            const int64_t row = row_raw < n ? row_raw : n - 1;
+            const uint32_t *wp = reinterpret_cast<const uint32_t *>(codes) + row * row_words + u * B;
+#pragma unroll
+            for (int i = 0; i < B; ++i) wn[r][i] = __builtin_nontemporal_load(wp + i);
+            const int64_t gi = row * ng + g;
+            sn[r] = scale[gi];
+            an[r] = a16[gi];
+            bn[r] = b16[gi];
+        }
+    };
+
+    float acc[RW];
+#pragma unroll
+    for (int i = 0; i < RW; ++i) acc[i] = 0.f;
+    if (items > 0) fetch(0);
+    for (int64_t it = 0; it < items; ++it) {
+        const int64_t tile = blockIdx.x + (it / cbw) * gridDim.x;
+        const int64_t ci = it % cbw;
+        const int64_t cb = wave + ci * nwaves;
+        const int64_t row0 = tile * RW;
+        uint32_t w[RW][B];
+        float s[RW];
+        uint32_t av[RW], bv[RW];
+#pragma unroll
+        for (int r = 0; r < RW; ++r) {
+#pragma unroll
+            for (int i = 0; i < B; ++i) w[r][i] = wn[r][i];
+            s[r] = sn[r];
+            av[r] = an[r];
+            bv[r] = bn[r];
+        }
+        if (it + 1 < items) fetch(it + 1);
+        const int64_t u_raw = cb * 64 + lane;
+        const bool live = u_raw < units;
+        const int64_t u = live ? u_raw : units - 1;
+        bool rok[RW];
+#pragma unroll
+        for (int r = 0; r < RW; ++r) rok[r] = live && (row0 + r < n);
+        // ---- activations of this unit, FP32 in registers
+        float xf[32];
+        {
+            const uint4 *xp = reinterpret_cast<const uint4 *>(x + u * 32);
+            uint4 xv[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) xv[q] = xp[q];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t vw[4] = {xv[q].x, xv[q].y, xv[q].z, xv[q].w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    xf[q * 8 + 2 * e] = act_to_f32<XDT>(uint16_t(vw[e] & 0xffffu));
+                    xf[q * 8 + 2 * e + 1] = act_to_f32<XDT>(uint16_t(vw[e] >> 16));
+                }
+            }
+        }
+        // ---- decode row by row
+#pragma unroll
+        for (int r = 0; r < RW; ++r) {
+            float a = 1.f, b = 0.f;
+            if constexpr (B >= 3) {
+                a = f16_to_f32(uint16_t(av[r]));
+                b = f16_to_f32(uint16_t(bv[r]));
+            }
+            const float cc = 1.f - a - b;
+            if constexpr (LUT) {
+                // Lane j of a group evaluates magnitudes j, j + UPG, ... (their t = i/M
+                // are per-lane constants) and stores +q at field i and -q at field
+                // NT - i into the table columns of all UPG lanes of the group; the lane
+                // holding magnitude 0 also clears the reserved field NT/2.
+                wave_lds_fence();  // the previous row's reads are issued
+#pragma unroll
+                for (int t = 0; t < MPL; ++t) {
+                    if (mag[t] <= M) {
+                        float q;
+                        if constexpr (B == 1) {
+                            q = 1.f;
+                        } else {
+                            q = tq[t] * __builtin_fmaf(tq[t], __builtin_fmaf(tq[t], cc, b), a);
+                            q = mag[t] == M ? 1.f : q;
+                        }
+                        const uint32_t up = gcol + uint32_t(B == 1 ? 1 : mag[t]) * 256u;
+                        const uint32_t um = gcol + uint32_t(mag[t] == 0 ? NT / 2 : (B == 1 ? 0 : NT - mag[t])) * 256u;
+                        const float qm = mag[t] == 0 ? 0.f : -q;
+                        if constexpr (UPG % 4 == 0) {
+#pragma unroll
+                            for (int c4 = 0; c4 < UPG; c4 += 4) {
+                                lds_st4(up + c4 * 4u, q);
+                                lds_st4(um + c4 * 4u, qm);
+                            }
+                        } else {
+#pragma unroll
+                            for (int c1 = 0; c1 < UPG; ++c1) {
+                                lds_st(up + c1 * 4u, q);
+                                lds_st(um + c1 * 4u, qm);
+                            }
+                        }
+                    }
+                }
+                wave_lds_fence();
+            }
+            const float al = a * (1.0f / float(M));
+            const float be = b * (1.0f / float(M * M));
+            const float ga = cc * (1.0f / float(M * M * M));
+            float p0 = 0.f, p1 = 0.f;
+#pragma unroll
+            for (int i8 = 0; i8 < 4; ++i8) {
+                float lv[8];
+                if constexpr (B == 4) {
+                    const uint32_t wd = w[r][i8];
+                    const uint32_t ev = (wd & 0x0f0f0f0fu) | wtag;
+                    const uint32_t od = ((wd >> 4) & 0x0f0f0f0fu) | wtag;
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj) {
+                        const uint32_t sel = 0x03020000u | (uint32_t(4 + jj) << 8);
+                        lv[2 * jj] = lds_ld(__builtin_amdgcn_perm(ev, col, sel));
+                        lv[2 * jj + 1] = lds_ld(__builtin_amdgcn_perm(od, col, sel));
+                    }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int i = i8 * 8 + e;
+                        const int bit = i * B;
+                        const int wd = bit >> 5, sh = bit & 31;
+                        uint32_t v;
+                        if (sh + B <= 32) v = w[r][wd] >> sh;
+                        else v = __builtin_amdgcn_alignbit(w[r][wd + 1], w[r][wd], sh);
+                        if constexpr (LUT) {
+                            lv[e] = lds_ld(((v & uint32_t(NT - 1)) << 8) + col);
+                        } else {
+                            const int kk = __builtin_amdgcn_sbfe(int(v), 0, B);
+                            const float kf = float(kk);
+                            const float ak = __builtin_fabsf(kf);
+                            const float lvv = kf * __builtin_fmaf(ak, __builtin_fmaf(ak, ga, be), al);
+                            lv[e] = (kk == -(1 << (B - 1))) ? 0.f : lvv;
+                        }
+                    }
+                }
+#pragma unroll
+                for (int e = 0; e < 8; e += 2) {
+                    p0 = __builtin_fmaf(xf[i8 * 8 + e], lv[e], p0);
+                    p1 = __builtin_fmaf(xf[i8 * 8 + e + 1], lv[e + 1], p1);
+                }
+            }
+            acc[r] = __builtin_fmaf(rok[r] ? s[r] : 0.f, p0 + p1, acc[r]);
+        }
+        if (ci == cbw - 1) {
+            // ---- tile done: reduce each row across the wave, then across waves
+#pragma unroll
+            for (int r = 0; r < RW; ++r) {
+                float v = acc[r];
+#pragma unroll
+                for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+                if (lane == 0) red[wave * RW + r] = v;
+                acc[r] = 0.f;
+            }
+            __syncthreads();
+            if (wave == 0 && lane < RW) {
+                const int64_t row = row0 + lane;
+                if (row < n) {
+                    float v = 0.f;
+                    for (int wv = 0; wv < nwaves; ++wv) v += red[wv * RW + lane];
+                    store_out<YDT>(y, row, v);
+                }
+            }
+            __syncthreads();  // red is reused by the next tile
+        }
+    }
+}
+
+template <int B, int UPG, int RW, int XDT, int YDT>
+static hipError_t stream_waves(const cq_weight &w, const void *x, void *y, hipStream_t stream) {
+    const int64_t ncb = ((w.k >> 5) + 63) >> 6;
+    constexpr int NT = B <= 5 ? (1 << B) : 1;
+    constexpr int kMaxW = NT >= 32 ? 4 : 8;  // keep the tables within 32 KB
+    // Two waves split the column blocks of a tile; more waves per workgroup
+    // only add tile-reduction cost (measured on Llama-3-8B layer shapes).
+    int nw = ncb >= 2 ? 2 : 1;
+    if (nw > kMaxW) nw = kMaxW;
+    const size_t lds = sizeof(float) * (size_t(nw) * NT * 64 + size_t(nw) * RW);
+    const int64_t tiles = (w.n + RW - 1) / RW;
+    // one workgroup per tile up to 64 per CU; the kernel strides over the rest
+    int64_t blocks = int64_t(device_cu_count()) * 64;
+    if (blocks > tiles) blocks = tiles;
+    hipLaunchKernelGGL((gemv_a16_stream<B, UPG, RW, XDT, YDT>), dim3(unsigned(blocks)), dim3(nw * 64), lds, stream,
+                       w.codes, w.scale, w.a, w.b, w.n, w.k, static_cast<const uint16_t *>(x), y);
+    return hipGetLastError();
+}
+
+template <int B, int UPG, int XDT, int YDT>
+static hipError_t stream_rows(const cq_weight &w, const void *x, void *y, hipStream_t stream) {
+    // two rows per workgroup: the smallest tile keeps the most workgroups in
+    // flight, which is what hides the load latency of a streaming GEMV
+    return stream_waves<B, UPG, 2, XDT, YDT>(w, x, y, stream);
+}
+
+template <int B, int XDT, int YDT>
+static hipError_t stream_group(const cq_weight &w, const void *x, void *y, hipStream_t stream) {
+    switch (w.group) {
+        case 32: return stream_rows<B, 1, XDT, YDT>(w, x, y, stream);
+        case 64: return stream_rows<B, 2, XDT, YDT>(w, x, y, stream);
+        case 128: return stream_rows<B, 4, XDT, YDT>(w, x, y, stream);
+        case 256: return stream_rows<B, 8, XDT, YDT>(w, x, y, stream);
+        case 512: return stream_rows<B, 16, XDT, YDT>(w, x, y, stream);
+    }
+    return hipErrorNotSupported;
+}
+
+template <int XDT, int YDT>
+static hipError_t stream_bits(const cq_weight &w, const void *x, void *y, hipStream_t stream) {
+    switch (w.bits) {
+        case 1: return stream_group<1, XDT, YDT>(w, x, y, stream);
+        case 2: return stream_group<2, XDT, YDT>(w, x, y, stream);
+        case 3: return stream_group<3, XDT, YDT>(w, x, y, stream);
+        case 4: return stream_group<4, XDT, YDT>(w, x, y, stream);
+        case 5: return stream_group<5, XDT, YDT>(w, x, y, stream);
+        case 6: return stream_group<6, XDT, YDT>(w, x, y, stream);
+        case 7: return stream_group<7, XDT, YDT>(w, x, y, stream);
+        case 8: return stream_group<8, XDT, YDT>(w, x, y, stream);
+    }
+    return hipErrorNotSupported;
+}
+
+hipError_t launch_gemv_a16_stream(const cq_weight &w, const void *x, int x_dt, void *y, int y_dt,
+                                  hipStream_t stream) {
+    if (x_dt == 0) {
+        if (y_dt == 0) return stream_bits<0, 0>(w, x, y, stream);
+        return stream_bits<0, 2>(w, x, y, stream);
+    }
+    if (y_dt == 1) return stream_bits<1, 1>(w, x, y, stream);
+    return stream_bits<1, 2>(w, x, y, stream);
+}
+
+}  // namespace cq
