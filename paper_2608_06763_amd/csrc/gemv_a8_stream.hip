@@ -1,0 +1,350 @@
+// Dynamic-A8 single-row GEMV, streaming byte-permute family (Sec. 5.4) for
+// m == 1 and B in {1, 2, 4}.
+//
+// Numerics are those of eq. a8-output: every weight contributes the INT8
+// carrier r(k) = sign(k) RNE(127 q(|k|/M)) (eq. carrier, Appendix A item 7)
+// times the INT8 activation, summed exactly in INT32 over a 32-code unit (a
+// K-tile partial of the group partial P_g, which Sec. 5.4 allows); each unit
+// partial is converted to FP32 and weighted by s_g, and the row factor
+// d_x / 127 multiplies the FP32 sum.
+//
+// Work mapping: identical to the model-dtype streaming GEMV (lane l owns unit
+// l of a 2048-code column block, RW rows per workgroup tile, waves split the
+// column blocks and meet in LDS, the next item's codes are requested before
+// the current item is decoded).
+//
+// Decode without memory tables.  A W4 field n (two's complement, 8 reserved)
+// selects from two 8-byte carrier tables held in registers:
+//   TA[i] = r(i) for n = i < 8, and TB[i] = -r(8 - i) for n = 8 + i (TB[0] = 0
+//   is the reserved pattern).
+// One v_perm_b32 looks up four fields in a table; a byte mask from bit 3 of each
+// field picks TA or TB per byte, and v_dot4_i32_i8 multiplies the four carriers
+// with four activations.  The carriers of a group are computed once per
+// (row, group): the group's lanes each evaluate two magnitudes and share them
+// through quad DPP moves.  W2 and W1 use constant tables ({0, 127, 0, -127}
+// and {-127, 127}).
+//
+// Exact carriers.  127 q(i/M) is first evaluated in FP32 (Horner, eq.
+// gpu-horner); its rounding error is below 127 * 2^-20 * (|a| + |b| + |c| + 1).
+// Only when the estimate lies closer than that to a half-integer is the
+// carrier recomputed with the exact FP64 residual test, so every carrier equals
+// the RNE of the exact rational value.
+#include "cq_device.h"
+#include "cq_internal.h"
+
+namespace cq {
+
+namespace {
+
+__device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel) {
+    return __builtin_amdgcn_perm(hi, lo, sel);
+}
+
+// INT8 carrier of magnitude i with t = i / M (exact when close to a tie).
+template <int M>
+__device__ __forceinline__ uint32_t carrier_u8(int i, float t, float a, float b, float c, float margin) {
+    const float f = 127.0f * (t * __builtin_fmaf(t, __builtin_fmaf(t, c, b), a));
+    float r = __builtin_rintf(f);
+    if (__builtin_expect(__builtin_fabsf(f - r) > 0.5f - margin, 0)) {
+        r = float(exact_carrier(i, M, double(a), double(b)));
+    }
+    r = r < 0.f ? 0.f : (r > 127.f ? 127.f : r);
+    return uint32_t(int(r));
+}
+
+// Quad-lane broadcast (DPP quad_perm): every lane reads lane `src` of the
+// lanes {4q, 4q + 1, 4q + 2, 4q + 3} as given by the control pattern.
+template <int CTRL>
+__device__ __forceinline__ uint32_t quad_bcast(uint32_t v) {
+    return uint32_t(__builtin_amdgcn_mov_dpp(int(v), CTRL, 0xf, 0xf, true));
+}
+
+// Byte transpose of a 4 x 4 byte matrix held in four words: out[s] byte b =
+// in[b] byte s.
+__device__ __forceinline__ void transpose4(const uint32_t in[4], uint32_t out[4]) {
+    const uint32_t t0 = perm(in[1], in[0], 0x05010400u);  // in0.b0 in1.b0 in0.b1 in1.b1
+    const uint32_t t1 = perm(in[1], in[0], 0x07030602u);  // in0.b2 in1.b2 in0.b3 in1.b3
+    const uint32_t t2 = perm(in[3], in[2], 0x05010400u);
+    const uint32_t t3 = perm(in[3], in[2], 0x07030602u);
+    out[0] = perm(t2, t0, 0x05040100u);  // in0.b0 in1.b0 in2.b0 in3.b0
+    out[1] = perm(t2, t0, 0x07060302u);
+    out[2] = perm(t3, t1, 0x05040100u);
+    out[3] = perm(t3, t1, 0x07060302u);
+}
+
+// Activations of one unit (32 INT8 values in 8 words), rearranged in the byte
+// order in which the decode produces carriers.
+template <int B>
+__device__ __forceinline__ void arrange_x(const uint32_t xw[8], uint32_t xa[8]) {
+    if constexpr (B == 4) {
+        // word i of codes holds fields 8i..8i+7; the even fields come out as
+        // bytes (8i, 8i+2, 8i+4, 8i+6), the odd ones as (8i+1, ...)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            xa[2 * i] = perm(xw[2 * i + 1], xw[2 * i], 0x06040200u);
+            xa[2 * i + 1] = perm(xw[2 * i + 1], xw[2 * i], 0x07050301u);
+        }
+    } else if constexpr (B == 2) {
+        // word i of codes holds fields 16i..16i+15; shift s gives fields
+        // (16i + s, +4, +8, +12), i.e. byte s of x words 4i..4i+3
+#pragma unroll
+        for (int i = 0; i < 2; ++i) transpose4(xw + 4 * i, xa + 4 * i);
+    } else {
+        // one word of codes holds all 32 fields; shift s gives fields
+        // (s, 8 + s, 16 + s, 24 + s): byte s%4 of x words s/4, 2 + s/4, 4 + s/4, 6 + s/4
+        const uint32_t ev[4] = {xw[0], xw[2], xw[4], xw[6]};
+        const uint32_t od[4] = {xw[1], xw[3], xw[5], xw[7]};
+        uint32_t te[4], to[4];
+        transpose4(ev, te);
+        transpose4(od, to);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            xa[s] = te[s];
+            xa[4 + s] = to[s];
+        }
+    }
+}
+
+}  // namespace
+
+template <int B, int UPG, int RW, int YDT>
+__global__ void __launch_bounds__(512) gemv_a8_stream(
+    const uint8_t *__restrict__ codes, const float *__restrict__ scale,
+    const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
+    int64_t n, int64_t k, const int8_t *__restrict__ x8, const float *__restrict__ dx, void *__restrict__ y) {
+    constexpr int M = max_code(B);
+    __shared__ float red[8 * RW];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int nwaves = blockDim.x >> 6;
+    const int64_t ntiles = (n + RW - 1) / RW;
+    const int64_t units = k >> 5;
+    const int64_t ncb = (units + 63) >> 6;
+    const int64_t ng = k / (UPG * 32);
+    const int64_t row_words = (k * B) >> 5;
+
+    // W4 carrier pairs evaluated by this lane: pair p covers magnitudes 2p, 2p+1.
+    // Q lanes of a quad share a group; lane j of them evaluates pairs j, j+Q, ...
+    constexpr int Q = UPG >= 4 ? 4 : UPG;
+    constexpr int NP = 4 / Q;
+    float tp0[NP], tp1[NP];
+    int ip0[NP];
+#pragma unroll
+    for (int j = 0; j < NP; ++j) {
+        ip0[j] = 2 * ((lane % Q) + Q * j);
+        tp0[j] = float(ip0[j]) / float(M);
+        tp1[j] = float(ip0[j] + 1) / float(M);
+    }
+
+    const int64_t my_tiles = blockIdx.x < ntiles ? (ntiles - 1 - blockIdx.x) / gridDim.x + 1 : 0;
+    const int64_t cbw = (ncb - wave + nwaves - 1) / nwaves;
+    const int64_t items = my_tiles * cbw;
+
+    uint32_t wn[RW][B];
+    float sn[RW];
+    uint32_t an[RW], bn[RW];
+    auto fetch = [&](int64_t it) {
+        const int64_t tile = blockIdx.x + (it / cbw) * gridDim.x;
+        const int64_t cb = wave + (it % cbw) * nwaves;
+        const int64_t u_raw = cb * 64 + lane;
+        const int64_t u = u_raw < units ? u_raw : units - 1;  // clamped: loads stay valid
+        const int64_t g = u / UPG;
+#pragma unroll
+        for (int r = 0; r < RW; ++r) {
+            const int64_t row_raw = tile * RW + r;
+            const int64_t row = row_raw < n ? row_raw : n - 1;
+            const uint32_t *wp = reinterpret_cast<const uint32_t *>(codes) + row * row_words + u * B;
+#pragma unroll
+            for (int i = 0; i < B; ++i) wn[r][i] = __builtin_nontemporal_load(wp + i);
+            const int64_t gi = row * ng + g;
+            sn[r] = scale[gi];
+            if constexpr (B == 4) {
+                an[r] = a16[gi];
+                bn[r] = b16[gi];
+            }
+        }
+    };
+
+    float acc[RW];
+#pragma unroll
+    for (int i = 0; i < RW; ++i) acc[i] = 0.f;
+    if (items > 0) fetch(0);
+    for (int64_t it = 0; it < items; ++it) {
+        const int64_t tile = blockIdx.x + (it / cbw) * gridDim.x;
+        const int64_t ci = it % cbw;
+        const int64_t cb = wave + ci * nwaves;
+        const int64_t row0 = tile * RW;
+        uint32_t w[RW][B];
+        float s[RW];
+        uint32_t av[RW], bv[RW];
+#pragma unroll
+        for (int r = 0; r < RW; ++r) {
+#pragma unroll
+            for (int i = 0; i < B; ++i) w[r][i] = wn[r][i];
+            s[r] = sn[r];
+            av[r] = an[r];
+            bv[r] = bn[r];
+        }
+        if (it + 1 < items) fetch(it + 1);
+        const int64_t u_raw = cb * 64 + lane;
+        const bool live = u_raw < units;
+        const int64_t u = live ? u_raw : units - 1;
+
+        uint32_t xa[8];
+        {
+            const uint4 *xp = reinterpret_cast<const uint4 *>(x8 + u * 32);
+            const uint4 v0 = xp[0], v1 = xp[1];
+            const uint32_t xw[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+            arrange_x<B>(xw, xa);
+        }
+
+#pragma unroll
+        for (int r = 0; r < RW; ++r) {
+            int p = 0;
+            if constexpr (B == 4) {
+                const float a = f16_to_f32(uint16_t(av[r]));
+                const float b = f16_to_f32(uint16_t(bv[r]));
+                const float c = 1.f - a - b;
+                const float margin =
+                    (__builtin_fabsf(a) + __builtin_fabsf(b) + __builtin_fabsf(c) + 1.f) * (127.0f / 1048576.0f);
+                uint32_t pr[NP];
+#pragma unroll
+                for (int j = 0; j < NP; ++j) {
+                    pr[j] = carrier_u8<M>(ip0[j], tp0[j], a, b, c, margin) |
+                            (carrier_u8<M>(ip0[j] + 1, tp1[j], a, b, c, margin) << 8);
+                }
+                uint32_t P[4];
+                if constexpr (Q == 4) {
+                    P[0] = quad_bcast<0x00>(pr[0]);
+                    P[1] = quad_bcast<0x55>(pr[0]);
+                    P[2] = quad_bcast<0xaa>(pr[0]);
+                    P[3] = quad_bcast<0xff>(pr[0]);
+                } else if constexpr (Q == 2) {
+                    P[0] = quad_bcast<0xa0>(pr[0]);
+                    P[1] = quad_bcast<0xf5>(pr[0]);
+                    P[2] = quad_bcast<0xa0>(pr[1]);
+                    P[3] = quad_bcast<0xf5>(pr[1]);
+                } else {
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) P[j] = pr[j];
+                }
+                const uint32_t ta0 = P[0] | (P[1] << 16);  // r0 r1 r2 r3
+                const uint32_t ta1 = P[2] | (P[3] << 16);  // r4 r5 r6 r7
+                // TB = [0, -r7, -r6, -r5 | -r4, -r3, -r2, -r1]; bytewise negation of
+                // values in [0, 127] without borrows: (0x80 - v) ^ 0x80
+                const uint32_t tbp0 = perm(ta1, ta0, 0x0506070cu);
+                const uint32_t tbp1 = perm(ta1, ta0, 0x01020304u);
+                const uint32_t tb0 = (0x80808080u - tbp0) ^ 0x80808080u;
+                const uint32_t tb1 = (0x80808080u - tbp1) ^ 0x80808080u;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const uint32_t wd = w[r][i];
+                    const uint32_t f2[2] = {wd & 0x0f0f0f0fu, (wd >> 4) & 0x0f0f0f0fu};
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const uint32_t idx = f2[h] & 0x07070707u;
+                        // 0xff in the bytes whose field has bit 3 set (selector 8 = sign of byte 1)
+                        const uint32_t msk = perm(0u, 0x00008000u, f2[h] & 0x08080808u);
+                        const uint32_t pa = perm(ta1, ta0, idx);
+                        const uint32_t pb = perm(tb1, tb0, idx);
+                        const uint32_t rc = (msk & pb) | (~msk & pa);
+                        p = __builtin_amdgcn_sdot4(int(rc), int(xa[2 * i + h]), p, false);
+                    }
+                }
+            } else if constexpr (B == 2) {
+                // fields 0 -> 0, 1 -> +127, 2 (reserved) -> 0, 3 -> -127
+                constexpr uint32_t T = 0x81007f00u;
+#pragma unroll
+                for (int i = 0; i < 2; ++i) {
+#pragma unroll
+                    for (int sft = 0; sft < 4; ++sft) {
+                        const uint32_t sel = (w[r][i] >> (2 * sft)) & 0x03030303u;
+                        p = __builtin_amdgcn_sdot4(int(perm(T, T, sel)), int(xa[4 * i + sft]), p, false);
+                    }
+                }
+            } else {
+                // bit 1 -> +127, bit 0 -> -127
+                constexpr uint32_t T = 0x00007f81u;
+#pragma unroll
+                for (int sft = 0; sft < 8; ++sft) {
+                    const uint32_t sel = (w[r][0] >> sft) & 0x01010101u;
+                    p = __builtin_amdgcn_sdot4(int(perm(T, T, sel)), int(xa[sft]), p, false);
+                }
+            }
+            const bool rok = live && (row0 + r < n);
+            acc[r] = __builtin_fmaf(rok ? s[r] : 0.f, float(p), acc[r]);
+        }
+        if (ci == cbw - 1) {
+#pragma unroll
+            for (int r = 0; r < RW; ++r) {
+                float v = acc[r];
+#pragma unroll
+                for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+                if (lane == 0) red[wave * RW + r] = v;
+                acc[r] = 0.f;
+            }
+            __syncthreads();
+            if (wave == 0 && lane < RW) {
+                const int64_t row = row0 + lane;
+                if (row < n) {
+                    float v = 0.f;
+                    for (int wv = 0; wv < nwaves; ++wv) v += red[wv * RW + lane];
+                    store_out<YDT>(y, row, v * (dx[0] / 127.0f));
+                }
+            }
+            __syncthreads();
+        }
+    }
+}
+
+template <int B, int UPG, int YDT>
+static hipError_t a8_stream_launch(const cq_weight &w, const int8_t *x8, const float *dx, void *y,
+                                   hipStream_t stream) {
+    constexpr int RW = 2;
+    const int64_t ncb = ((w.k >> 5) + 63) >> 6;
+    const int nw = ncb >= 2 ? 2 : 1;
+    const int64_t tiles = (w.n + RW - 1) / RW;
+    int64_t blocks = int64_t(device_cu_count()) * 64;
+    if (blocks > tiles) blocks = tiles;
+    hipLaunchKernelGGL((gemv_a8_stream<B, UPG, RW, YDT>), dim3(unsigned(blocks)), dim3(nw * 64), 0, stream, w.codes,
+                       w.scale, w.a, w.b, w.n, w.k, x8, dx, y);
+    return hipGetLastError();
+}
+
+template <int B, int YDT>
+static hipError_t a8_stream_group(const cq_weight &w, const int8_t *x8, const float *dx, void *y,
+                                  hipStream_t stream) {
+    switch (w.group) {
+        case 32: return a8_stream_launch<B, 1, YDT>(w, x8, dx, y, stream);
+        case 64: return a8_stream_launch<B, 2, YDT>(w, x8, dx, y, stream);
+        case 128: return a8_stream_launch<B, 4, YDT>(w, x8, dx, y, stream);
+        case 256: return a8_stream_launch<B, 8, YDT>(w, x8, dx, y, stream);
+        case 512: return a8_stream_launch<B, 16, YDT>(w, x8, dx, y, stream);
+    }
+    return hipErrorNotSupported;
+}
+
+template <int YDT>
+static hipError_t a8_stream_bits(const cq_weight &w, const int8_t *x8, const float *dx, void *y,
+                                 hipStream_t stream) {
+    switch (w.bits) {
+        case 1: return a8_stream_group<1, YDT>(w, x8, dx, y, stream);
+        case 2: return a8_stream_group<2, YDT>(w, x8, dx, y, stream);
+        case 4: return a8_stream_group<4, YDT>(w, x8, dx, y, stream);
+    }
+    return hipErrorNotSupported;
+}
+
+bool gemv_a8_stream_supported(const cq_weight &w, int64_t m) {
+    return m == 1 && (w.bits == 1 || w.bits == 2 || w.bits == 4);
+}
+
+hipError_t launch_gemv_a8_stream(const cq_weight &w, const int8_t *x8, const float *dx, void *y, int y_dt,
+                                 hipStream_t stream) {
+    if (y_dt == 0) return a8_stream_bits<0>(w, x8, dx, y, stream);
+    if (y_dt == 1) return a8_stream_bits<1>(w, x8, dx, y, stream);
+    return a8_stream_bits<2>(w, x8, dx, y, stream);
+}
+
+}  // namespace cq

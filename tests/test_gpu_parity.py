@@ -12,7 +12,7 @@ import pytest
 from oracle import a8 as A8
 from oracle import format as F
 from oracle import ref as R
-from tests._cases import act, fitted, ref_a8, ref_model_dtype, say
+from tests._cases import act, carrier_probe, fitted, ref_a8, ref_model_dtype, say
 
 pytestmark = pytest.mark.gpu
 
@@ -296,3 +296,50 @@ def test_edge_shapes(torch_dev, n, k, g, m):
     ya, parts = _cq().cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32, want_partials=True)
     assert np.array_equal(parts.cpu().numpy(), p_ref)
     assert R.eps_comp(_np(ya), ya_ref, "fp32") <= 1e-5
+
+
+# ---------------------------------------------------------------- single-row A8 streaming family
+
+
+@pytest.mark.parametrize("bits", [1, 2, 4])
+@pytest.mark.parametrize("group", GROUPS)
+@pytest.mark.parametrize("k", [768, 4096 + 2048 + 512])
+def test_gemv_a8_stream(torch_dev, bits, group, k):
+    # m == 1 without a partials dump takes the streaming byte-permute kernel
+    if k % group:
+        pytest.skip("K must be a multiple of G")
+    r = fitted(23, 67, k, bits, group)
+    xb, xv = act(24, 1, k)
+    x8_ref, d_ref, y_ref, _ = ref_a8(xv, r, bits, group)
+    say("gemv_a8_stream", bits, group, k)
+    w = _weight(r, bits, group)
+    x8 = torch_dev.from_numpy(x8_ref).cuda()
+    dx = torch_dev.from_numpy(d_ref).cuda()
+    y = _cq().cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32)
+    y16 = _cq().cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.bfloat16)
+    assert R.eps_comp(_np(y), y_ref, "fp32") <= 1e-5
+    assert R.eps_comp(_np(y16), y_ref, "bf16") <= TOL
+
+
+@pytest.mark.parametrize("bits", [3, 4, 5, 6, 7, 8])
+@pytest.mark.parametrize("family", ["stream", "gemv", "gemm"])
+def test_a8_near_tie_carriers_exact(torch_dev, bits, family):
+    # rows whose shapes put a carrier within 3e-4 of a half-integer; with unit
+    # scales and d_x = 127 the FP32 output is the exact integer sum of P_g
+    codes, s, a, b, x8, dx, p = carrier_probe(bits, 128)
+    say("a8_near_tie", bits, family, len(a))
+    cq = _cq()
+    w = cq.CQWeight.from_codes(codes, s, a, b, bits, 128)
+    x8_t = torch_dev.from_numpy(x8).cuda()
+    dx_t = torch_dev.from_numpy(dx).cuda()
+    if family == "gemm":
+        cq.cq_set_gemv_max_rows(1, 0)
+    try:
+        if family == "stream":
+            y = cq.cq_gemm_a8(w, x8_t, dx_t, y_dtype=torch_dev.float32)
+        else:
+            y, parts = cq.cq_gemm_a8(w, x8_t, dx_t, y_dtype=torch_dev.float32, want_partials=True)
+            assert np.array_equal(parts.cpu().numpy(), p)
+    finally:
+        cq.cq_set_gemv_max_rows(1, -1)
+    assert np.array_equal(_np(y).astype(np.float64), p.sum(axis=-1).astype(np.float64))
