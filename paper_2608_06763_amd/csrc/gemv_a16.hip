@@ -11,6 +11,7 @@
 // supported G.
 #include "cq_device.h"
 #include "cq_internal.h"
+#include "stream_common.h"
 
 namespace cq {
 
@@ -113,7 +114,7 @@ static hipError_t dispatch_bits(const cq_weight &w, const void *x, int64_t m, vo
 
 hipError_t launch_gemv_a16(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                            hipStream_t stream) {
-    if (m == 1) return launch_gemv_a16_stream(w, x, x_dt, y, y_dt, stream);
+    if (m == 1 && stream_fits(w.n, w.k, w.bits, w.group)) return launch_gemv_a16_stream(w, x, x_dt, y, y_dt, stream);
     if (gemv_a16_lut_supported(w, m)) {
         const hipError_t e = launch_gemv_a16_lut(w, x, x_dt, m, y, y_dt, stream);
         if (e != hipErrorNotSupported) return e;

@@ -24,6 +24,7 @@
 // evaluates the cubic in registers instead of keeping a 64..256-entry table.
 #include "cq_device.h"
 #include "cq_internal.h"
+#include "stream_common.h"
 
 namespace cq {
 
@@ -50,10 +51,10 @@ __device__ __forceinline__ void wave_lds_fence() {
 }  // namespace
 
 template <int B, int UPG, int RW, int XDT, int YDT>
-__global__ void __launch_bounds__(512) gemv_a16_stream(
+__global__ void __launch_bounds__(256) gemv_a16_stream(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
-    int64_t n, int64_t k, const uint16_t *__restrict__ x, void *__restrict__ y) {
+    int n, int k, const uint16_t *__restrict__ x, void *__restrict__ y) {
     constexpr int G = UPG * 32;
     constexpr int M = max_code(B);
     constexpr bool LUT = (B <= 5);
@@ -65,13 +66,18 @@ __global__ void __launch_bounds__(512) gemv_a16_stream(
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int nwaves = blockDim.x >> 6;
+    const int nwaves = blockDim.x >> 6;  // the host keeps nwaves <= ncb
     float *red = tab + nwaves * NT * 64;
-    const int64_t ntiles = (n + RW - 1) / RW;
-    const int64_t units = k >> 5;
-    const int64_t ncb = (units + 63) >> 6;
-    const int64_t ng = k / G;
-    const int64_t row_words = (k * B) >> 5;
+    const int ntiles = (n + RW - 1) / RW;
+    const int units = k >> 5;
+    const int ncb = (units + 63) >> 6;
+    const int ng = k / G;
+    const uint32_t row_bytes = uint32_t(k) * B / 8;
+    const auto rc = make_rsrc(codes, uint32_t(n) * row_bytes);
+    const auto rs = make_rsrc(scale, uint32_t(n) * ng * 4u);
+    const auto ra = make_rsrc(a16, uint32_t(n) * ng * 2u);
+    const auto rb = make_rsrc(b16, uint32_t(n) * ng * 2u);
+    const auto rx = make_rsrc(x, uint32_t(k) * 2u);
     const uint32_t tbase = uint32_t(uintptr_t((lds_f *)tab));
     const uint32_t col = tbase + uint32_t(wave) * (NT * 256u) + uint32_t(lane) * 4u;
     // first column of this lane's group inside the wave (the group's UPG lanes are adjacent)
@@ -88,46 +94,35 @@ __global__ void __launch_bounds__(512) gemv_a16_stream(
         tq[t] = float(mag[t]) * (1.0f / float(M));
     }
 
-    // Persistent grid: a workgroup walks row tiles blockIdx.x, + gridDim.x, ...
-    // and every wave walks its column blocks of each tile.  The codes and
-    // metadata of the next (tile, column block) item are requested before the
-    // current item is decoded, so HBM reads always overlap decoding.
-    const int64_t my_tiles = blockIdx.x < ntiles ? (ntiles - 1 - blockIdx.x) / gridDim.x + 1 : 0;
-    const int64_t cbw = (ncb - wave + nwaves - 1) / nwaves;  // column blocks of this wave per tile
-    const int64_t items = my_tiles * cbw;
-
+    // An item is (row tile, column block).  A workgroup walks the tiles
+    // blockIdx.x + j * gridDim.x; its wave w takes column blocks w, w + nwaves,
+    // ... of each tile.  The codes and metadata of the next item are requested
+    // before the current one is decoded.  Rows and lanes past the matrix load
+    // an out-of-range offset and read zeros (zero scale, so they add nothing).
     uint32_t wn[RW][B];
     float sn[RW];
     uint32_t an[RW], bn[RW];
-    auto fetch = [&](int64_t it) {
-        const int64_t tile = blockIdx.x + (it / cbw) * gridDim.x;
-        const int64_t cb = wave + (it % cbw) * nwaves;
-        const int64_t u_raw = cb * 64 + lane;
-        const int64_t u = u_raw < units ? u_raw : units - 1;  // clamped: loads stay valid
-        const int64_t g = u / UPG;
+    auto fetch = [&](int t, int c) {
+        const int u = c * 64 + lane;
 #pragma unroll
         for (int r = 0; r < RW; ++r) {
-            const int64_t row_raw = tile * RW + r;
-            const int64_t row = row_raw < n ? row_raw : n - 1;
-            const uint32_t *wp = reinterpret_cast<const uint32_t *>(codes) + row * row_words + u * B;
-#pragma unroll
-            for (int i = 0; i < B; ++i) wn[r][i] = __builtin_nontemporal_load(wp + i);
-            const int64_t gi = row * ng + g;
-            sn[r] = scale[gi];
-            an[r] = a16[gi];
-            bn[r] = b16[gi];
+            const int row = t * RW + r;
+            const bool ok = (u < units) && (row < n);
+            const uint32_t gi = uint32_t(row) * ng + uint32_t(u / UPG);
+            load_words<B>(rc, ok ? uint32_t(row) * row_bytes + uint32_t(u) * (4 * B) : kOobOffset, wn[r]);
+            sn[r] = load_f32(rs, ok ? gi * 4u : kOobOffset);
+            an[r] = load_u16(ra, ok ? gi * 2u : kOobOffset);
+            bn[r] = load_u16(rb, ok ? gi * 2u : kOobOffset);
         }
     };
 
     float acc[RW];
 #pragma unroll
     for (int i = 0; i < RW; ++i) acc[i] = 0.f;
-    if (items > 0) fetch(0);
-    for (int64_t it = 0; it < items; ++it) {
-        const int64_t tile = blockIdx.x + (it / cbw) * gridDim.x;
-        const int64_t ci = it % cbw;
-        const int64_t cb = wave + ci * nwaves;
-        const int64_t row0 = tile * RW;
+    int tile = blockIdx.x, cb = wave;
+    bool have = tile < ntiles;
+    if (have) fetch(tile, cb);
+    while (have) {
         uint32_t w[RW][B];
         float s[RW];
         uint32_t av[RW], bv[RW];
@@ -139,23 +134,25 @@ __global__ void __launch_bounds__(512) gemv_a16_stream(
             av[r] = an[r];
             bv[r] = bn[r];
         }
-        if (it + 1 < items) fetch(it + 1);
-        const int64_t u_raw = cb * 64 + lane;
-        const bool live = u_raw < units;
-        const int64_t u = live ? u_raw : units - 1;
-        bool rok[RW];
-#pragma unroll
-        for (int r = 0; r < RW; ++r) rok[r] = live && (row0 + r < n);
+        int cb_next = cb + nwaves, tile_next = tile;
+        const bool last_cb = cb_next >= ncb;
+        if (last_cb) {
+            cb_next = wave;
+            tile_next = tile + int(gridDim.x);
+        }
+        const bool have_next = tile_next < ntiles;
+        if (have_next) fetch(tile_next, cb_next);
+        const int u = cb * 64 + lane;
         // ---- activations of this unit, FP32 in registers
         float xf[32];
         {
-            const uint4 *xp = reinterpret_cast<const uint4 *>(x + u * 32);
-            uint4 xv[4];
+            const uint32_t xo = u < units ? uint32_t(u) * 64u : kOobOffset;
+            uint32_t xv[4][4];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) xv[q] = xp[q];
+            for (int q = 0; q < 4; ++q) load_words<4>(rx, xo + 16u * q, xv[q]);
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                const uint32_t vw[4] = {xv[q].x, xv[q].y, xv[q].z, xv[q].w};
+                const uint32_t *vw = xv[q];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     xf[q * 8 + 2 * e] = act_to_f32<XDT>(uint16_t(vw[e] & 0xffffu));
@@ -251,29 +248,36 @@ __global__ void __launch_bounds__(512) gemv_a16_stream(
                     p1 = __builtin_fmaf(xf[i8 * 8 + e + 1], lv[e + 1], p1);
                 }
             }
-            acc[r] = __builtin_fmaf(rok[r] ? s[r] : 0.f, p0 + p1, acc[r]);
+            acc[r] = __builtin_fmaf(s[r], p0 + p1, acc[r]);
         }
-        if (ci == cbw - 1) {
-            // ---- tile done: reduce each row across the wave, then across waves
+        if (last_cb) {
+            const int row0 = tile * RW;
+            if (nwaves == 1) {
 #pragma unroll
-            for (int r = 0; r < RW; ++r) {
-                float v = acc[r];
+                for (int r = 0; r < RW; ++r) {
+                    const float v = wave_sum(acc[r]);
+                    acc[r] = 0.f;
+                    if (lane == r && row0 + r < n) store_out<YDT>(y, row0 + r, v);
+                }
+            } else {
 #pragma unroll
-                for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-                if (lane == 0) red[wave * RW + r] = v;
-                acc[r] = 0.f;
-            }
-            __syncthreads();
-            if (wave == 0 && lane < RW) {
-                const int64_t row = row0 + lane;
-                if (row < n) {
+                for (int r = 0; r < RW; ++r) {
+                    const float v = wave_sum(acc[r]);
+                    acc[r] = 0.f;
+                    if (lane == 0) red[wave * RW + r] = v;
+                }
+                __syncthreads();
+                if (wave == 0 && lane < RW && row0 + lane < n) {
                     float v = 0.f;
                     for (int wv = 0; wv < nwaves; ++wv) v += red[wv * RW + lane];
-                    store_out<YDT>(y, row, v);
+                    store_out<YDT>(y, row0 + lane, v);
                 }
+                __syncthreads();  // red is reused by the next tile
             }
-            __syncthreads();  // red is reused by the next tile
         }
+        tile = tile_next;
+        cb = cb_next;
+        have = have_next;
     }
 }
 
@@ -292,7 +296,7 @@ static hipError_t stream_waves(const cq_weight &w, const void *x, void *y, hipSt
     int64_t blocks = int64_t(device_cu_count()) * 64;
     if (blocks > tiles) blocks = tiles;
     hipLaunchKernelGGL((gemv_a16_stream<B, UPG, RW, XDT, YDT>), dim3(unsigned(blocks)), dim3(nw * 64), lds, stream,
-                       w.codes, w.scale, w.a, w.b, w.n, w.k, static_cast<const uint16_t *>(x), y);
+                       w.codes, w.scale, w.a, w.b, int(w.n), int(w.k), static_cast<const uint16_t *>(x), y);
     return hipGetLastError();
 }
 

@@ -31,6 +31,7 @@
 // the RNE of the exact rational value.
 #include "cq_device.h"
 #include "cq_internal.h"
+#include "stream_common.h"
 
 namespace cq {
 
@@ -108,21 +109,26 @@ __device__ __forceinline__ void arrange_x(const uint32_t xw[8], uint32_t xa[8]) 
 }  // namespace
 
 template <int B, int UPG, int RW, int YDT>
-__global__ void __launch_bounds__(512) gemv_a8_stream(
+__global__ void __launch_bounds__(256) gemv_a8_stream(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
-    int64_t n, int64_t k, const int8_t *__restrict__ x8, const float *__restrict__ dx, void *__restrict__ y) {
+    int n, int k, const int8_t *__restrict__ x8, const float *__restrict__ dx, void *__restrict__ y) {
     constexpr int M = max_code(B);
-    __shared__ float red[8 * RW];
+    __shared__ float red[4 * RW];
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int nwaves = blockDim.x >> 6;
-    const int64_t ntiles = (n + RW - 1) / RW;
-    const int64_t units = k >> 5;
-    const int64_t ncb = (units + 63) >> 6;
-    const int64_t ng = k / (UPG * 32);
-    const int64_t row_words = (k * B) >> 5;
+    const int nwaves = blockDim.x >> 6;  // the host keeps nwaves <= ncb
+    const int ntiles = (n + RW - 1) / RW;
+    const int units = k >> 5;
+    const int ncb = (units + 63) >> 6;
+    const int ng = k / (UPG * 32);
+    const uint32_t row_bytes = uint32_t(k) * B / 8;
+    const auto rc = make_rsrc(codes, uint32_t(n) * row_bytes);
+    const auto rs = make_rsrc(scale, uint32_t(n) * ng * 4u);
+    const auto ra = make_rsrc(a16, uint32_t(n) * ng * 2u);
+    const auto rb = make_rsrc(b16, uint32_t(n) * ng * 2u);
+    const auto rx = make_rsrc(x8, uint32_t(k));
 
     // W4 carrier pairs evaluated by this lane: pair p covers magnitudes 2p, 2p+1.
     // Q lanes of a quad share a group; lane j of them evaluates pairs j, j+Q, ...
@@ -137,31 +143,25 @@ __global__ void __launch_bounds__(512) gemv_a8_stream(
         tp1[j] = float(ip0[j] + 1) / float(M);
     }
 
-    const int64_t my_tiles = blockIdx.x < ntiles ? (ntiles - 1 - blockIdx.x) / gridDim.x + 1 : 0;
-    const int64_t cbw = (ncb - wave + nwaves - 1) / nwaves;
-    const int64_t items = my_tiles * cbw;
-
+    // An item is (row tile, column block).  A workgroup walks the tiles
+    // blockIdx.x + j * gridDim.x; its wave w takes column blocks w, w + nwaves,
+    // ... of each tile.  Rows and lanes past the matrix load an out-of-range
+    // offset and read zeros (zero scale, so they add nothing).
     uint32_t wn[RW][B];
     float sn[RW];
     uint32_t an[RW], bn[RW];
-    auto fetch = [&](int64_t it) {
-        const int64_t tile = blockIdx.x + (it / cbw) * gridDim.x;
-        const int64_t cb = wave + (it % cbw) * nwaves;
-        const int64_t u_raw = cb * 64 + lane;
-        const int64_t u = u_raw < units ? u_raw : units - 1;  // clamped: loads stay valid
-        const int64_t g = u / UPG;
+    auto fetch = [&](int t, int c) {
+        const int u = c * 64 + lane;
 #pragma unroll
         for (int r = 0; r < RW; ++r) {
-            const int64_t row_raw = tile * RW + r;
-            const int64_t row = row_raw < n ? row_raw : n - 1;
-            const uint32_t *wp = reinterpret_cast<const uint32_t *>(codes) + row * row_words + u * B;
-#pragma unroll
-            for (int i = 0; i < B; ++i) wn[r][i] = __builtin_nontemporal_load(wp + i);
-            const int64_t gi = row * ng + g;
-            sn[r] = scale[gi];
+            const int row = t * RW + r;
+            const bool ok = (u < units) && (row < n);
+            const uint32_t gi = uint32_t(row) * ng + uint32_t(u / UPG);
+            load_words<B>(rc, ok ? uint32_t(row) * row_bytes + uint32_t(u) * (4 * B) : kOobOffset, wn[r]);
+            sn[r] = load_f32(rs, ok ? gi * 4u : kOobOffset);
             if constexpr (B == 4) {
-                an[r] = a16[gi];
-                bn[r] = b16[gi];
+                an[r] = load_u16(ra, ok ? gi * 2u : kOobOffset);
+                bn[r] = load_u16(rb, ok ? gi * 2u : kOobOffset);
             }
         }
     };
@@ -169,12 +169,10 @@ __global__ void __launch_bounds__(512) gemv_a8_stream(
     float acc[RW];
 #pragma unroll
     for (int i = 0; i < RW; ++i) acc[i] = 0.f;
-    if (items > 0) fetch(0);
-    for (int64_t it = 0; it < items; ++it) {
-        const int64_t tile = blockIdx.x + (it / cbw) * gridDim.x;
-        const int64_t ci = it % cbw;
-        const int64_t cb = wave + ci * nwaves;
-        const int64_t row0 = tile * RW;
+    int tile = blockIdx.x, cb = wave;
+    bool have = tile < ntiles;
+    if (have) fetch(tile, cb);
+    while (have) {
         uint32_t w[RW][B];
         float s[RW];
         uint32_t av[RW], bv[RW];
@@ -186,16 +184,22 @@ __global__ void __launch_bounds__(512) gemv_a8_stream(
             av[r] = an[r];
             bv[r] = bn[r];
         }
-        if (it + 1 < items) fetch(it + 1);
-        const int64_t u_raw = cb * 64 + lane;
-        const bool live = u_raw < units;
-        const int64_t u = live ? u_raw : units - 1;
+        int cb_next = cb + nwaves, tile_next = tile;
+        const bool last_cb = cb_next >= ncb;
+        if (last_cb) {
+            cb_next = wave;
+            tile_next = tile + int(gridDim.x);
+        }
+        const bool have_next = tile_next < ntiles;
+        if (have_next) fetch(tile_next, cb_next);
 
+        const int u = cb * 64 + lane;
         uint32_t xa[8];
         {
-            const uint4 *xp = reinterpret_cast<const uint4 *>(x8 + u * 32);
-            const uint4 v0 = xp[0], v1 = xp[1];
-            const uint32_t xw[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+            uint32_t xw[8];
+            const uint32_t xo = u < units ? uint32_t(u) * 32u : kOobOffset;
+            load_words<4>(rx, xo, xw);
+            load_words<4>(rx, xo + 16u, xw + 4);
             arrange_x<B>(xw, xa);
         }
 
@@ -248,8 +252,8 @@ __global__ void __launch_bounds__(512) gemv_a8_stream(
                         const uint32_t msk = perm(0u, 0x00008000u, f2[h] & 0x08080808u);
                         const uint32_t pa = perm(ta1, ta0, idx);
                         const uint32_t pb = perm(tb1, tb0, idx);
-                        const uint32_t rc = (msk & pb) | (~msk & pa);
-                        p = __builtin_amdgcn_sdot4(int(rc), int(xa[2 * i + h]), p, false);
+                        const uint32_t rcar = (msk & pb) | (~msk & pa);
+                        p = __builtin_amdgcn_sdot4(int(rcar), int(xa[2 * i + h]), p, false);
                     }
                 }
             } else if constexpr (B == 2) {
@@ -272,29 +276,37 @@ __global__ void __launch_bounds__(512) gemv_a8_stream(
                     p = __builtin_amdgcn_sdot4(int(perm(T, T, sel)), int(xa[sft]), p, false);
                 }
             }
-            const bool rok = live && (row0 + r < n);
-            acc[r] = __builtin_fmaf(rok ? s[r] : 0.f, float(p), acc[r]);
+            acc[r] = __builtin_fmaf(s[r], float(p), acc[r]);
         }
-        if (ci == cbw - 1) {
+        if (last_cb) {
+            const int row0 = tile * RW;
+            const float fac = dx[0] / 127.0f;
+            if (nwaves == 1) {
 #pragma unroll
-            for (int r = 0; r < RW; ++r) {
-                float v = acc[r];
+                for (int r = 0; r < RW; ++r) {
+                    const float v = wave_sum(acc[r]);
+                    acc[r] = 0.f;
+                    if (lane == r && row0 + r < n) store_out<YDT>(y, row0 + r, v * fac);
+                }
+            } else {
 #pragma unroll
-                for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-                if (lane == 0) red[wave * RW + r] = v;
-                acc[r] = 0.f;
-            }
-            __syncthreads();
-            if (wave == 0 && lane < RW) {
-                const int64_t row = row0 + lane;
-                if (row < n) {
+                for (int r = 0; r < RW; ++r) {
+                    const float v = wave_sum(acc[r]);
+                    acc[r] = 0.f;
+                    if (lane == 0) red[wave * RW + r] = v;
+                }
+                __syncthreads();
+                if (wave == 0 && lane < RW && row0 + lane < n) {
                     float v = 0.f;
                     for (int wv = 0; wv < nwaves; ++wv) v += red[wv * RW + lane];
-                    store_out<YDT>(y, row, v * (dx[0] / 127.0f));
+                    store_out<YDT>(y, row0 + lane, v * fac);
                 }
+                __syncthreads();  // red is reused by the next tile
             }
-            __syncthreads();
         }
+        tile = tile_next;
+        cb = cb_next;
+        have = have_next;
     }
 }
 
@@ -308,7 +320,7 @@ static hipError_t a8_stream_launch(const cq_weight &w, const int8_t *x8, const f
     int64_t blocks = int64_t(device_cu_count()) * 64;
     if (blocks > tiles) blocks = tiles;
     hipLaunchKernelGGL((gemv_a8_stream<B, UPG, RW, YDT>), dim3(unsigned(blocks)), dim3(nw * 64), 0, stream, w.codes,
-                       w.scale, w.a, w.b, w.n, w.k, x8, dx, y);
+                       w.scale, w.a, w.b, int(w.n), int(w.k), x8, dx, y);
     return hipGetLastError();
 }
 
@@ -337,7 +349,7 @@ static hipError_t a8_stream_bits(const cq_weight &w, const int8_t *x8, const flo
 }
 
 bool gemv_a8_stream_supported(const cq_weight &w, int64_t m) {
-    return m == 1 && (w.bits == 1 || w.bits == 2 || w.bits == 4);
+    return m == 1 && (w.bits == 1 || w.bits == 2 || w.bits == 4) && stream_fits(w.n, w.k, w.bits, w.group);
 }
 
 hipError_t launch_gemv_a8_stream(const cq_weight &w, const int8_t *x8, const float *dx, void *y, int y_dt,
