@@ -160,6 +160,40 @@ def rows_sweep(torch, cq, bits=4, group=128, k=8192, n=28672, ms=(1, 2, 8, 32, 1
     return {"shape": {"k": k, "n": n, "bits": bits, "group": group}, "rows": out, "a8_faster_from_m": cross}
 
 
+KERNEL_SOURCES = ("paper_2608_06763_amd/csrc/gemv_a16_stream.hip", "paper_2608_06763_amd/csrc/stream_common.h",
+                  "paper_2608_06763_amd/csrc/cq_device.h", "paper_2608_06763_amd/csrc/gemv_a16.hip")
+COUNTERS_FILE = "profiles/gemv_a16_stream_llama8b_decode_m1_counters.txt"
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    summary, or None when that summary was taken on other kernel sources."""
+    path = os.path.join(ROOT, COUNTERS_FILE)
+    if not os.path.exists(path):
+        return None, "no counter summary"
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line:
+                key, val = line.split(":", 1)
+                fields[key.strip()] = val.strip()
+    if fields.get("source_sha256") != kernel_source_hash():
+        return None, "kernel sources changed since the counters were taken"
+    try:
+        return float(fields["traffic_bytes_per_launch"]), "FETCH_SIZE + WRITE_SIZE, copy-calibrated"
+    except (KeyError, ValueError):
+        return None, "counter summary incomplete"
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -167,6 +201,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 256 MiB device copy (reference for HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
@@ -180,57 +217,124 @@ def main():
 
     bits, group, m = 4, 128, 1
     log("[bench] building weights")
-    weights, xs, ys, x8s, dxs, layers_np = [], [], [], [], [], []
+    weights, xs, y16s, y8s, x8s, dxs, layers_np = [], [], [], [], [], [], []
     from workloads import synthetic_representation
     for li, (name, k, n) in enumerate(LLAMA8B_LAYERS):
         codes, s, a, b = synthetic_representation(2000 + li, n, k, bits, group)
         weights.append(cq.CQWeight.from_codes(codes, s, a, b, bits, group))
         xb = llama8b_act(m, k, li)
         xs.append(torch.from_numpy(xb.view(np.int16)).cuda().view(torch.bfloat16))
-        ys.append(torch.empty((m, n), dtype=torch.bfloat16, device="cuda"))
+        y16s.append(torch.empty((m, n), dtype=torch.bfloat16, device="cuda"))
+        y8s.append(torch.empty((m, n), dtype=torch.bfloat16, device="cuda"))
         x8s.append(torch.empty((m, k), dtype=torch.int8, device="cuda"))
         dxs.append(torch.empty((m,), dtype=torch.float32, device="cuda"))
         layers_np.append((name, k, n, codes, s, a, b, bf16_bits_to_f32(xb).astype(np.float64)))
     t_w = sum(weight_bytes(n, k, bits, group) for _, k, n in LLAMA8B_LAYERS)
     copies = rotation(weights, t_w)
+    nl = len(LLAMA8B_LAYERS)
     log(f"[bench] {len(copies)} weight copies x {t_w / 1e6:.1f} MB")
-
-    def step(i):
-        ws = copies[i % len(copies)]
-        for li in range(len(ws)):
-            cq.cq_gemm_model_dtype(ws[li], xs[li], out=ys[li])
-            cq.cq_quantize_act_a8(xs[li], x8s[li], dxs[li])
-            cq.cq_gemm_a8(ws[li], x8s[li], dxs[li], out=ys[li])
 
     bytes_a16 = sum(a16_bytes(m, n, k, bits, group) for _, k, n in LLAMA8B_LAYERS)
     bytes_a8 = sum(a8_bytes(m, n, k, bits, group) for _, k, n in LLAMA8B_LAYERS)
+
+    def step(i, evs=None):
+        ws = copies[i % len(copies)]
+        for li in range(nl):
+            if evs is not None:
+                evs[i * nl + li][0].record()
+            cq.cq_gemm_model_dtype(ws[li], xs[li], out=y16s[li])
+            if evs is not None:
+                evs[i * nl + li][1].record()
+            cq.cq_quantize_act_a8(xs[li], x8s[li], dxs[li])
+            cq.cq_gemm_a8(ws[li], x8s[li], dxs[li], out=y8s[li])
+
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    ms = timed(torch, step, args.steps)
+    # Timed region: K eager steps.  Event pairs around every model-dtype GEMV
+    # launch (the dominant kernel) give its average duration on the launch stream.
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps * nl)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t0.record()
+    for i in range(args.steps):
+        step(i, evs)
+    t1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = t0.elapsed_time(t1) / args.steps
+    gemv_ms = sum(a.elapsed_time(b) for a, b in evs) / len(evs)
     value = (bytes_a16 + bytes_a8) / (ms / 1e3) / 1e9
-    log(f"[bench] step {ms:.4f} ms -> {value:.1f} GB/s effective")
-
-    # per-path and per-kernel timing (dominant kernel: the model-dtype GEMV)
-    nl = len(LLAMA8B_LAYERS)
-    a16_path = lambda i: [cq.cq_gemm_model_dtype(copies[i % len(copies)][li], xs[li], out=ys[li]) for li in range(nl)]
-    a8_path = lambda i: [(cq.cq_quantize_act_a8(xs[li], x8s[li], dxs[li]),
-                          cq.cq_gemm_a8(copies[i % len(copies)][li], x8s[li], dxs[li], out=ys[li])) for li in range(nl)]
-    ms16 = timed(torch, a16_path, args.steps)
-    ms8 = timed(torch, a8_path, args.steps)
-    launches = nl * len(copies) * 4
-    gemv_ms = per_launch_ms(torch, lambda i: cq.cq_gemm_model_dtype(
-        copies[(i // nl) % len(copies)][i % nl], xs[i % nl], out=ys[i % nl]), launches)
-    per_layer = {}
-    for li, (name, k, n) in enumerate(LLAMA8B_LAYERS):
-        t = per_launch_ms(torch, lambda i: cq.cq_gemm_model_dtype(copies[i % len(copies)][li], xs[li], out=ys[li]),
-                          len(copies) * 4)
-        per_layer[name] = {"k": k, "n": n, "us": t * 1e3,
-                           "gbs": a16_bytes(m, n, k, bits, group) / t / 1e6}
+    log(f"[bench] eager step {ms:.4f} ms -> {value:.1f} GB/s effective (wall {wall:.3f} s)")
     achieved = (bytes_a16 / nl) / gemv_ms / 1e6  # average algorithmic bytes per launch / avg duration
     log(f"[bench] model-dtype GEMV avg launch {gemv_ms * 1e3:.2f} us -> {achieved:.1f} GB/s")
 
+    # per-path and per-layer timing (outside the timed region)
+    a16_path = lambda i: [cq.cq_gemm_model_dtype(copies[i % len(copies)][li], xs[li], out=y16s[li])
+                          for li in range(nl)]
+    a8_path = lambda i: [(cq.cq_quantize_act_a8(xs[li], x8s[li], dxs[li]),
+                          cq.cq_gemm_a8(copies[i % len(copies)][li], x8s[li], dxs[li], out=y8s[li]))
+                         for li in range(nl)]
+    ms16 = timed(torch, a16_path, args.steps)
+    ms8 = timed(torch, a8_path, args.steps)
+    per_layer = {}
+    for li, (name, k, n) in enumerate(LLAMA8B_LAYERS):
+        t16 = per_launch_ms(torch, lambda i: cq.cq_gemm_model_dtype(copies[i % len(copies)][li], xs[li],
+                                                                   out=y16s[li]), len(copies) * 4)
+        t8 = per_launch_ms(torch, lambda i: cq.cq_gemm_a8(copies[i % len(copies)][li], x8s[li], dxs[li],
+                                                         out=y8s[li]), len(copies) * 4)
+        per_layer[name] = {"k": k, "n": n, "model_dtype_us": round(t16 * 1e3, 2),
+                           "model_dtype_gbs": round(a16_bytes(m, n, k, bits, group) / t16 / 1e6, 1),
+                           "a8_gemv_us": round(t8 * 1e3, 2),
+                           "a8_gemv_gbs": round(a8_bytes(m, n, k, bits, group) / t8 / 1e6, 1)}
+
+    graph = None
+    if not args.no_graph:
+        # The same step sequence captured once per weight copy into one HIP graph
+        # and replayed; launch gaps between the 12 kernels of a step disappear.
+        ref16 = [y.clone() for y in y16s]
+        ref8 = [y.clone() for y in y8s]
+        g = torch.cuda.CUDAGraph()
+        cs = torch.cuda.Stream()
+        cs.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cs):
+            step(len(copies) - 1)
+        torch.cuda.current_stream().wait_stream(cs)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            for i in range(len(copies)):
+                step(i)
+        reps = max(1, math.ceil(args.steps / len(copies)))
+        for _ in range(2):
+            g.replay()
+        torch.cuda.synchronize()
+        same = all(torch.equal(a, b) for a, b in zip(ref16 + ref8, y16s + y8s))
+        g0 = torch.cuda.Event(enable_timing=True)
+        g1 = torch.cuda.Event(enable_timing=True)
+        g0.record()
+        for _ in range(reps):
+            g.replay()
+        g1.record()
+        g1.synchronize()
+        gms = g0.elapsed_time(g1) / (reps * len(copies))
+        same = same and all(torch.equal(a, b) for a, b in zip(ref16 + ref8, y16s + y8s))
+        graph = {"ms_per_step": round(gms, 5), "gbs": round((bytes_a16 + bytes_a8) / gms / 1e6, 1),
+                 "steps": reps * len(copies), "matches_eager": bool(same)}
+        log(f"[bench] graph step {gms:.4f} ms -> {graph['gbs']:.1f} GB/s (matches eager: {same})")
+        del g
+
+    if args.copy_calibration:
+        src = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("[bench] copy calibration: 3 x 256 MiB device copies")
+
+    traffic, traffic_note = measured_traffic()
     result = {
         "metric": "W4G128 GEMV effective HBM GB/s (M=1) + GEMM TFLOPS/TOPS vs rows M, % roofline",
         "value": round(value, 2),
@@ -242,20 +346,23 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "bf16+int8",
         "data": "synthetic",
         "config": {"workload": "Llama-3-8B-shaped decode layers (QKV 4096x6144, O 4096x4096, gate+up "
                                "4096x28672, down 14336x4096), W4 G128, M=1, bf16 activations; step = "
-                               "model-dtype GEMV + Dynamic-A8 (quantize + GEMV) on all four layers",
+                               "model-dtype GEMV + Dynamic-A8 (quantize + GEMV) on all four layers, eager launches",
                    "bits": bits, "group": group, "m": m, "weight_copies": len(copies),
                    "weight_bytes_per_copy": t_w, "weights": "synthetic packed representation (random codes, "
                    "printed-shape curves); kernel timing is value independent"},
-        "paths": {"model_dtype": {"ms": ms16, "gbs": bytes_a16 / ms16 / 1e6},
-                  "a8": {"ms": ms8, "gbs": bytes_a8 / ms8 / 1e6}},
-        "per_layer_model_dtype": per_layer,
-        "roofline": {"bound": "hbm", "kernel": "model-dtype GEMV (W4 G128, M=1)", "achieved": round(achieved, 1),
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "avg_launch_us": round(gemv_ms * 1e3, 3), "traffic": None},
+        "paths": {"model_dtype": {"ms": round(ms16, 5), "gbs": round(bytes_a16 / ms16 / 1e6, 1)},
+                  "a8": {"ms": round(ms8, 5), "gbs": round(bytes_a8 / ms8 / 1e6, 1)}},
+        "graph": graph,
+        "per_layer": per_layer,
+        "roofline": {"bound": "hbm", "kernel": "gemv_a16_stream (model-dtype GEMV, W4 G128, M=1)",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "avg_launch_us": round(gemv_ms * 1e3, 3),
+                     "bytes_per_launch": round(bytes_a16 / nl, 1), "traffic": traffic,
+                     "traffic_note": traffic_note, "kernel_source_sha256": kernel_source_hash()},
     }
     if not args.no_sweep:
         log("[bench] rows sweep")
