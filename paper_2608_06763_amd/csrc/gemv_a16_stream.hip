@@ -252,13 +252,13 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
         }
         if (last_cb) {
             const int row0 = tile * RW;
+            static_assert(RW == 2, "the output store writes row pairs");
             if (nwaves == 1) {
-#pragma unroll
-                for (int r = 0; r < RW; ++r) {
-                    const float v = wave_sum(acc[r]);
-                    acc[r] = 0.f;
-                    if (lane == r && row0 + r < n) store_out<YDT>(y, row0 + r, v);
-                }
+                const float v0 = wave_sum(acc[0]);
+                const float v1 = wave_sum(acc[1]);
+                acc[0] = 0.f;
+                acc[1] = 0.f;
+                if (lane == 0 && row0 < n) store_row_pair<YDT>(y, row0, v0, v1, row0 + 1 < n);
             } else {
 #pragma unroll
                 for (int r = 0; r < RW; ++r) {
@@ -267,10 +267,13 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                     if (lane == 0) red[wave * RW + r] = v;
                 }
                 __syncthreads();
-                if (wave == 0 && lane < RW && row0 + lane < n) {
-                    float v = 0.f;
-                    for (int wv = 0; wv < nwaves; ++wv) v += red[wv * RW + lane];
-                    store_out<YDT>(y, row0 + lane, v);
+                if (wave == 0 && lane == 0 && row0 < n) {
+                    float v0 = 0.f, v1 = 0.f;
+                    for (int wv = 0; wv < nwaves; ++wv) {
+                        v0 += red[wv * RW];
+                        v1 += red[wv * RW + 1];
+                    }
+                    store_row_pair<YDT>(y, row0, v0, v1, row0 + 1 < n);
                 }
                 __syncthreads();  // red is reused by the next tile
             }

@@ -10,6 +10,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "cq_device.h"
+
 namespace cq {
 
 // Byte offset that lies past the end of every resource used here.
@@ -51,6 +53,31 @@ __device__ __forceinline__ float load_f32(__amdgpu_buffer_rsrc_t r, uint32_t off
 
 __device__ __forceinline__ uint32_t load_u16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     return uint32_t(__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0));
+}
+
+// Store the outputs of two consecutive rows (row0 even, so a bf16/fp16 pair is
+// 4-byte aligned and an FP32 pair 8-byte aligned) with one write; a lone last
+// row is written alone.
+template <int YDT>
+__device__ __forceinline__ void store_row_pair(void *y, int row0, float v0, float v1, bool has1) {
+    if constexpr (YDT == 2) {
+        float *p = static_cast<float *>(y) + row0;
+        if (has1) {
+            typedef float f2_t __attribute__((ext_vector_type(2)));
+            *reinterpret_cast<f2_t *>(p) = f2_t{v0, v1};
+        } else {
+            p[0] = v0;
+        }
+    } else {
+        uint16_t *p = static_cast<uint16_t *>(y) + row0;
+        const uint32_t h0 = YDT == 0 ? f32_to_bf16(v0) : f32_to_f16(v0);
+        if (has1) {
+            const uint32_t h1 = YDT == 0 ? f32_to_bf16(v1) : f32_to_f16(v1);
+            *reinterpret_cast<uint32_t *>(p) = h0 | (h1 << 16);
+        } else {
+            p[0] = uint16_t(h0);
+        }
+    }
 }
 
 // Host check: every buffer a streaming kernel reads (codes, FP32 scales,
