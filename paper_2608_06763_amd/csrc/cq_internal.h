@@ -50,6 +50,11 @@ hipError_t launch_gemv_a8_stream(const cq_weight &w, const int8_t *x8, const flo
 hipError_t launch_gemm_a8(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
                           int32_t *partials, hipStream_t stream);
 
+// Dynamic-A8 many-row GEMM for W4, G >= 64 (tensors below 2 GiB).
+bool gemm_a8_mfma_supported(const cq_weight &w, int64_t m);
+hipError_t launch_gemm_a8_mfma(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
+                               int32_t *partials, hipStream_t stream);
+
 // Largest row count each GEMV family accepts.
 constexpr int64_t kGemvMaxRows = 16;
 

@@ -13,52 +13,20 @@
 // column blocks and meet in LDS, the next item's codes are requested before
 // the current item is decoded).
 //
-// Decode without memory tables.  A W4 field n (two's complement, 8 reserved)
-// selects from two 8-byte carrier tables held in registers:
-//   TA[i] = r(i) for n = i < 8, and TB[i] = -r(8 - i) for n = 8 + i (TB[0] = 0
-//   is the reserved pattern).
-// One v_perm_b32 looks up four fields in a table; a byte mask from bit 3 of each
-// field picks TA or TB per byte, and v_dot4_i32_i8 multiplies the four carriers
-// with four activations.  The carriers of a group are computed once per
-// (row, group): the group's lanes each evaluate two magnitudes and share them
-// through quad DPP moves.  W2 and W1 use constant tables ({0, 127, 0, -127}
-// and {-127, 127}).
-//
-// Exact carriers.  127 q(i/M) is first evaluated in FP32 (Horner, eq.
-// gpu-horner); its rounding error is below 127 * 2^-20 * (|a| + |b| + |c| + 1).
-// Only when the estimate lies closer than that to a half-integer is the
-// carrier recomputed with the exact FP64 residual test, so every carrier equals
-// the RNE of the exact rational value.
+// Decode without memory tables: W4 carriers come from two 8-byte tables held
+// in registers and looked up with byte permutes (a8_carriers.h), multiplied
+// with four activations at a time by v_dot4_i32_i8.  The carriers of a group
+// are computed once per (row, group): the group's lanes each evaluate two
+// magnitudes and share them through quad DPP moves.  W2 and W1 use constant
+// tables ({0, 127, 0, -127} and {-127, 127}).
 #include "cq_device.h"
 #include "cq_internal.h"
 #include "stream_common.h"
+#include "a8_carriers.h"
 
 namespace cq {
 
 namespace {
-
-__device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel) {
-    return __builtin_amdgcn_perm(hi, lo, sel);
-}
-
-// INT8 carrier of magnitude i with t = i / M (exact when close to a tie).
-template <int M>
-__device__ __forceinline__ uint32_t carrier_u8(int i, float t, float a, float b, float c, float margin) {
-    const float f = 127.0f * (t * __builtin_fmaf(t, __builtin_fmaf(t, c, b), a));
-    float r = __builtin_rintf(f);
-    if (__builtin_expect(__builtin_fabsf(f - r) > 0.5f - margin, 0)) {
-        r = float(exact_carrier(i, M, double(a), double(b)));
-    }
-    r = r < 0.f ? 0.f : (r > 127.f ? 127.f : r);
-    return uint32_t(int(r));
-}
-
-// Quad-lane broadcast (DPP quad_perm): every lane reads lane `src` of the
-// lanes {4q, 4q + 1, 4q + 2, 4q + 3} as given by the control pattern.
-template <int CTRL>
-__device__ __forceinline__ uint32_t quad_bcast(uint32_t v) {
-    return uint32_t(__builtin_amdgcn_mov_dpp(int(v), CTRL, 0xf, 0xf, true));
-}
 
 // Byte transpose of a 4 x 4 byte matrix held in four words: out[s] byte b =
 // in[b] byte s.
@@ -210,8 +178,7 @@ __global__ void __launch_bounds__(256) gemv_a8_stream(
                 const float a = f16_to_f32(uint16_t(av[r]));
                 const float b = f16_to_f32(uint16_t(bv[r]));
                 const float c = 1.f - a - b;
-                const float margin =
-                    (__builtin_fabsf(a) + __builtin_fabsf(b) + __builtin_fabsf(c) + 1.f) * (127.0f / 1048576.0f);
+                const float margin = carrier_margin(a, b, c);
                 uint32_t pr[NP];
 #pragma unroll
                 for (int j = 0; j < NP; ++j) {
@@ -235,26 +202,16 @@ __global__ void __launch_bounds__(256) gemv_a8_stream(
                 }
                 const uint32_t ta0 = P[0] | (P[1] << 16);  // r0 r1 r2 r3
                 const uint32_t ta1 = P[2] | (P[3] << 16);  // r4 r5 r6 r7
-                // TB = [0, -r7, -r6, -r5 | -r4, -r3, -r2, -r1]; bytewise negation of
-                // values in [0, 127] without borrows: (0x80 - v) ^ 0x80
-                const uint32_t tbp0 = perm(ta1, ta0, 0x0506070cu);
-                const uint32_t tbp1 = perm(ta1, ta0, 0x01020304u);
-                const uint32_t tb0 = (0x80808080u - tbp0) ^ 0x80808080u;
-                const uint32_t tb1 = (0x80808080u - tbp1) ^ 0x80808080u;
+                uint32_t tb0, tb1;
+                w4_negative_table(ta0, ta1, tb0, tb1);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const uint32_t wd = w[r][i];
                     const uint32_t f2[2] = {wd & 0x0f0f0f0fu, (wd >> 4) & 0x0f0f0f0fu};
 #pragma unroll
-                    for (int h = 0; h < 2; ++h) {
-                        const uint32_t idx = f2[h] & 0x07070707u;
-                        // 0xff in the bytes whose field has bit 3 set (selector 8 = sign of byte 1)
-                        const uint32_t msk = perm(0u, 0x00008000u, f2[h] & 0x08080808u);
-                        const uint32_t pa = perm(ta1, ta0, idx);
-                        const uint32_t pb = perm(tb1, tb0, idx);
-                        const uint32_t rcar = (msk & pb) | (~msk & pa);
-                        p = __builtin_amdgcn_sdot4(int(rcar), int(xa[2 * i + h]), p, false);
-                    }
+                    for (int h = 0; h < 2; ++h)
+                        p = __builtin_amdgcn_sdot4(int(w4_lookup(f2[h], ta0, ta1, tb0, tb1)), int(xa[2 * i + h]), p,
+                                                   false);
                 }
             } else if constexpr (B == 2) {
                 // fields 0 -> 0, 1 -> +127, 2 (reserved) -> 0, 3 -> -127

@@ -343,3 +343,31 @@ def test_a8_near_tie_carriers_exact(torch_dev, bits, family):
     finally:
         cq.cq_set_gemv_max_rows(1, -1)
     assert np.array_equal(_np(y).astype(np.float64), p.sum(axis=-1).astype(np.float64))
+
+
+# ---------------------------------------------------------------- many-row matrix-core GEMMs
+
+
+@pytest.mark.parametrize("bits,group", [(4, 64), (4, 128), (4, 512), (3, 128)])
+@pytest.mark.parametrize("m,n", [(300, 600), (129, 257)])
+def test_gemm_multi_tile(torch_dev, bits, group, m, n):
+    # several row and column tiles with ragged edges; A8 partials bit-exact
+    k = 1024
+    r = fitted(31, n, k, bits, group)
+    xb, xv = act(32, m, k)
+    x8_ref, d_ref, ya_ref, p_ref = ref_a8(xv, r, bits, group)
+    y_ref = ref_model_dtype(xv, r, bits, group)
+    say("gemm_multi_tile", bits, group, m, n)
+    cq = _cq()
+    w = _weight(r, bits, group)
+    x8 = torch_dev.from_numpy(x8_ref).cuda()
+    dx = torch_dev.from_numpy(d_ref).cuda()
+    ya, parts = cq.cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32, want_partials=True)
+    assert np.array_equal(parts.cpu().numpy(), p_ref)
+    assert R.eps_comp(_np(ya), ya_ref, "fp32") <= 1e-5
+    ya16 = cq.cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.bfloat16)
+    assert R.eps_comp(_np(ya16), ya_ref, "bf16") <= TOL
+    ya32 = cq.cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32)
+    assert torch_dev.equal(ya32, ya)
+    y = cq.cq_gemm_model_dtype(w, _x(torch_dev, xb, "bf16"))
+    assert R.eps_comp(_np(y), y_ref, "bf16") <= TOL
