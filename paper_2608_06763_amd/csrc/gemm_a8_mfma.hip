@@ -6,19 +6,21 @@
 // partial is converted to FP32 and multiplied by s_g, and the row factor
 // d_x / 127 multiplies the FP32 sum.
 //
-// Tiling.  A workgroup of 2 x WN waves owns a 128 x (64 WN) tile of y (rows of
-// x by rows of W); each wave owns 64 x 64 and issues v_mfma_i32_16x16x64_i8
+// Tiling.  A workgroup of WM x WN waves owns a (64 WM) x (64 WN) tile of y
+// (rows of x by rows of W; 256 x 128 on the fast path, so that every decoded
+// carrier feeds 256 activation rows); each wave owns 64 x 64 and issues v_mfma_i32_16x16x64_i8
 // on 16 x 16 blocks.  K advances in steps of 64 through two LDS buffers: while
 // the matrix cores work on one buffer, every thread loads the next step's
 // codes and activations, decodes its 32 codes to carriers and writes them to
 // the other buffer, so one barrier per step suffices.
 //
-// Decode.  Thread t serves weight row t / 2 and the 32-code half t % 2 of each
-// step.  At the start of a group the two threads of a row each evaluate three
-// carriers (exact, see a8_carriers.h) and swap them with a DPP move, which
-// gives both the two 8-byte W4 carrier tables of that (row, group); every
-// code word then costs two byte-permute lookups and two permutes that restore
-// field order.
+// Decode.  The WM adjacent threads t of a quad (or half quad) serve weight row
+// t / WM, each one 64 / WM codes of every step.  At the start of a group they
+// each evaluate 8 / WM of the row's carriers (exact, see a8_carriers.h) and
+// share them with DPP quad moves, which gives every one of them the two
+// 8-byte W4 carrier tables of that (row, group); every code word then costs
+// two byte-permute lookups and two permutes that restore field order.  The
+// first MFMA of a group takes a zero accumulator, so partials need no clearing.
 //
 // MFMA operand layout (16x16x64 int8): lane l supplies row l % 16 of A and
 // column l % 16 of B with K slots 16 (l / 16) .. +15; the INT32 result of a
@@ -39,7 +41,6 @@ namespace {
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kTM = 128;               // rows of x per workgroup tile
 constexpr int kKS = 64;                // K step
 constexpr int kStride = kKS + 16;      // LDS bytes per tile row (padded)
 constexpr int kBand = 8;               // row tiles per raster band
@@ -50,20 +51,25 @@ __device__ __forceinline__ void lds_store16(int8_t *p, const uint32_t *v) {
 
 }  // namespace
 
-template <int WN, int UPG, int YDT, bool DUMP>
-__global__ void __launch_bounds__(128 * WN) gemm_a8_w4_mfma(
+template <int WM, int WN, int UPG, int YDT, bool DUMP>
+__global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
     int n, int k, const int8_t *__restrict__ x8, const float *__restrict__ dx, int m,
     void *__restrict__ y, int32_t *__restrict__ partials, int tiles_m, int tiles_n) {
     constexpr int M = 7;
-    constexpr int TN = 64 * WN;
-    constexpr int NT = 128 * WN;            // threads
+    constexpr int TM = 64 * WM;             // rows of x per tile
+    constexpr int TN = 64 * WN;             // rows of W per tile
+    constexpr int NT = 64 * WM * WN;        // threads
     constexpr int G = 32 * UPG;
     constexpr int SPG = G / kKS;            // K steps per group
-    constexpr int XB = kTM * kKS / NT;      // activation bytes per thread per step (32 or 16)
+    constexpr int CPT = kKS / WM;           // codes per thread per step (16 or 32)
+    constexpr int XB = kKS / WN * 1;        // activation bytes per thread per step (32 or 16)
+    constexpr int Q = WM;                   // threads sharing a weight row (2 or 4)
+    constexpr int NP = 4 / Q;               // carrier pairs evaluated per thread
     static_assert(SPG >= 1 && G % kKS == 0, "group must be a multiple of the K step");
-    __shared__ __attribute__((aligned(16))) int8_t As[2][kTM * kStride];
+    static_assert(Q == 2 || Q == 4, "two or four threads per weight row");
+    __shared__ __attribute__((aligned(16))) int8_t As[2][TM * kStride];
     __shared__ __attribute__((aligned(16))) int8_t Bs[2][TN * kStride];
 
     // ---- tile of this workgroup
@@ -74,7 +80,7 @@ __global__ void __launch_bounds__(128 * WN) gemm_a8_w4_mfma(
     const int first_m = band * kBand;
     const int band_rows = min(kBand, tiles_m - first_m);
     const int in_band = wg - band * kBand * tiles_n;
-    const int m0 = (first_m + in_band % band_rows) * kTM;
+    const int m0 = (first_m + in_band % band_rows) * TM;
     const int n0 = (in_band / band_rows) * TN;
 
     const int tid = threadIdx.x;
@@ -91,9 +97,9 @@ __global__ void __launch_bounds__(128 * WN) gemm_a8_w4_mfma(
     const auto rb = make_rsrc(b16, uint32_t(n) * ng * 2u);
     const auto rx = make_rsrc(x8, uint32_t(m) * uint32_t(k));
 
-    // loader roles
-    const int lr = tid >> 1;                 // weight row of the tile
-    const int lh = tid & 1;                  // 32-code half of the step
+    // loader roles: Q adjacent threads (one quad or half quad) share a weight row
+    const int lr = tid / Q;                  // weight row of the tile
+    const int lq = tid % Q;                  // which CPT-code part of the step
     const int wrow = n0 + lr;
     const bool wok = wrow < n;
     const int xr = tid / (kKS / XB);         // activation row of the tile
@@ -101,19 +107,24 @@ __global__ void __launch_bounds__(128 * WN) gemm_a8_w4_mfma(
     const int xrow = m0 + xr;
     const bool xok = xrow < m;
 
-    // carriers this thread evaluates: magnitudes 1..3 (first thread of the row)
-    // or 4..6 (second); r(0) = 0 and r(7) = 127 are fixed
-    const int i0 = 1 + 3 * lh;
-    const float t0 = float(i0) / float(M), t1 = float(i0 + 1) / float(M), t2 = float(i0 + 2) / float(M);
+    // carrier pairs this thread evaluates: pair p covers magnitudes 2p, 2p + 1
+    float tp0[NP], tp1[NP];
+    int ip0[NP];
+#pragma unroll
+    for (int j = 0; j < NP; ++j) {
+        ip0[j] = 2 * (lq + Q * j);
+        tp0[j] = float(ip0[j]) / float(M);
+        tp1[j] = float(ip0[j] + 1) / float(M);
+    }
 
-    uint32_t cw[4];        // codes of the next step
-    uint32_t xw[XB / 4];   // activations of the next step
+    uint32_t cw[CPT / 8];   // codes of the next step
+    uint32_t xw[XB / 4];    // activations of the next step
     uint32_t av = 0, bv = 0;
-    float sj[4], sjn[4];   // group scales of this lane's four output columns
+    float sj[4], sjn[4];    // group scales of this lane's four output columns
 
     auto load_step = [&](int st) {
         const uint32_t kk = uint32_t(st) * kKS;
-        load_words<4>(rc, wok ? uint32_t(wrow) * row_bytes + (kk + 32u * lh) / 2u : kOobOffset, cw);
+        load_words<CPT / 8>(rc, wok ? uint32_t(wrow) * row_bytes + (kk + uint32_t(CPT * lq)) / 2u : kOobOffset, cw);
         load_words<XB / 4>(rx, xok ? uint32_t(xrow) * uint32_t(k) + kk + uint32_t(xc) : kOobOffset, xw);
         if (st % SPG == 0) {
             const int g = st / SPG;
@@ -134,24 +145,34 @@ __global__ void __launch_bounds__(128 * WN) gemm_a8_w4_mfma(
         const float b = f16_to_f32(uint16_t(bv));
         const float c = 1.f - a - b;
         const float mg = carrier_margin(a, b, c);
-        const uint32_t c0 = carrier_u8<M>(i0, t0, a, b, c, mg);
-        const uint32_t c1 = carrier_u8<M>(i0 + 1, t1, a, b, c, mg);
-        const uint32_t c2 = carrier_u8<M>(i0 + 2, t2, a, b, c, mg);
-        const uint32_t own = lh == 0 ? ((c0 << 8) | (c1 << 16) | (c2 << 24))   // r0 r1 r2 r3
-                                     : (c0 | (c1 << 8) | (c2 << 16) | (127u << 24));  // r4 r5 r6 r7
-        const uint32_t other = quad_bcast<0xb1>(own);  // the row's other thread (lane ^ 1)
-        ta0 = lh == 0 ? own : other;
-        ta1 = lh == 0 ? other : own;
+        uint32_t pr[NP];
+#pragma unroll
+        for (int j = 0; j < NP; ++j)
+            pr[j] = carrier_u8<M>(ip0[j], tp0[j], a, b, c, mg) | (carrier_u8<M>(ip0[j] + 1, tp1[j], a, b, c, mg) << 8);
+        uint32_t P[4];
+        if constexpr (Q == 4) {
+            P[0] = quad_bcast<0x00>(pr[0]);
+            P[1] = quad_bcast<0x55>(pr[0]);
+            P[2] = quad_bcast<0xaa>(pr[0]);
+            P[3] = quad_bcast<0xff>(pr[0]);
+        } else {
+            P[0] = quad_bcast<0xa0>(pr[0]);
+            P[1] = quad_bcast<0xf5>(pr[0]);
+            P[2] = quad_bcast<0xa0>(pr[1]);
+            P[3] = quad_bcast<0xf5>(pr[1]);
+        }
+        ta0 = P[0] | (P[1] << 16);  // r0 r1 r2 r3
+        ta1 = P[2] | (P[3] << 16);  // r4 r5 r6 r7
         w4_negative_table(ta0, ta1, tb0, tb1);
     };
 
     auto store_step = [&](int buf) {
-        uint32_t cr[8];
+        uint32_t cr[CPT / 4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) w4_word_carriers(cw[i], ta0, ta1, tb0, tb1, cr[2 * i], cr[2 * i + 1]);
-        int8_t *bp = &Bs[buf][lr * kStride + 32 * lh];
-        lds_store16(bp, cr);
-        lds_store16(bp + 16, cr + 4);
+        for (int i = 0; i < CPT / 8; ++i) w4_word_carriers(cw[i], ta0, ta1, tb0, tb1, cr[2 * i], cr[2 * i + 1]);
+        int8_t *bp = &Bs[buf][lr * kStride + CPT * lq];
+#pragma unroll
+        for (int q = 0; q < CPT / 16; ++q) lds_store16(bp + 16 * q, cr + 4 * q);
         int8_t *ap = &As[buf][xr * kStride + xc];
 #pragma unroll
         for (int q = 0; q < XB / 16; ++q) lds_store16(ap + 16 * q, xw + 4 * q);
@@ -162,11 +183,9 @@ __global__ void __launch_bounds__(128 * WN) gemm_a8_w4_mfma(
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            acc[i][j] = i32x4{0, 0, 0, 0};
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
             for (int e = 0; e < 4; ++e) accf[i][j][e] = 0.f;
-        }
 
     const int nsteps = k / kKS;
     load_step(0);
@@ -188,11 +207,25 @@ __global__ void __launch_bounds__(128 * WN) gemm_a8_w4_mfma(
 #pragma unroll
         for (int j = 0; j < 4; ++j)
             bf[j] = *reinterpret_cast<const i32x4 *>(&Bs[buf][(wn + 16 * j + (lane & 15)) * kStride + 16 * (lane >> 4)]);
+        if (st % SPG == 0) {
+            // first step of a group: the partials start from zero
+            const i32x4 zero = {0, 0, 0, 0};
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bf[j], acc[i][j], 0, 0, 0);
+                for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bf[j], zero, 0, 0, 0);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bf[j], acc[i][j], 0, 0, 0);
+        }
 
+        if (more) {
+            if ((st + 1) % SPG == 0) build_tables();
+            store_step(buf ^ 1);
+        }
         if (st % SPG == SPG - 1) {
             // group complete: FP32 rescale of the exact partials
             const int g = st / SPG;
@@ -218,15 +251,7 @@ __global__ void __launch_bounds__(128 * WN) gemm_a8_w4_mfma(
                     }
             }
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = i32x4{0, 0, 0, 0};
-#pragma unroll
             for (int j = 0; j < 4; ++j) sj[j] = sjn[j];
-        }
-        if (more) {
-            if ((st + 1) % SPG == 0) build_tables();
-            store_step(buf ^ 1);
         }
         __syncthreads();
     }
@@ -246,14 +271,14 @@ __global__ void __launch_bounds__(128 * WN) gemm_a8_w4_mfma(
         }
 }
 
-template <int WN, int UPG, int YDT, bool DUMP>
+template <int WM, int WN, int UPG, int YDT, bool DUMP>
 static hipError_t a8_mfma_launch(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
                                  int32_t *partials, hipStream_t stream) {
-    const int tiles_m = int((m + kTM - 1) / kTM);
+    const int tiles_m = int((m + 64 * WM - 1) / (64 * WM));
     const int tiles_n = int((w.n + 64 * WN - 1) / (64 * WN));
     const int64_t nwg = int64_t(tiles_m) * tiles_n;
     if (nwg > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((gemm_a8_w4_mfma<WN, UPG, YDT, DUMP>), dim3(unsigned(nwg)), dim3(128 * WN), 0, stream, w.codes,
+    hipLaunchKernelGGL((gemm_a8_w4_mfma<WM, WN, UPG, YDT, DUMP>), dim3(unsigned(nwg)), dim3(64 * WM * WN), 0, stream, w.codes,
                        w.scale, w.a, w.b, int(w.n), int(w.k), x8, dx, int(m), y, partials, tiles_m, tiles_n);
     return hipGetLastError();
 }
@@ -265,18 +290,18 @@ static hipError_t a8_mfma_group(const cq_weight &w, const int8_t *x8, const floa
     // leaves room for its extra registers; the fast path runs eight.
     if (partials) {
         switch (w.group) {
-            case 64: return a8_mfma_launch<2, 2, YDT, true>(w, x8, dx, m, y, partials, stream);
-            case 128: return a8_mfma_launch<2, 4, YDT, true>(w, x8, dx, m, y, partials, stream);
-            case 256: return a8_mfma_launch<2, 8, YDT, true>(w, x8, dx, m, y, partials, stream);
-            case 512: return a8_mfma_launch<2, 16, YDT, true>(w, x8, dx, m, y, partials, stream);
+            case 64: return a8_mfma_launch<2, 2, 2, YDT, true>(w, x8, dx, m, y, partials, stream);
+            case 128: return a8_mfma_launch<2, 2, 4, YDT, true>(w, x8, dx, m, y, partials, stream);
+            case 256: return a8_mfma_launch<2, 2, 8, YDT, true>(w, x8, dx, m, y, partials, stream);
+            case 512: return a8_mfma_launch<2, 2, 16, YDT, true>(w, x8, dx, m, y, partials, stream);
         }
         return hipErrorNotSupported;
     }
     switch (w.group) {
-        case 64: return a8_mfma_launch<4, 2, YDT, false>(w, x8, dx, m, y, partials, stream);
-        case 128: return a8_mfma_launch<4, 4, YDT, false>(w, x8, dx, m, y, partials, stream);
-        case 256: return a8_mfma_launch<4, 8, YDT, false>(w, x8, dx, m, y, partials, stream);
-        case 512: return a8_mfma_launch<4, 16, YDT, false>(w, x8, dx, m, y, partials, stream);
+        case 64: return a8_mfma_launch<4, 2, 2, YDT, false>(w, x8, dx, m, y, partials, stream);
+        case 128: return a8_mfma_launch<4, 2, 4, YDT, false>(w, x8, dx, m, y, partials, stream);
+        case 256: return a8_mfma_launch<4, 2, 8, YDT, false>(w, x8, dx, m, y, partials, stream);
+        case 512: return a8_mfma_launch<4, 2, 16, YDT, false>(w, x8, dx, m, y, partials, stream);
     }
     return hipErrorNotSupported;
 }
