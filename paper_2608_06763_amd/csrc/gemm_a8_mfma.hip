@@ -12,7 +12,9 @@
 // on 16 x 16 blocks.  K advances in steps of 64 through two LDS buffers: while
 // the matrix cores work on one buffer, every thread loads the next step's
 // codes and activations, decodes its 32 codes to carriers and writes them to
-// the other buffer, so one barrier per step suffices.
+// the other buffer, so one barrier per step suffices.  Codes and activations are
+// requested two steps ahead into two register slots (the step loop is
+// unrolled by two so that slots are fixed registers).
 //
 // Decode.  The WM adjacent threads t of a quad (or half quad) serve weight row
 // t / WM, each one 64 / WM codes of every step.  At the start of a group they
@@ -33,6 +35,8 @@
 #include "cq_internal.h"
 #include "stream_common.h"
 #include "a8_carriers.h"
+
+#include <type_traits>
 
 namespace cq {
 
@@ -117,32 +121,38 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
         tp1[j] = float(ip0[j] + 1) / float(M);
     }
 
-    uint32_t cw[CPT / 8];   // codes of the next step
-    uint32_t xw[XB / 4];    // activations of the next step
-    uint32_t av = 0, bv = 0;
+    // Two register slots: step s is loaded into slot s % 2 two steps before it
+    // is decoded, so a load has a whole step of matrix work to arrive.
+    uint32_t cw[2][CPT / 8];
+    uint32_t xw[2][XB / 4];
+    uint32_t av[2] = {0, 0}, bv[2] = {0, 0};
     float sj[4], sjn[4];    // group scales of this lane's four output columns
 
-    auto load_step = [&](int st) {
+    auto load_step = [&](int st, auto slot_c) {
+        constexpr int SL = decltype(slot_c)::value;
         const uint32_t kk = uint32_t(st) * kKS;
-        load_words<CPT / 8>(rc, wok ? uint32_t(wrow) * row_bytes + (kk + uint32_t(CPT * lq)) / 2u : kOobOffset, cw);
-        load_words<XB / 4>(rx, xok ? uint32_t(xrow) * uint32_t(k) + kk + uint32_t(xc) : kOobOffset, xw);
+        load_words<CPT / 8>(rc, wok ? uint32_t(wrow) * row_bytes + (kk + uint32_t(CPT * lq)) / 2u : kOobOffset,
+                            cw[SL]);
+        load_words<XB / 4>(rx, xok ? uint32_t(xrow) * uint32_t(k) + kk + uint32_t(xc) : kOobOffset, xw[SL]);
         if (st % SPG == 0) {
-            const int g = st / SPG;
-            const uint32_t gi = uint32_t(wrow) * ng + g;
-            av = load_u16(ra, wok ? gi * 2u : kOobOffset);
-            bv = load_u16(rb, wok ? gi * 2u : kOobOffset);
+            const uint32_t gi = uint32_t(wrow) * ng + st / SPG;
+            av[SL] = load_u16(ra, wok ? gi * 2u : kOobOffset);
+            bv[SL] = load_u16(rb, wok ? gi * 2u : kOobOffset);
+        }
+    };
+    auto load_scales = [&](int g) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int col = n0 + wn + 16 * j + (lane & 15);
-                sjn[j] = load_f32(rs, col < n ? (uint32_t(col) * ng + g) * 4u : kOobOffset);
-            }
+        for (int j = 0; j < 4; ++j) {
+            const int col = n0 + wn + 16 * j + (lane & 15);
+            sjn[j] = load_f32(rs, col < n ? (uint32_t(col) * ng + g) * 4u : kOobOffset);
         }
     };
 
     uint32_t ta0 = 0, ta1 = 0, tb0 = 0, tb1 = 0;
-    auto build_tables = [&]() {
-        const float a = f16_to_f32(uint16_t(av));
-        const float b = f16_to_f32(uint16_t(bv));
+    auto build_tables = [&](auto slot_c) {
+        constexpr int SL = decltype(slot_c)::value;
+        const float a = f16_to_f32(uint16_t(av[SL]));
+        const float b = f16_to_f32(uint16_t(bv[SL]));
         const float c = 1.f - a - b;
         const float mg = carrier_margin(a, b, c);
         uint32_t pr[NP];
@@ -166,16 +176,17 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
         w4_negative_table(ta0, ta1, tb0, tb1);
     };
 
-    auto store_step = [&](int buf) {
+    auto store_step = [&](int buf, auto slot_c) {
+        constexpr int SL = decltype(slot_c)::value;
         uint32_t cr[CPT / 4];
 #pragma unroll
-        for (int i = 0; i < CPT / 8; ++i) w4_word_carriers(cw[i], ta0, ta1, tb0, tb1, cr[2 * i], cr[2 * i + 1]);
+        for (int i = 0; i < CPT / 8; ++i) w4_word_carriers(cw[SL][i], ta0, ta1, tb0, tb1, cr[2 * i], cr[2 * i + 1]);
         int8_t *bp = &Bs[buf][lr * kStride + CPT * lq];
 #pragma unroll
         for (int q = 0; q < CPT / 16; ++q) lds_store16(bp + 16 * q, cr + 4 * q);
         int8_t *ap = &As[buf][xr * kStride + xc];
 #pragma unroll
-        for (int q = 0; q < XB / 16; ++q) lds_store16(ap + 16 * q, xw + 4 * q);
+        for (int q = 0; q < XB / 16; ++q) lds_store16(ap + 16 * q, xw[SL] + 4 * q);
     };
 
     i32x4 acc[4][4];
@@ -187,19 +198,26 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
 #pragma unroll
             for (int e = 0; e < 4; ++e) accf[i][j][e] = 0.f;
 
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
     const int nsteps = k / kKS;
-    load_step(0);
-    build_tables();
+    load_step(0, S0{});
+    if (nsteps > 1) load_step(1, S1{});
+    load_scales(0);
+    build_tables(S0{});
 #pragma unroll
     for (int j = 0; j < 4; ++j) sj[j] = sjn[j];
-    store_step(0);
+    store_step(0, S0{});
     __syncthreads();
 
-    for (int st = 0; st < nsteps; ++st) {
+    // One K step: matrix work on LDS buffer st % 2, then decode step st + 1
+    // (register slot SN) into the other buffer and request step st + 2 into
+    // the slot just freed.
+    auto do_step = [&](int st, auto sn_c) {
+        constexpr int SN = decltype(sn_c)::value;  // slot of step st + 1
         const int buf = st & 1;
-        const bool more = st + 1 < nsteps;
-        if (more) load_step(st + 1);
-
+        // slot 1 - SN held step st, decoded during the previous step
+        if (st + 2 < nsteps) load_step(st + 2, std::integral_constant<int, 1 - SN>{});
         i32x4 af[4], bf[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -221,10 +239,12 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
                 for (int j = 0; j < 4; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bf[j], acc[i][j], 0, 0, 0);
         }
-
-        if (more) {
-            if ((st + 1) % SPG == 0) build_tables();
-            store_step(buf ^ 1);
+        if (st + 1 < nsteps) {
+            if ((st + 1) % SPG == 0) {
+                build_tables(sn_c);
+                load_scales((st + 1) / SPG);
+            }
+            store_step(buf ^ 1, sn_c);
         }
         if (st % SPG == SPG - 1) {
             // group complete: FP32 rescale of the exact partials
@@ -254,6 +274,11 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
             for (int j = 0; j < 4; ++j) sj[j] = sjn[j];
         }
         __syncthreads();
+    };
+
+    for (int st = 0; st < nsteps; st += 2) {
+        do_step(st, S1{});
+        if (st + 1 < nsteps) do_step(st + 1, S0{});
     }
 
 #pragma unroll
