@@ -33,6 +33,11 @@ hipError_t launch_gemv_a16_lut(const cq_weight &w, const void *x, int x_dt, int6
 hipError_t launch_gemm_a16(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                            hipStream_t stream);
 
+// Model-dtype many-row GEMM for B <= 5 (tensors below 2 GiB).
+bool gemm_a16_mfma_supported(const cq_weight &w, int64_t m);
+hipError_t launch_gemm_a16_mfma(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                                hipStream_t stream);
+
 // Dynamic-A8 activation quantizer.
 hipError_t launch_quant_a8(const void *x, int x_dt, int64_t m, int64_t k, int8_t *x8, float *dx,
                            hipStream_t stream);

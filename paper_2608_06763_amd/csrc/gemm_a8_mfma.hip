@@ -29,8 +29,9 @@
 // block has lane l holding rows 4 (l / 16) + i of column l % 16.
 //
 // Tile order: workgroups are first spread so that those on one XCD (blockIdx
-// modulo 8) take consecutive tile indices, then tiles are walked in bands of
-// 8 row tiles so that neighbouring workgroups share weight tiles in cache.
+// modulo 8) take consecutive tile indices; consecutive indices then walk the
+// weight tiles of one activation tile, which stays in that XCD's L2 while the
+// packed weights stream past it.
 #include "cq_device.h"
 #include "cq_internal.h"
 #include "stream_common.h"
@@ -47,7 +48,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kKS = 64;                // K step
 constexpr int kStride = kKS + 16;      // LDS bytes per tile row (padded)
-constexpr int kBand = 8;               // row tiles per raster band
+constexpr int kBand = 1;               // row tiles per raster band
 
 __device__ __forceinline__ void lds_store16(int8_t *p, const uint32_t *v) {
     *reinterpret_cast<u32x4 *>(p) = u32x4{v[0], v[1], v[2], v[3]};
