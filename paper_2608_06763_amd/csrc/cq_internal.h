@@ -29,6 +29,14 @@ bool gemv_a16_lut_supported(const cq_weight &w, int64_t m);
 hipError_t launch_gemv_a16_lut(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                                hipStream_t stream);
 
+// Narrow-row (2 <= m <= 16) matrix-core products; see gemv_narrow.hip.
+bool gemv_a16_narrow_supported(const cq_weight &w, int64_t m);
+hipError_t launch_gemv_a16_narrow(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                                  hipStream_t stream);
+bool gemv_a8_narrow_supported(const cq_weight &w, int64_t m);
+hipError_t launch_gemv_a8_narrow(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
+                                 hipStream_t stream);
+
 // Model-dtype tiled matrix-core GEMM family.
 hipError_t launch_gemm_a16(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                            hipStream_t stream);

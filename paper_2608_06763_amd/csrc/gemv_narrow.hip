@@ -1,0 +1,345 @@
+// Narrow-row products (2 <= m <= 16) on gfx950 matrix cores, both paths.
+//
+// With m <= 16 activation rows every group is a dense m x G x 16 contraction
+// for 16 weight rows, so the narrow-row regime (Sec. 5.3 and 5.4) maps onto
+// 16 x 16 MFMA blocks whose weight operand is decoded straight into registers:
+// no LDS staging of decoded weights, and the decode cost per weight does not
+// depend on m.
+//
+// Work mapping.  A workgroup of four waves owns a strip of 16 weight rows; its
+// waves take the groups of K round-robin and add their 16 x 16 FP32 partial
+// tiles through LDS at the end.  In a wave, lane l serves weight row l % 16
+// (the MFMA column) and K slots 16 (l / 16) .. +15 of a 64-slot step (A8) or
+// 8 (l / 16) .. +7 of a 32-slot step (model dtype).  Activation rows past m
+// and weight rows past n load out-of-range offsets and read zeros.
+//
+// Dynamic-A8 (eq. a8-output), W4, G >= 64: each lane decodes its 16 codes to
+// exact INT8 carriers with the register tables of a8_carriers.h (the four
+// lanes of a row each evaluate two of the row's carriers and gather the rest
+// with ds_bpermute); v_mfma_i32_16x16x64_i8 accumulates exact INT32 group
+// partials, which are scaled by s_g in FP32 at the end of each group.
+//
+// Model dtype (Sec. 5.3), B <= 5: the four lanes of a row build the row's
+// table of the 2^B levels s_g sign(k) q(|k|/M) for each group in LDS, each an
+// unevaluated hi + lo pair in the activation dtype (16 or 22 significant bits,
+// so the products keep the FP32 quality of the narrow-row tactic); every code
+// costs one LDS read and both halves feed v_mfma_f32_16x16x32_{bf16,f16}.
+#include "cq_device.h"
+#include "cq_internal.h"
+#include "stream_common.h"
+#include "a8_carriers.h"
+
+namespace cq {
+
+namespace {
+
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+
+constexpr int kWaves = 4;
+
+__device__ __forceinline__ uint32_t lane_read(uint32_t v, int src_lane) {
+    return uint32_t(__builtin_amdgcn_ds_bpermute(src_lane << 2, int(v)));
+}
+
+__device__ __forceinline__ void wave_lds_order() {
+    __asm__ __volatile__("" ::: "memory");
+    __builtin_amdgcn_wave_barrier();
+}
+
+// Sum the waves' 16 x 16 tiles (lane l holds rows 4 (l / 16) + i, column
+// l % 16) and store rows < m of the 16-row strip.
+template <int YDT>
+__device__ __forceinline__ void reduce_store(float (*red)[16][17], const float v[4], int lane, int wave, int n0, int n,
+                                             int m, const float *row_factor, void *y) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red[wave][4 * (lane >> 4) + i][lane & 15] = v[i];
+    __syncthreads();
+    for (int e = threadIdx.x; e < 256; e += blockDim.x) {
+        const int r = e >> 4, c = e & 15;
+        if (r < m && n0 + c < n) {
+            float s = 0.f;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) s += red[w][r][c];
+            if (row_factor) s *= row_factor[r];
+            store_out<YDT>(y, int64_t(r) * n + n0 + c, s);
+        }
+    }
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- Dynamic-A8, W4
+
+template <int UPG, int YDT>
+__global__ void __launch_bounds__(256) gemv_a8_narrow(
+    const uint8_t *__restrict__ codes, const float *__restrict__ scale,
+    const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
+    int n, int k, const int8_t *__restrict__ x8, const float *__restrict__ dx, int m, void *__restrict__ y) {
+    constexpr int M = 7;
+    constexpr int SPG = UPG / 2;  // 64-slot steps per group
+    __shared__ float red[kWaves][16][17];
+    __shared__ float fac[16];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int n0 = blockIdx.x * 16;
+    const int col = lane & 15;     // weight row of the strip / activation row
+    const int part = lane >> 4;    // K part of a step
+    const int wrow = n0 + col;
+    const bool wok = wrow < n;
+    const bool xok = col < m;
+    const int ng = k / (32 * UPG);
+    const uint32_t row_bytes = uint32_t(k) / 2u;
+    const auto rc = make_rsrc(codes, uint32_t(n) * row_bytes);
+    const auto rs = make_rsrc(scale, uint32_t(n) * ng * 4u);
+    const auto ra = make_rsrc(a16, uint32_t(n) * ng * 2u);
+    const auto rb = make_rsrc(b16, uint32_t(n) * ng * 2u);
+    const auto rx = make_rsrc(x8, uint32_t(m) * uint32_t(k));
+    if (threadIdx.x < 16) fac[threadIdx.x] = threadIdx.x < m ? dx[threadIdx.x] / 127.0f : 0.f;
+
+    // carriers of pair `part` of the row: magnitudes 2 part, 2 part + 1
+    const int i0 = 2 * part;
+    const float t0 = float(i0) / float(M), t1 = float(i0 + 1) / float(M);
+
+    float accf[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int g = wave; g < ng; g += kWaves) {
+        const uint32_t gi = uint32_t(wrow) * ng + g;
+        const float s = load_f32(rs, wok ? gi * 4u : kOobOffset);
+        const float a = f16_to_f32(uint16_t(load_u16(ra, wok ? gi * 2u : kOobOffset)));
+        const float b = f16_to_f32(uint16_t(load_u16(rb, wok ? gi * 2u : kOobOffset)));
+        uint32_t cw[SPG][2];
+        u32x4_t xa[SPG];
+#pragma unroll
+        for (int q = 0; q < SPG; ++q) {
+            const uint32_t kk = uint32_t(g) * (32u * UPG) + 64u * q + 16u * part;
+            load_words<2>(rc, wok ? uint32_t(wrow) * row_bytes + kk / 2u : kOobOffset, cw[q]);
+            uint32_t xv[4];
+            load_words<4>(rx, xok ? uint32_t(col) * uint32_t(k) + kk : kOobOffset, xv);
+            xa[q] = u32x4_t{xv[0], xv[1], xv[2], xv[3]};
+        }
+        const float c = 1.f - a - b;
+        const float mg = carrier_margin(a, b, c);
+        const uint32_t pr = carrier_u8<M>(i0, t0, a, b, c, mg) | (carrier_u8<M>(i0 + 1, t1, a, b, c, mg) << 8);
+        const uint32_t p0 = lane_read(pr, col), p1 = lane_read(pr, col + 16);
+        const uint32_t p2 = lane_read(pr, col + 32), p3 = lane_read(pr, col + 48);
+        const uint32_t ta0 = p0 | (p1 << 16), ta1 = p2 | (p3 << 16);
+        uint32_t tb0, tb1;
+        w4_negative_table(ta0, ta1, tb0, tb1);
+        i32x4_t acc = {0, 0, 0, 0};
+#pragma unroll
+        for (int q = 0; q < SPG; ++q) {
+            uint32_t cr[4];
+            w4_word_carriers(cw[q][0], ta0, ta1, tb0, tb1, cr[0], cr[1]);
+            w4_word_carriers(cw[q][1], ta0, ta1, tb0, tb1, cr[2], cr[3]);
+            const i32x4_t bop = {int(cr[0]), int(cr[1]), int(cr[2]), int(cr[3])};
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4_t, xa[q]), bop, acc, 0, 0, 0);
+        }
+        // rows of acc are activation rows, its column this lane's weight row
+#pragma unroll
+        for (int i = 0; i < 4; ++i) accf[i] = __builtin_fmaf(s, float(acc[i]), accf[i]);
+    }
+    // the scale loaded above is this lane's column (weight row), so the
+    // rescale above is s_{n,g} P_g for output (row 4 part + i, column col)
+    reduce_store<YDT>(red, accf, lane, wave, n0, n, m, fac, y);
+}
+
+// ---------------------------------------------------------------- model dtype, B <= 5
+
+template <int B, int UPG, int XDT, int YDT>
+__global__ void __launch_bounds__(256) gemv_a16_narrow(
+    const uint8_t *__restrict__ codes, const float *__restrict__ scale,
+    const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
+    int n, int k, const uint16_t *__restrict__ x, int m, void *__restrict__ y) {
+    constexpr int M = max_code(B);
+    constexpr int NE = 1 << B;
+    constexpr int EPT = NE >= 4 ? NE / 4 : 1;
+    constexpr int TSTR = NE + 1;
+    __shared__ float red[kWaves][16][17];
+    __shared__ uint32_t tab[kWaves][16 * TSTR];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int n0 = blockIdx.x * 16;
+    const int col = lane & 15;
+    const int part = lane >> 4;
+    const int wrow = n0 + col;
+    const bool wok = wrow < n;
+    const bool xok = col < m;
+    const int ng = k / (32 * UPG);
+    const uint32_t row_bytes = uint32_t(k) * B / 8u;
+    const auto rc = make_rsrc(codes, uint32_t(n) * row_bytes);
+    const auto rs = make_rsrc(scale, uint32_t(n) * ng * 4u);
+    const auto ra = make_rsrc(a16, uint32_t(n) * ng * 2u);
+    const auto rb = make_rsrc(b16, uint32_t(n) * ng * 2u);
+    const auto rx = make_rsrc(x, uint32_t(m) * uint32_t(k) * 2u);
+    uint32_t *mytab = tab[wave] + col * TSTR;
+
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    for (int g = wave; g < ng; g += kWaves) {
+        const uint32_t gi = uint32_t(wrow) * ng + g;
+        const float s = load_f32(rs, wok ? gi * 4u : kOobOffset);
+        float a = 1.f, b = 0.f;
+        if constexpr (B >= 3) {
+            a = f16_to_f32(uint16_t(load_u16(ra, wok ? gi * 2u : kOobOffset)));
+            b = f16_to_f32(uint16_t(load_u16(rb, wok ? gi * 2u : kOobOffset)));
+        }
+        // the row's level table: lane part of the row writes fields part, part + 4, ...
+        const float c = 1.f - a - b;
+        wave_lds_order();  // the previous group's reads are issued
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+            const int f = part + 4 * e;
+            if (f < NE) {
+                const int kc = field_to_code(uint32_t(f), B);
+                const float v = s * ((B == 1) ? float(kc) : signed_level(kc, M, a, b, c));
+                uint32_t ent;
+                if constexpr (XDT == 0) {
+                    const __bf16 hi = __bf16(v);
+                    const __bf16 lo = __bf16(v - float(hi));
+                    ent = uint32_t(__builtin_bit_cast(uint16_t, hi)) | (uint32_t(__builtin_bit_cast(uint16_t, lo)) << 16);
+                } else {
+                    const _Float16 hi = _Float16(v);
+                    const _Float16 lo = _Float16(v - float(hi));
+                    ent = uint32_t(__builtin_bit_cast(uint16_t, hi)) | (uint32_t(__builtin_bit_cast(uint16_t, lo)) << 16);
+                }
+                mytab[f] = ent;
+            }
+        }
+        wave_lds_order();
+        // units of the group in batches of at most four (registers)
+        constexpr int QB = UPG < 4 ? UPG : 4;
+        for (int q0 = 0; q0 < UPG; q0 += QB) {
+            uint32_t cw[QB][B];
+            u32x4_t xa[QB];
+#pragma unroll
+            for (int q = 0; q < QB; ++q) {
+                const uint32_t u = uint32_t(g) * UPG + q0 + q;  // unit index along K
+                load_words<B>(rc, wok ? uint32_t(wrow) * row_bytes + u * (4u * B) : kOobOffset, cw[q]);
+                uint32_t xv[4];
+                load_words<4>(rx, xok ? (uint32_t(col) * uint32_t(k) + u * 32u + 8u * part) * 2u : kOobOffset, xv);
+                xa[q] = u32x4_t{xv[0], xv[1], xv[2], xv[3]};
+            }
+#pragma unroll
+            for (int q = 0; q < QB; ++q) {
+                uint32_t ent[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int i = 8 * part + e;
+                    const int bit = i * B;
+                    const int wd = bit >> 5, sh = bit & 31;
+                    uint32_t v;
+                    if (sh + B <= 32) v = cw[q][wd] >> sh;
+                    else v = __builtin_amdgcn_alignbit(cw[q][wd + 1], cw[q][wd], sh);
+                    ent[e] = mytab[v & uint32_t(NE - 1)];
+                }
+                u32x4_t hi, lo;
+#pragma unroll
+                for (int p = 0; p < 4; ++p) {
+                    hi[p] = __builtin_amdgcn_perm(ent[2 * p + 1], ent[2 * p], 0x05040100u);
+                    lo[p] = __builtin_amdgcn_perm(ent[2 * p + 1], ent[2 * p], 0x07060302u);
+                }
+                if constexpr (XDT == 0) {
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xa[q]),
+                                                                  __builtin_bit_cast(bf16x8_t, hi), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xa[q]),
+                                                                  __builtin_bit_cast(bf16x8_t, lo), acc, 0, 0, 0);
+                } else {
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xa[q]),
+                                                                 __builtin_bit_cast(f16x8_t, hi), acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xa[q]),
+                                                                 __builtin_bit_cast(f16x8_t, lo), acc, 0, 0, 0);
+                }
+            }
+        }
+    }
+    const float v[4] = {acc[0], acc[1], acc[2], acc[3]};
+    reduce_store<YDT>(red, v, lane, wave, n0, n, m, nullptr, y);
+}
+
+// ---------------------------------------------------------------- launchers
+
+template <int UPG, int YDT>
+static hipError_t a8_narrow_launch(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
+                                   hipStream_t stream) {
+    const int64_t blocks = (w.n + 15) / 16;
+    hipLaunchKernelGGL((gemv_a8_narrow<UPG, YDT>), dim3(unsigned(blocks)), dim3(256), 0, stream, w.codes, w.scale, w.a,
+                       w.b, int(w.n), int(w.k), x8, dx, int(m), y);
+    return hipGetLastError();
+}
+
+template <int YDT>
+static hipError_t a8_narrow_group(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
+                                  hipStream_t stream) {
+    switch (w.group) {
+        case 64: return a8_narrow_launch<2, YDT>(w, x8, dx, m, y, stream);
+        case 128: return a8_narrow_launch<4, YDT>(w, x8, dx, m, y, stream);
+        case 256: return a8_narrow_launch<8, YDT>(w, x8, dx, m, y, stream);
+        case 512: return a8_narrow_launch<16, YDT>(w, x8, dx, m, y, stream);
+    }
+    return hipErrorNotSupported;
+}
+
+bool gemv_a8_narrow_supported(const cq_weight &w, int64_t m) {
+    return m >= 2 && m <= 16 && w.bits == 4 && w.group >= 64 && stream_fits(w.n, w.k, w.bits, w.group) &&
+           m * w.k < (int64_t(1) << 31);
+}
+
+hipError_t launch_gemv_a8_narrow(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
+                                 hipStream_t stream) {
+    if (y_dt == 0) return a8_narrow_group<0>(w, x8, dx, m, y, stream);
+    if (y_dt == 1) return a8_narrow_group<1>(w, x8, dx, m, y, stream);
+    return a8_narrow_group<2>(w, x8, dx, m, y, stream);
+}
+
+template <int B, int UPG, int XDT, int YDT>
+static hipError_t a16_narrow_launch(const cq_weight &w, const void *x, int64_t m, void *y, hipStream_t stream) {
+    const int64_t blocks = (w.n + 15) / 16;
+    hipLaunchKernelGGL((gemv_a16_narrow<B, UPG, XDT, YDT>), dim3(unsigned(blocks)), dim3(256), 0, stream, w.codes,
+                       w.scale, w.a, w.b, int(w.n), int(w.k), static_cast<const uint16_t *>(x), int(m), y);
+    return hipGetLastError();
+}
+
+template <int B, int XDT, int YDT>
+static hipError_t a16_narrow_group(const cq_weight &w, const void *x, int64_t m, void *y, hipStream_t stream) {
+    switch (w.group) {
+        case 32: return a16_narrow_launch<B, 1, XDT, YDT>(w, x, m, y, stream);
+        case 64: return a16_narrow_launch<B, 2, XDT, YDT>(w, x, m, y, stream);
+        case 128: return a16_narrow_launch<B, 4, XDT, YDT>(w, x, m, y, stream);
+        case 256: return a16_narrow_launch<B, 8, XDT, YDT>(w, x, m, y, stream);
+        case 512: return a16_narrow_launch<B, 16, XDT, YDT>(w, x, m, y, stream);
+    }
+    return hipErrorNotSupported;
+}
+
+template <int XDT, int YDT>
+static hipError_t a16_narrow_bits(const cq_weight &w, const void *x, int64_t m, void *y, hipStream_t stream) {
+    switch (w.bits) {
+        case 1: return a16_narrow_group<1, XDT, YDT>(w, x, m, y, stream);
+        case 2: return a16_narrow_group<2, XDT, YDT>(w, x, m, y, stream);
+        case 3: return a16_narrow_group<3, XDT, YDT>(w, x, m, y, stream);
+        case 4: return a16_narrow_group<4, XDT, YDT>(w, x, m, y, stream);
+        case 5: return a16_narrow_group<5, XDT, YDT>(w, x, m, y, stream);
+    }
+    return hipErrorNotSupported;
+}
+
+bool gemv_a16_narrow_supported(const cq_weight &w, int64_t m) {
+    return m >= 2 && m <= 16 && w.bits <= 5 && stream_fits(w.n, w.k, w.bits, w.group) &&
+           m * w.k * 2 < (int64_t(1) << 31);
+}
+
+hipError_t launch_gemv_a16_narrow(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                                  hipStream_t stream) {
+    if (x_dt == 0) {
+        if (y_dt == 0) return a16_narrow_bits<0, 0>(w, x, m, y, stream);
+        return a16_narrow_bits<0, 2>(w, x, m, y, stream);
+    }
+    if (y_dt == 1) return a16_narrow_bits<1, 1>(w, x, m, y, stream);
+    return a16_narrow_bits<1, 2>(w, x, m, y, stream);
+}
+
+}  // namespace cq

@@ -371,3 +371,32 @@ def test_gemm_multi_tile(torch_dev, bits, group, m, n):
     assert torch_dev.equal(ya32, ya)
     y = cq.cq_gemm_model_dtype(w, _x(torch_dev, xb, "bf16"))
     assert R.eps_comp(_np(y), y_ref, "bf16") <= TOL
+
+
+# ---------------------------------------------------------------- narrow rows (2 <= m <= 16), matrix cores
+
+
+@pytest.mark.parametrize("group", [64, 128, 256, 512])
+@pytest.mark.parametrize("m", [2, 7, 16])
+def test_narrow_rows_both_paths(torch_dev, group, m):
+    # 75 weight rows (ragged 16-row strip), K = 2560: group counts not a
+    # multiple of the four waves that share a strip
+    k = 2560 if 2560 % group == 0 else 2048
+    r = fitted(41, 75, k, 4, group)
+    xb, xv = act(42 + m, m, k)
+    x8_ref, d_ref, ya_ref, _ = ref_a8(xv, r, 4, group)
+    y_ref = ref_model_dtype(xv, r, 4, group)
+    say("narrow", group, m, k)
+    cq = _cq()
+    w = _weight(r, 4, group)
+    x8 = torch_dev.from_numpy(x8_ref).cuda()
+    dx = torch_dev.from_numpy(d_ref).cuda()
+    ya = cq.cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32)
+    assert R.eps_comp(_np(ya), ya_ref, "fp32") <= 1e-5
+    for dtype in ("bf16", "fp16"):
+        xb2, xv2 = act(42 + m, m, k, dtype)
+        y2_ref = ref_model_dtype(xv2, r, 4, group)
+        y = cq.cq_gemm_model_dtype(w, _x(torch_dev, xb2, dtype), y_dtype=torch_dev.float32)
+        assert R.eps_comp(_np(y), y2_ref, "fp32") <= 2e-4
+        y16 = cq.cq_gemm_model_dtype(w, _x(torch_dev, xb2, dtype))
+        assert R.eps_comp(_np(y16), y2_ref, dtype) <= TOL
