@@ -67,7 +67,7 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int nwaves = blockDim.x >> 6;  // the host keeps nwaves <= ncb
-    float *red = tab + nwaves * NT * 64;
+    float *red = tab + nwaves * RW * NT * 64;
     const int ntiles = (n + RW - 1) / RW;
     const int units = k >> 5;
     const int ncb = (units + 63) >> 6;
@@ -79,10 +79,11 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
     const auto rb = make_rsrc(b16, uint32_t(n) * ng * 2u);
     const auto rx = make_rsrc(x, uint32_t(k) * 2u);
     const uint32_t tbase = uint32_t(uintptr_t((lds_f *)tab));
-    const uint32_t col = tbase + uint32_t(wave) * (NT * 256u) + uint32_t(lane) * 4u;
+    // one table per (wave, row of the tile): slot index wave * RW + r
+    const uint32_t col = tbase + uint32_t(wave * RW) * (NT * 256u) + uint32_t(lane) * 4u;
     // first column of this lane's group inside the wave (the group's UPG lanes are adjacent)
-    const uint32_t gcol = tbase + uint32_t(wave) * (NT * 256u) + uint32_t(lane - lane % UPG) * 4u;
-    const uint32_t wtag = uint32_t(wave) * 0x10101010u;
+    const uint32_t gcol = tbase + uint32_t(wave * RW) * (NT * 256u) + uint32_t(lane - lane % UPG) * 4u;
+    const uint32_t wtag = uint32_t(wave * RW) * 0x10101010u;
 
     // magnitudes this lane evaluates for its group's table, and their t = i/M
     constexpr int MPL = (B == 1) ? 1 : (M + 1 + UPG - 1) / UPG;
@@ -160,7 +161,10 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                 }
             }
         }
-        // ---- decode row by row
+        // ---- level tables of all rows of the tile first (one slot per row), so
+        // that the LDS writes of one row overlap the reads of the previous one
+        float al_r[RW], be_r[RW], ga_r[RW];
+        if constexpr (LUT) wave_lds_fence();  // the previous item's reads are issued
 #pragma unroll
         for (int r = 0; r < RW; ++r) {
             float a = 1.f, b = 0.f;
@@ -169,12 +173,15 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                 b = f16_to_f32(uint16_t(bv[r]));
             }
             const float cc = 1.f - a - b;
+            al_r[r] = a * (1.0f / float(M));
+            be_r[r] = b * (1.0f / float(M * M));
+            ga_r[r] = cc * (1.0f / float(M * M * M));
             if constexpr (LUT) {
                 // Lane j of a group evaluates magnitudes j, j + UPG, ... (their t = i/M
                 // are per-lane constants) and stores +q at field i and -q at field
                 // NT - i into the table columns of all UPG lanes of the group; the lane
                 // holding magnitude 0 also clears the reserved field NT/2.
-                wave_lds_fence();  // the previous row's reads are issued
+                const uint32_t gslot = gcol + uint32_t(r) * (NT * 256u);
 #pragma unroll
                 for (int t = 0; t < MPL; ++t) {
                     if (mag[t] <= M) {
@@ -185,8 +192,8 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                             q = tq[t] * __builtin_fmaf(tq[t], __builtin_fmaf(tq[t], cc, b), a);
                             q = mag[t] == M ? 1.f : q;
                         }
-                        const uint32_t up = gcol + uint32_t(B == 1 ? 1 : mag[t]) * 256u;
-                        const uint32_t um = gcol + uint32_t(mag[t] == 0 ? NT / 2 : (B == 1 ? 0 : NT - mag[t])) * 256u;
+                        const uint32_t up = gslot + uint32_t(B == 1 ? 1 : mag[t]) * 256u;
+                        const uint32_t um = gslot + uint32_t(mag[t] == 0 ? NT / 2 : (B == 1 ? 0 : NT - mag[t])) * 256u;
                         const float qm = mag[t] == 0 ? 0.f : -q;
                         if constexpr (UPG % 4 == 0) {
 #pragma unroll
@@ -203,24 +210,28 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                         }
                     }
                 }
-                wave_lds_fence();
             }
-            const float al = a * (1.0f / float(M));
-            const float be = b * (1.0f / float(M * M));
-            const float ga = cc * (1.0f / float(M * M * M));
+        }
+        if constexpr (LUT) wave_lds_fence();
+        // ---- decode row by row
+#pragma unroll
+        for (int r = 0; r < RW; ++r) {
+            const uint32_t colr = col + uint32_t(r) * (NT * 256u);
+            const uint32_t wtagr = wtag + uint32_t(r) * 0x10101010u;
+            const float al = al_r[r], be = be_r[r], ga = ga_r[r];
             float p0 = 0.f, p1 = 0.f;
 #pragma unroll
             for (int i8 = 0; i8 < 4; ++i8) {
                 float lv[8];
                 if constexpr (B == 4) {
                     const uint32_t wd = w[r][i8];
-                    const uint32_t ev = (wd & 0x0f0f0f0fu) | wtag;
-                    const uint32_t od = ((wd >> 4) & 0x0f0f0f0fu) | wtag;
+                    const uint32_t ev = (wd & 0x0f0f0f0fu) | wtagr;
+                    const uint32_t od = ((wd >> 4) & 0x0f0f0f0fu) | wtagr;
 #pragma unroll
                     for (int jj = 0; jj < 4; ++jj) {
                         const uint32_t sel = 0x03020000u | (uint32_t(4 + jj) << 8);
-                        lv[2 * jj] = lds_ld(__builtin_amdgcn_perm(ev, col, sel));
-                        lv[2 * jj + 1] = lds_ld(__builtin_amdgcn_perm(od, col, sel));
+                        lv[2 * jj] = lds_ld(__builtin_amdgcn_perm(ev, colr, sel));
+                        lv[2 * jj + 1] = lds_ld(__builtin_amdgcn_perm(od, colr, sel));
                     }
                 } else {
 #pragma unroll
@@ -232,7 +243,7 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                         if (sh + B <= 32) v = w[r][wd] >> sh;
                         else v = __builtin_amdgcn_alignbit(w[r][wd + 1], w[r][wd], sh);
                         if constexpr (LUT) {
-                            lv[e] = lds_ld(((v & uint32_t(NT - 1)) << 8) + col);
+                            lv[e] = lds_ld(((v & uint32_t(NT - 1)) << 8) + colr);
                         } else {
                             const int kk = __builtin_amdgcn_sbfe(int(v), 0, B);
                             const float kf = float(kk);
@@ -288,12 +299,12 @@ template <int B, int UPG, int RW, int XDT, int YDT>
 static hipError_t stream_waves(const cq_weight &w, const void *x, void *y, hipStream_t stream) {
     const int64_t ncb = ((w.k >> 5) + 63) >> 6;
     constexpr int NT = B <= 5 ? (1 << B) : 1;
-    constexpr int kMaxW = NT >= 32 ? 4 : 8;  // keep the tables within 32 KB
+    constexpr int kMaxW = NT >= 32 ? 2 : 4;  // keep the tables within 32 KB and the W4 slot tag in 4 bits
     // Two waves split the column blocks of a tile; more waves per workgroup
     // only add tile-reduction cost (measured on Llama-3-8B layer shapes).
     int nw = ncb >= 2 ? 2 : 1;
     if (nw > kMaxW) nw = kMaxW;
-    const size_t lds = sizeof(float) * (size_t(nw) * NT * 64 + size_t(nw) * RW);
+    const size_t lds = sizeof(float) * (size_t(nw) * RW * NT * 64 + size_t(nw) * RW);
     const int64_t tiles = (w.n + RW - 1) / RW;
     // one workgroup per tile up to 64 per CU; the kernel strides over the rest
     int64_t blocks = int64_t(device_cu_count()) * 64;
