@@ -1,0 +1,176 @@
+"""GPU parity at the full workload sizes, on sampled outputs.
+
+The library runs each configuration at its real shape, in the launch
+configuration the benchmark times (same entry points, same dispatch); the
+oracle recomputes a seeded sample of output rows (weight rows decoded in
+float64, A8 carriers from exact rationals) and the sampled outputs must meet
+the same bars as the small parity tests: eps_comp <= 2e-3 for bf16 outputs,
+1e-5 for FP32 outputs of the FP32-product paths, and bit-exact INT32 group
+partials where they are dumped.
+"""
+import functools
+
+import numpy as np
+import pytest
+
+from oracle import a8 as A8
+from oracle import ref as R
+from tests._cases import say
+from workloads import (LLAMA8B_LAYERS, PREFILL70B_SHAPES, bf16_bits_to_f32, crossover_act, gemv_4k, llama8b_act,
+                       prefill70b_act, sweep_act, synthetic_representation)
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-3
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    import paper_2608_06763_amd as cq
+    cq.lib()
+    return torch
+
+
+def _cq():
+    import paper_2608_06763_amd as cq
+    return cq
+
+
+def _dev_x(torch, bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
+
+
+@functools.lru_cache(maxsize=2)
+def _synthetic(seed, n, k, bits, group):
+    """Seeded packed representation, uploaded once per module run."""
+    codes, s, a, b = synthetic_representation(seed, n, k, bits, group)
+    return codes, s, a, b, _cq().CQWeight.from_codes(codes, s, a, b, bits, group)
+
+
+def _sample(seed, count, total):
+    return np.sort(np.random.default_rng(seed).choice(total, size=min(count, total), replace=False))
+
+
+def _ref_rows(xv, codes, s, a, b, bits, group, rows):
+    """Oracle model-dtype outputs y[:, rows] (float64)."""
+    return R.gemm_model_dtype(xv, codes[rows], bits, group, s[rows], a[rows], b[rows])
+
+
+def _ref_a8_rows(x8, dx, codes, s, a, b, bits, group, rows):
+    y, p = A8.gemm_a8(x8, dx, codes[rows], bits, group, s[rows], a[rows], b[rows])
+    return y, p
+
+
+def _eps(got, ref, dtype):
+    return R.eps_comp(np.asarray(got, np.float64), ref, dtype)
+
+
+def _check_both_paths(torch, w, xb, codes, s, a, b, bits, group, rows, tag, xrows=None):
+    """Run both entry points at full size; compare sampled columns (and
+    sampled activation rows when xrows is given) with the oracle."""
+    cq = _cq()
+    xs = bf16_bits_to_f32(xb if xrows is None else xb[xrows]).astype(np.float64)
+    x = _dev_x(torch, xb)
+    say(tag, "model-dtype")
+    y = cq.cq_gemm_model_dtype(w, x).float().cpu().numpy()
+    y_ref = _ref_rows(xs, codes, s, a, b, bits, group, rows)
+    got = y[:, rows] if xrows is None else y[xrows][:, rows]
+    assert _eps(got, y_ref, "bf16") <= TOL
+    say(tag, "a8")
+    x8, dx = cq.cq_quantize_act_a8(x)
+    x8_ref, d_ref = A8.quantize_act(xs)
+    x8_got = x8.cpu().numpy() if xrows is None else x8.cpu().numpy()[xrows]
+    d_got = dx.cpu().numpy() if xrows is None else dx.cpu().numpy()[xrows]
+    assert np.array_equal(x8_got, x8_ref)
+    assert np.array_equal(d_got, d_ref.astype(np.float32))
+    ya = cq.cq_gemm_a8(w, x8, dx, y_dtype=torch.float32).cpu().numpy()
+    ya_ref, _ = _ref_a8_rows(x8_ref, d_ref, codes, s, a, b, bits, group, rows)
+    gota = ya[:, rows] if xrows is None else ya[xrows][:, rows]
+    assert _eps(gota, ya_ref, "fp32") <= 1e-5
+
+
+def test_fullsize_single_gemv_fitted(torch_dev):
+    # W4 G128, M = 1, K = N = 4096, weights fitted by the oracle; every output
+    x_bits, w = gemv_4k()
+    from oracle import fit as FIT
+    say("fullsize gemv_4k fit")
+    r = FIT.fit(w, 4, 128)
+    cq = _cq()
+    wt = cq.CQWeight.from_codes(r.codes, r.scale, r.a_bits, r.b_bits, 4, 128)
+    _check_both_paths(torch_dev, wt, x_bits, r.codes, r.scale, r.a_bits, r.b_bits, 4, 128,
+                      np.arange(4096), "gemv_4k")
+
+
+@pytest.mark.parametrize("m", [1, 4, 16])
+@pytest.mark.parametrize("layer", range(4))
+def test_fullsize_llama8b_decode_layers(torch_dev, layer, m):
+    # the benchmark's layers and weights (same seeds), 96 sampled output rows
+    name, k, n = LLAMA8B_LAYERS[layer]
+    codes, s, a, b = synthetic_representation(2000 + layer, n, k, 4, 128)
+    w = _cq().CQWeight.from_codes(codes, s, a, b, 4, 128)
+    xb = llama8b_act(m, k, layer)
+    rows = _sample(7 + layer, 96, n)
+    _check_both_paths(torch_dev, w, xb, codes, s, a, b, 4, 128, rows, f"llama8b {name} m={m}")
+
+
+@pytest.mark.parametrize("m", [1, 2, 8, 32, 128, 512, 2048, 8192])
+def test_fullsize_crossover_shape(torch_dev, m):
+    # K = 8192, N = 28672, W4 G128 at every row count of the crossover sweep;
+    # 48 sampled weight rows x (all or 24 sampled) activation rows
+    k, n = 8192, 28672
+    codes, s, a, b, w = _synthetic(4001, n, k, 4, 128)
+    xb = crossover_act(m, k)
+    rows = _sample(11, 48, n)
+    xrows = None if m <= 32 else _sample(12, 24, m)
+    _check_both_paths(torch_dev, w, xb, codes, s, a, b, 4, 128, rows, f"crossover m={m}", xrows)
+
+
+@pytest.mark.parametrize("bits", [1, 2, 3, 4, 6, 8])
+@pytest.mark.parametrize("group", [32, 64, 128, 256])
+def test_fullsize_width_group_sweep(torch_dev, bits, group):
+    # M = 1, K = N = 8192 for every B x G of the sweep; 32 sampled rows
+    k = n = 8192
+    codes, s, a, b = synthetic_representation(5000 + 10 * bits + group // 32, n, k, bits, group)
+    w = _cq().CQWeight.from_codes(codes, s, a, b, bits, group)
+    xb = sweep_act(k)
+    rows = _sample(13, 32, n)
+    _check_both_paths(torch_dev, w, xb, codes, s, a, b, bits, group, rows, f"sweep B={bits} G={group}")
+
+
+@pytest.mark.parametrize("m", [2048, 8192])
+@pytest.mark.parametrize("bits", [3, 4])
+@pytest.mark.parametrize("shape", range(3))
+def test_fullsize_prefill70b(torch_dev, shape, bits, m):
+    # 70B-class prefill GEMMs, W3 and W4 G128; 16 x 24 sampled outputs
+    k, n = PREFILL70B_SHAPES[shape]
+    codes, s, a, b, w = _synthetic(6000 + 10 * shape + bits, n, k, bits, 128)
+    xb = prefill70b_act(m, k)
+    rows = _sample(17, 16, n)
+    xrows = _sample(18, 24, m)
+    _check_both_paths(torch_dev, w, xb, codes, s, a, b, bits, 128, rows, f"prefill70b {k}x{n} m={m} B={bits}",
+                      xrows)
+
+
+def test_fullsize_fitted_slice_partials(torch_dev):
+    # oracle-fitted Laplace-with-outliers weights at a full decode-layer width
+    # (K = 14336), 64 rows: INT32 group partials of both matrix-core families
+    # compared bit for bit
+    from workloads import llama8b_weight
+    w_full = llama8b_weight(3, 14336, 64)
+    say("fitted slice K=14336 fit")
+    from oracle import fit as FIT
+    r = FIT.fit(w_full, 4, 128)
+    cq = _cq()
+    wt = cq.CQWeight.from_codes(r.codes, r.scale, r.a_bits, r.b_bits, 4, 128)
+    for m in (1, 16, 300):
+        xb = llama8b_act(m, 14336, 9)
+        xv = bf16_bits_to_f32(xb).astype(np.float64)
+        x8_ref, d_ref = A8.quantize_act(xv)
+        _, p_ref = A8.gemm_a8(x8_ref, d_ref, r.codes, 4, 128, r.scale, r.a_bits, r.b_bits)
+        say("fitted slice partials m=", m)
+        x8 = torch_dev.from_numpy(x8_ref).cuda()
+        dx = torch_dev.from_numpy(d_ref).cuda()
+        _, parts = cq.cq_gemm_a8(wt, x8, dx, y_dtype=torch_dev.float32, want_partials=True)
+        assert np.array_equal(parts.cpu().numpy(), p_ref)
