@@ -275,7 +275,9 @@ static hipError_t a8_stream_launch(const cq_weight &w, const int8_t *x8, const f
                                    hipStream_t stream) {
     constexpr int RW = 2;
     const int64_t ncb = ((w.k >> 5) + 63) >> 6;
-    const int nw = ncb >= 2 ? 2 : 1;
+    // up to two column blocks a single wave per tile is fastest (no LDS
+    // reduction); longer rows split their column blocks over two waves
+    const int nw = ncb > 2 ? 2 : 1;
     const int64_t tiles = (w.n + RW - 1) / RW;
     int64_t blocks = int64_t(device_cu_count()) * 64;
     if (blocks > tiles) blocks = tiles;
