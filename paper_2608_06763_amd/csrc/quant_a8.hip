@@ -104,7 +104,7 @@ template <int XDT>
 static hipError_t quant_launch(const void *x, int64_t m, int64_t k, int8_t *x8, float *dx, hipStream_t stream) {
     const int64_t per_thread = ((k >> 3) + 255) / 256;
     const uint16_t *xp = static_cast<const uint16_t *>(x);
-    const dim3 grid(unsigned(m)), block(256);
+    const dim3 grid(static_cast<uint32_t>(m)), block(256);
     if (per_thread <= 1) hipLaunchKernelGGL((quant_a8_kernel<XDT, 1>), grid, block, 0, stream, xp, k, x8, dx);
     else if (per_thread <= 2) hipLaunchKernelGGL((quant_a8_kernel<XDT, 2>), grid, block, 0, stream, xp, k, x8, dx);
     else if (per_thread <= 4) hipLaunchKernelGGL((quant_a8_kernel<XDT, 4>), grid, block, 0, stream, xp, k, x8, dx);
