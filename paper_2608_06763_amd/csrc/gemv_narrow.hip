@@ -6,9 +6,10 @@
 // no LDS staging of decoded weights, and the decode cost per weight does not
 // depend on m.
 //
-// Work mapping.  A workgroup of four waves owns a strip of 16 weight rows; its
-// waves take the groups of K round-robin and add their 16 x 16 FP32 partial
-// tiles through LDS at the end.  In a wave, lane l serves weight row l % 16
+// Work mapping.  A workgroup owns a strip of 16 weight rows; its 4..16 waves
+// (chosen by the host so that the grid holds about eight waves per SIMD) take
+// the groups of K round-robin and add their 16 x 16 FP32 partial tiles
+// through LDS at the end.  In a wave, lane l serves weight row l % 16
 // (the MFMA column) and K slots 16 (l / 16) .. +15 of a 64-slot step (A8) or
 // 8 (l / 16) .. +7 of a 32-slot step (model dtype).  Activation rows past m
 // and weight rows past n load out-of-range offsets and read zeros.
@@ -39,7 +40,7 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 
-constexpr int kWaves = 4;
+constexpr int kMaxWaves = 16;  // waves per workgroup (one 16-row strip), chosen by the host
 
 __device__ __forceinline__ uint32_t lane_read(uint32_t v, int src_lane) {
     return uint32_t(__builtin_amdgcn_ds_bpermute(src_lane << 2, int(v)));
@@ -53,8 +54,8 @@ __device__ __forceinline__ void wave_lds_order() {
 // Sum the waves' 16 x 16 tiles (lane l holds rows 4 (l / 16) + i, column
 // l % 16) and store rows < m of the 16-row strip.
 template <int YDT>
-__device__ __forceinline__ void reduce_store(float (*red)[16][17], const float v[4], int lane, int wave, int n0, int n,
-                                             int m, const float *row_factor, void *y) {
+__device__ __forceinline__ void reduce_store(float (*red)[16][17], const float v[4], int lane, int wave, int nwaves,
+                                             int n0, int n, int m, const float *row_factor, void *y) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) red[wave][4 * (lane >> 4) + i][lane & 15] = v[i];
     __syncthreads();
@@ -62,8 +63,7 @@ __device__ __forceinline__ void reduce_store(float (*red)[16][17], const float v
         const int r = e >> 4, c = e & 15;
         if (r < m && n0 + c < n) {
             float s = 0.f;
-#pragma unroll
-            for (int w = 0; w < kWaves; ++w) s += red[w][r][c];
+            for (int w = 0; w < nwaves; ++w) s += red[w][r][c];
             if (row_factor) s *= row_factor[r];
             store_out<YDT>(y, int64_t(r) * n + n0 + c, s);
         }
@@ -75,17 +75,18 @@ __device__ __forceinline__ void reduce_store(float (*red)[16][17], const float v
 // ---------------------------------------------------------------- Dynamic-A8, W4
 
 template <int UPG, int YDT>
-__global__ void __launch_bounds__(256) gemv_a8_narrow(
+__global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
     int n, int k, const int8_t *__restrict__ x8, const float *__restrict__ dx, int m, void *__restrict__ y) {
     constexpr int M = 7;
     constexpr int SPG = UPG / 2;  // 64-slot steps per group
-    __shared__ float red[kWaves][16][17];
+    __shared__ float red[kMaxWaves][16][17];
     __shared__ float fac[16];
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
+    const int nwaves = blockDim.x >> 6;
     const int n0 = blockIdx.x * 16;
     const int col = lane & 15;     // weight row of the strip / activation row
     const int part = lane >> 4;    // K part of a step
@@ -105,22 +106,31 @@ __global__ void __launch_bounds__(256) gemv_a8_narrow(
     const int i0 = 2 * part;
     const float t0 = float(i0) / float(M), t1 = float(i0 + 1) / float(M);
 
-    float accf[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int g = wave; g < ng; g += kWaves) {
-        const uint32_t gi = uint32_t(wrow) * ng + g;
-        const float s = load_f32(rs, wok ? gi * 4u : kOobOffset);
-        const float a = f16_to_f32(uint16_t(load_u16(ra, wok ? gi * 2u : kOobOffset)));
-        const float b = f16_to_f32(uint16_t(load_u16(rb, wok ? gi * 2u : kOobOffset)));
+    // A wave walks its groups g = wave, wave + 4, ...; the codes, activations
+    // and metadata of its next group are requested before the current group is
+    // decoded (two register stages, the loop unrolled by two).
+    struct Stage {
         uint32_t cw[SPG][2];
         u32x4_t xa[SPG];
+        float s, a, b;
+    };
+    auto load = [&](int g, Stage &st) {
+        const uint32_t gi = uint32_t(wrow) * ng + g;
+        st.s = load_f32(rs, wok ? gi * 4u : kOobOffset);
+        st.a = f16_to_f32(uint16_t(load_u16(ra, wok ? gi * 2u : kOobOffset)));
+        st.b = f16_to_f32(uint16_t(load_u16(rb, wok ? gi * 2u : kOobOffset)));
 #pragma unroll
         for (int q = 0; q < SPG; ++q) {
             const uint32_t kk = uint32_t(g) * (32u * UPG) + 64u * q + 16u * part;
-            load_words<2>(rc, wok ? uint32_t(wrow) * row_bytes + kk / 2u : kOobOffset, cw[q]);
+            load_words<2>(rc, wok ? uint32_t(wrow) * row_bytes + kk / 2u : kOobOffset, st.cw[q]);
             uint32_t xv[4];
             load_words<4>(rx, xok ? uint32_t(col) * uint32_t(k) + kk : kOobOffset, xv);
-            xa[q] = u32x4_t{xv[0], xv[1], xv[2], xv[3]};
+            st.xa[q] = u32x4_t{xv[0], xv[1], xv[2], xv[3]};
         }
+    };
+    float accf[4] = {0.f, 0.f, 0.f, 0.f};
+    auto process = [&](const Stage &st) {
+        const float a = st.a, b = st.b;
         const float c = 1.f - a - b;
         const float mg = carrier_margin(a, b, c);
         const uint32_t pr = carrier_u8<M>(i0, t0, a, b, c, mg) | (carrier_u8<M>(i0 + 1, t1, a, b, c, mg) << 8);
@@ -133,24 +143,37 @@ __global__ void __launch_bounds__(256) gemv_a8_narrow(
 #pragma unroll
         for (int q = 0; q < SPG; ++q) {
             uint32_t cr[4];
-            w4_word_carriers(cw[q][0], ta0, ta1, tb0, tb1, cr[0], cr[1]);
-            w4_word_carriers(cw[q][1], ta0, ta1, tb0, tb1, cr[2], cr[3]);
+            w4_word_carriers(st.cw[q][0], ta0, ta1, tb0, tb1, cr[0], cr[1]);
+            w4_word_carriers(st.cw[q][1], ta0, ta1, tb0, tb1, cr[2], cr[3]);
             const i32x4_t bop = {int(cr[0]), int(cr[1]), int(cr[2]), int(cr[3])};
-            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4_t, xa[q]), bop, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4_t, st.xa[q]), bop, acc, 0, 0, 0);
         }
         // rows of acc are activation rows, its column this lane's weight row
 #pragma unroll
-        for (int i = 0; i < 4; ++i) accf[i] = __builtin_fmaf(s, float(acc[i]), accf[i]);
+        for (int i = 0; i < 4; ++i) accf[i] = __builtin_fmaf(st.s, float(acc[i]), accf[i]);
+    };
+    Stage s0, s1;
+    int g = wave;
+    if (g < ng) load(g, s0);
+    while (g < ng) {
+        const int g1 = g + nwaves;
+        if (g1 < ng) load(g1, s1);
+        process(s0);
+        if (g1 >= ng) break;
+        const int g2 = g1 + nwaves;
+        if (g2 < ng) load(g2, s0);
+        process(s1);
+        g = g2;
     }
     // the scale loaded above is this lane's column (weight row), so the
     // rescale above is s_{n,g} P_g for output (row 4 part + i, column col)
-    reduce_store<YDT>(red, accf, lane, wave, n0, n, m, fac, y);
+    reduce_store<YDT>(red, accf, lane, wave, nwaves, n0, n, m, fac, y);
 }
 
 // ---------------------------------------------------------------- model dtype, B <= 5
 
 template <int B, int UPG, int XDT, int YDT>
-__global__ void __launch_bounds__(256) gemv_a16_narrow(
+__global__ void __launch_bounds__(1024) gemv_a16_narrow(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
     int n, int k, const uint16_t *__restrict__ x, int m, void *__restrict__ y) {
@@ -158,11 +181,12 @@ __global__ void __launch_bounds__(256) gemv_a16_narrow(
     constexpr int NE = 1 << B;
     constexpr int EPT = NE >= 4 ? NE / 4 : 1;
     constexpr int TSTR = NE + 1;
-    __shared__ float red[kWaves][16][17];
-    __shared__ uint32_t tab[kWaves][16 * TSTR];
+    __shared__ float red[kMaxWaves][16][17];
+    __shared__ uint32_t tab[kMaxWaves][16 * TSTR];
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
+    const int nwaves = blockDim.x >> 6;
     const int n0 = blockIdx.x * 16;
     const int col = lane & 15;
     const int part = lane >> 4;
@@ -178,95 +202,141 @@ __global__ void __launch_bounds__(256) gemv_a16_narrow(
     const auto rx = make_rsrc(x, uint32_t(m) * uint32_t(k) * 2u);
     uint32_t *mytab = tab[wave] + col * TSTR;
 
+    // Items are (group, batch of at most four units); a wave walks the items
+    // of its groups g = wave, wave + 4, ... and requests the next item's codes,
+    // activations and metadata before decoding the current one (two register
+    // stages, the loop unrolled by two).
+    constexpr int QB = UPG < 4 ? UPG : 4;   // units per item
+    constexpr int NB = UPG / QB;            // items per group
+    // The 8 codes of this lane in a unit are the B bytes at byte B * part of
+    // the unit; an aligned 8-byte window holds them (B <= 5), so each unit
+    // costs one 64-bit load and the fields come out with 64-bit shifts.
+    struct Stage {
+        uint32_t cw[QB][2];
+        u32x4_t xa[QB];
+        float s, a, b;
+    };
+    const uint32_t part_byte = uint32_t(B * part);
+    const uint32_t win_shift = 8u * (part_byte & 3u);   // bit of the first field in the window
+    const int my_groups = wave < ng ? (ng - 1 - wave) / nwaves + 1 : 0;
+    const int items = my_groups * NB;
+    auto load = [&](int it, Stage &st) {
+        const int g = wave + (it / NB) * nwaves;
+        const int q0 = (it % NB) * QB;
+        {
+            // every item carries its group's metadata (a cache hit after the first batch)
+            const uint32_t gi = uint32_t(wrow) * ng + g;
+            st.s = load_f32(rs, wok ? gi * 4u : kOobOffset);
+            st.a = 1.f;
+            st.b = 0.f;
+            if constexpr (B >= 3) {
+                st.a = f16_to_f32(uint16_t(load_u16(ra, wok ? gi * 2u : kOobOffset)));
+                st.b = f16_to_f32(uint16_t(load_u16(rb, wok ? gi * 2u : kOobOffset)));
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < QB; ++q) {
+            const uint32_t u = uint32_t(g) * UPG + q0 + q;  // unit index along K
+            const uint32_t byte0 = uint32_t(wrow) * row_bytes + u * (4u * B) + part_byte;
+            load_words<2>(rc, wok ? (byte0 & ~3u) : kOobOffset, st.cw[q]);
+            uint32_t xv[4];
+            load_words<4>(rx, xok ? (uint32_t(col) * uint32_t(k) + u * 32u + 8u * part) * 2u : kOobOffset, xv);
+            st.xa[q] = u32x4_t{xv[0], xv[1], xv[2], xv[3]};
+        }
+    };
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-    for (int g = wave; g < ng; g += kWaves) {
-        const uint32_t gi = uint32_t(wrow) * ng + g;
-        const float s = load_f32(rs, wok ? gi * 4u : kOobOffset);
-        float a = 1.f, b = 0.f;
-        if constexpr (B >= 3) {
-            a = f16_to_f32(uint16_t(load_u16(ra, wok ? gi * 2u : kOobOffset)));
-            b = f16_to_f32(uint16_t(load_u16(rb, wok ? gi * 2u : kOobOffset)));
-        }
-        // the row's level table: lane part of the row writes fields part, part + 4, ...
-        const float c = 1.f - a - b;
-        wave_lds_order();  // the previous group's reads are issued
+    auto process = [&](int it, const Stage &st) {
+        if (it % NB == 0) {
+            // the row's level table: lane part of the row writes fields part, part + 4, ...
+            const float a = st.a, b = st.b;
+            const float c = 1.f - a - b;
+            wave_lds_order();  // the previous group's reads are issued
 #pragma unroll
-        for (int e = 0; e < EPT; ++e) {
-            const int f = part + 4 * e;
-            if (f < NE) {
-                const int kc = field_to_code(uint32_t(f), B);
-                const float v = s * ((B == 1) ? float(kc) : signed_level(kc, M, a, b, c));
-                uint32_t ent;
-                if constexpr (XDT == 0) {
-                    const __bf16 hi = __bf16(v);
-                    const __bf16 lo = __bf16(v - float(hi));
-                    ent = uint32_t(__builtin_bit_cast(uint16_t, hi)) | (uint32_t(__builtin_bit_cast(uint16_t, lo)) << 16);
-                } else {
-                    const _Float16 hi = _Float16(v);
-                    const _Float16 lo = _Float16(v - float(hi));
-                    ent = uint32_t(__builtin_bit_cast(uint16_t, hi)) | (uint32_t(__builtin_bit_cast(uint16_t, lo)) << 16);
-                }
-                mytab[f] = ent;
-            }
-        }
-        wave_lds_order();
-        // units of the group in batches of at most four (registers)
-        constexpr int QB = UPG < 4 ? UPG : 4;
-        for (int q0 = 0; q0 < UPG; q0 += QB) {
-            uint32_t cw[QB][B];
-            u32x4_t xa[QB];
-#pragma unroll
-            for (int q = 0; q < QB; ++q) {
-                const uint32_t u = uint32_t(g) * UPG + q0 + q;  // unit index along K
-                load_words<B>(rc, wok ? uint32_t(wrow) * row_bytes + u * (4u * B) : kOobOffset, cw[q]);
-                uint32_t xv[4];
-                load_words<4>(rx, xok ? (uint32_t(col) * uint32_t(k) + u * 32u + 8u * part) * 2u : kOobOffset, xv);
-                xa[q] = u32x4_t{xv[0], xv[1], xv[2], xv[3]};
-            }
-#pragma unroll
-            for (int q = 0; q < QB; ++q) {
-                uint32_t ent[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int i = 8 * part + e;
-                    const int bit = i * B;
-                    const int wd = bit >> 5, sh = bit & 31;
-                    uint32_t v;
-                    if (sh + B <= 32) v = cw[q][wd] >> sh;
-                    else v = __builtin_amdgcn_alignbit(cw[q][wd + 1], cw[q][wd], sh);
-                    ent[e] = mytab[v & uint32_t(NE - 1)];
-                }
-                u32x4_t hi, lo;
-#pragma unroll
-                for (int p = 0; p < 4; ++p) {
-                    hi[p] = __builtin_amdgcn_perm(ent[2 * p + 1], ent[2 * p], 0x05040100u);
-                    lo[p] = __builtin_amdgcn_perm(ent[2 * p + 1], ent[2 * p], 0x07060302u);
-                }
-                if constexpr (XDT == 0) {
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xa[q]),
-                                                                  __builtin_bit_cast(bf16x8_t, hi), acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xa[q]),
-                                                                  __builtin_bit_cast(bf16x8_t, lo), acc, 0, 0, 0);
-                } else {
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xa[q]),
-                                                                 __builtin_bit_cast(f16x8_t, hi), acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, xa[q]),
-                                                                 __builtin_bit_cast(f16x8_t, lo), acc, 0, 0, 0);
+            for (int e = 0; e < EPT; ++e) {
+                const int f = part + 4 * e;
+                if (f < NE) {
+                    const int kc = field_to_code(uint32_t(f), B);
+                    const float v = st.s * ((B == 1) ? float(kc) : signed_level(kc, M, a, b, c));
+                    uint32_t ent;
+                    if constexpr (XDT == 0) {
+                        const __bf16 hi = __bf16(v);
+                        const __bf16 lo = __bf16(v - float(hi));
+                        ent = uint32_t(__builtin_bit_cast(uint16_t, hi)) |
+                              (uint32_t(__builtin_bit_cast(uint16_t, lo)) << 16);
+                    } else {
+                        const _Float16 hi = _Float16(v);
+                        const _Float16 lo = _Float16(v - float(hi));
+                        ent = uint32_t(__builtin_bit_cast(uint16_t, hi)) |
+                              (uint32_t(__builtin_bit_cast(uint16_t, lo)) << 16);
+                    }
+                    mytab[f] = ent;
                 }
             }
+            wave_lds_order();
         }
+#pragma unroll
+        for (int q = 0; q < QB; ++q) {
+            uint32_t ent[8];
+            const uint64_t win = (uint64_t(st.cw[q][1]) << 32) | st.cw[q][0];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const uint32_t v = uint32_t(win >> (win_shift + uint32_t(B * e)));
+                ent[e] = mytab[v & uint32_t(NE - 1)];
+            }
+            u32x4_t hi, lo;
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                hi[p] = __builtin_amdgcn_perm(ent[2 * p + 1], ent[2 * p], 0x05040100u);
+                lo[p] = __builtin_amdgcn_perm(ent[2 * p + 1], ent[2 * p], 0x07060302u);
+            }
+            if constexpr (XDT == 0) {
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, st.xa[q]),
+                                                              __builtin_bit_cast(bf16x8_t, hi), acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, st.xa[q]),
+                                                              __builtin_bit_cast(bf16x8_t, lo), acc, 0, 0, 0);
+            } else {
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, st.xa[q]),
+                                                             __builtin_bit_cast(f16x8_t, hi), acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, st.xa[q]),
+                                                             __builtin_bit_cast(f16x8_t, lo), acc, 0, 0, 0);
+            }
+        }
+    };
+    Stage s0, s1;
+    if (items > 0) load(0, s0);
+    for (int it = 0; it < items; it += 2) {
+        if (it + 1 < items) load(it + 1, s1);
+        process(it, s0);
+        if (it + 1 >= items) break;
+        if (it + 2 < items) load(it + 2, s0);
+        process(it + 1, s1);
     }
     const float v[4] = {acc[0], acc[1], acc[2], acc[3]};
-    reduce_store<YDT>(red, v, lane, wave, n0, n, m, nullptr, y);
+    reduce_store<YDT>(red, v, lane, wave, nwaves, n0, n, m, nullptr, y);
 }
 
 // ---------------------------------------------------------------- launchers
+
+// Waves per 16-row strip: enough strips x waves to give every SIMD about eight
+// waves of work (latency hiding), at least four, at most sixteen, and no more
+// than there are groups along K.
+static int narrow_waves(const cq_weight &w, int max_waves = kMaxWaves) {
+    const int64_t strips = (w.n + 15) / 16;
+    const int64_t ng = w.k / w.group;
+    int64_t want = (int64_t(device_cu_count()) * 4 * 8 + strips - 1) / strips;
+    int nw = 4;
+    while (nw < max_waves && nw < want) nw *= 2;
+    while (nw > 1 && nw > ng) nw /= 2;
+    return nw;
+}
 
 template <int UPG, int YDT>
 static hipError_t a8_narrow_launch(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
                                    hipStream_t stream) {
     const int64_t blocks = (w.n + 15) / 16;
-    hipLaunchKernelGGL((gemv_a8_narrow<UPG, YDT>), dim3(unsigned(blocks)), dim3(256), 0, stream, w.codes, w.scale, w.a,
+    // G = 512 keeps two stages of eight 64-code steps in registers: at most 8 waves
+    const int nw = narrow_waves(w, UPG >= 16 ? 8 : kMaxWaves);
+    hipLaunchKernelGGL((gemv_a8_narrow<UPG, YDT>), dim3(unsigned(blocks)), dim3(64 * nw), 0, stream, w.codes, w.scale, w.a,
                        w.b, int(w.n), int(w.k), x8, dx, int(m), y);
     return hipGetLastError();
 }
@@ -298,7 +368,7 @@ hipError_t launch_gemv_a8_narrow(const cq_weight &w, const int8_t *x8, const flo
 template <int B, int UPG, int XDT, int YDT>
 static hipError_t a16_narrow_launch(const cq_weight &w, const void *x, int64_t m, void *y, hipStream_t stream) {
     const int64_t blocks = (w.n + 15) / 16;
-    hipLaunchKernelGGL((gemv_a16_narrow<B, UPG, XDT, YDT>), dim3(unsigned(blocks)), dim3(256), 0, stream, w.codes,
+    hipLaunchKernelGGL((gemv_a16_narrow<B, UPG, XDT, YDT>), dim3(unsigned(blocks)), dim3(64 * narrow_waves(w)), 0, stream, w.codes,
                        w.scale, w.a, w.b, int(w.n), int(w.k), static_cast<const uint16_t *>(x), int(m), y);
     return hipGetLastError();
 }
