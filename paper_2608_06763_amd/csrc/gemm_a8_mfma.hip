@@ -13,8 +13,13 @@
 // the matrix cores work on one buffer, every thread loads the next step's
 // codes and activations, decodes its 32 codes to carriers and writes them to
 // the other buffer, so one barrier per step suffices.  Codes and activations are
-// requested two steps ahead into two register slots (the step loop is
-// unrolled by two so that slots are fixed registers).
+// requested two steps ahead into two register slots; a group's (a, b) and
+// scales are requested a whole group ahead, right after the registers that
+// hold them are consumed.  The step loop is unrolled over the positions of a
+// group, so that slots, buffers and group boundaries are compile-time and
+// each step is one basic block, in which scheduling hints spread the
+// decode and rescale VALU work between the 16 MFMAs (the kernel is bound
+// by VALU issue, not by the matrix cores).
 //
 // Decode.  The WM adjacent threads t of a quad (or half quad) serve weight row
 // t / WM, each one 64 / WM codes of every step.  At the start of a group they
@@ -52,6 +57,29 @@ constexpr int kBand = 1;               // row tiles per raster band
 
 __device__ __forceinline__ void lds_store16(int8_t *p, const uint32_t *v) {
     *reinterpret_cast<u32x4 *>(p) = u32x4{v[0], v[1], v[2], v[3]};
+}
+
+// f(integral_constant<P>) for P = P0 .. PN - 1, in order
+template <int P0, int PN, typename F>
+__device__ __forceinline__ void unroll_positions(F &&f) {
+    if constexpr (P0 < PN) {
+        f(std::integral_constant<int, P0>{});
+        unroll_positions<P0 + 1, PN>(f);
+    }
+}
+
+// Scheduling hints for one step: the LDS fragment reads first, then each of
+// the 16 MFMAs followed by R VALU instructions; the first VM of them also
+// take one global load each.
+template <int R, int VM>
+__device__ __forceinline__ void interleave_step() {
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // DS reads
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, R, 0);  // VALU
+        if (q < VM) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
+    }
 }
 
 }  // namespace
@@ -126,8 +154,8 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
     // is decoded, so a load has a whole step of matrix work to arrive.
     uint32_t cw[2][CPT / 8];
     uint32_t xw[2][XB / 4];
-    uint32_t av[2] = {0, 0}, bv[2] = {0, 0};
-    float sj[4], sjn[4];    // group scales of this lane's four output columns
+    uint32_t av = 0, bv = 0;  // (a, b) of the next group's row (FP16 bits)
+    float sj[4];              // group scales of this lane's four output columns
 
     auto load_step = [&](int st, auto slot_c) {
         constexpr int SL = decltype(slot_c)::value;
@@ -135,31 +163,35 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
         load_words<CPT / 8>(rc, wok ? uint32_t(wrow) * row_bytes + (kk + uint32_t(CPT * lq)) / 2u : kOobOffset,
                             cw[SL]);
         load_words<XB / 4>(rx, xok ? uint32_t(xrow) * uint32_t(k) + kk + uint32_t(xc) : kOobOffset, xw[SL]);
-        if (st % SPG == 0) {
-            const uint32_t gi = uint32_t(wrow) * ng + st / SPG;
-            av[SL] = load_u16(ra, wok ? gi * 2u : kOobOffset);
-            bv[SL] = load_u16(rb, wok ? gi * 2u : kOobOffset);
-        }
+    };
+    auto load_ab = [&](int g) {
+        const uint32_t gi = uint32_t(wrow) * ng + g;
+        av = load_u16(ra, wok ? gi * 2u : kOobOffset);
+        bv = load_u16(rb, wok ? gi * 2u : kOobOffset);
     };
     auto load_scales = [&](int g) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int col = n0 + wn + 16 * j + (lane & 15);
-            sjn[j] = load_f32(rs, col < n ? (uint32_t(col) * ng + g) * 4u : kOobOffset);
+            sj[j] = load_f32(rs, col < n ? (uint32_t(col) * ng + g) * 4u : kOobOffset);
         }
     };
 
-    uint32_t ta0 = 0, ta1 = 0, tb0 = 0, tb1 = 0;
-    auto build_tables = [&](auto slot_c) {
-        constexpr int SL = decltype(slot_c)::value;
-        const float a = f16_to_f32(uint16_t(av[SL]));
-        const float b = f16_to_f32(uint16_t(bv[SL]));
+    // Carriers of a group: each thread evaluates NP pairs (exact; the rare
+    // near-tie fallback is a branch, kept at the end of a step); the tables
+    // are assembled from them by DPP quad moves, branch-free, when needed.
+    uint32_t pr[NP];
+    auto eval_carriers = [&]() {
+        const float a = f16_to_f32(uint16_t(av));
+        const float b = f16_to_f32(uint16_t(bv));
         const float c = 1.f - a - b;
         const float mg = carrier_margin(a, b, c);
-        uint32_t pr[NP];
 #pragma unroll
         for (int j = 0; j < NP; ++j)
             pr[j] = carrier_u8<M>(ip0[j], tp0[j], a, b, c, mg) | (carrier_u8<M>(ip0[j] + 1, tp1[j], a, b, c, mg) << 8);
+    };
+    uint32_t ta0 = 0, ta1 = 0, tb0 = 0, tb1 = 0;
+    auto build_tables = [&]() {
         uint32_t P[4];
         if constexpr (Q == 4) {
             P[0] = quad_bcast<0x00>(pr[0]);
@@ -204,29 +236,44 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
     const int nsteps = k / kKS;
     load_step(0, S0{});
     if (nsteps > 1) load_step(1, S1{});
+    load_ab(0);
     load_scales(0);
-    build_tables(S0{});
-#pragma unroll
-    for (int j = 0; j < 4; ++j) sj[j] = sjn[j];
+    eval_carriers();
+    build_tables();
+    // carriers of the group that starts at step 1 (G = 64 only: later group
+    // starts are evaluated two steps ahead inside the loop)
+    load_ab(min(1, ng - 1));
+    if constexpr (SPG == 1) {
+        eval_carriers();
+        load_ab(min(2, ng - 1));
+    }
     store_step(0, S0{});
     __syncthreads();
 
-    // One K step: matrix work on LDS buffer st % 2, then decode step st + 1
-    // (register slot SN) into the other buffer and request step st + 2 into
-    // the slot just freed.
-    auto do_step = [&](int st, auto sn_c) {
-        constexpr int SN = decltype(sn_c)::value;  // slot of step st + 1
-        const int buf = st & 1;
-        // slot 1 - SN held step st, decoded during the previous step
-        if (st + 2 < nsteps) load_step(st + 2, std::integral_constant<int, 1 - SN>{});
+    // One K step at position P of the unrolled period: matrix work on LDS
+    // buffer P % 2 (step st), decode of step st + 1 from slot (P + 1) % 2
+    // into the other buffer, and the request for step st + 2 into the slot
+    // step st came from.  At the last step of a group the next group's
+    // tables are assembled (its first step is decoded now), the partials are
+    // rescaled and the next group's scales requested.  Two steps before a
+    // group starts, its carriers are evaluated at the end of the step, and
+    // the (a, b) of the group after it requested.  Requests past the last
+    // step or group repeat the last one (in bounds; their data is unused).
+    constexpr int PER = SPG >= 2 ? SPG : 2;  // steps per period (even)
+    auto do_step = [&](int st, auto p_c) {
+        constexpr int P = decltype(p_c)::value;
+        constexpr int BUF = P % 2;
+        constexpr bool kFirst = P % SPG == 0;
+        constexpr bool kLast = P % SPG == SPG - 1;
+        load_step(min(st + 2, nsteps - 1), std::integral_constant<int, BUF>{});
         i32x4 af[4], bf[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            af[i] = *reinterpret_cast<const i32x4 *>(&As[buf][(wm + 16 * i + (lane & 15)) * kStride + 16 * (lane >> 4)]);
+            af[i] = *reinterpret_cast<const i32x4 *>(&As[BUF][(wm + 16 * i + (lane & 15)) * kStride + 16 * (lane >> 4)]);
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            bf[j] = *reinterpret_cast<const i32x4 *>(&Bs[buf][(wn + 16 * j + (lane & 15)) * kStride + 16 * (lane >> 4)]);
-        if (st % SPG == 0) {
+            bf[j] = *reinterpret_cast<const i32x4 *>(&Bs[BUF][(wn + 16 * j + (lane & 15)) * kStride + 16 * (lane >> 4)]);
+        if constexpr (kFirst) {
             // first step of a group: the partials start from zero
             const i32x4 zero = {0, 0, 0, 0};
 #pragma unroll
@@ -240,16 +287,11 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
                 for (int j = 0; j < 4; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bf[j], acc[i][j], 0, 0, 0);
         }
-        if (st + 1 < nsteps) {
-            if ((st + 1) % SPG == 0) {
-                build_tables(sn_c);
-                load_scales((st + 1) / SPG);
-            }
-            store_step(buf ^ 1, sn_c);
-        }
-        if (st % SPG == SPG - 1) {
+        const int g = st / SPG;
+        if constexpr (kLast) build_tables();  // group g + 1
+        store_step(BUF ^ 1, std::integral_constant<int, BUF ^ 1>{});
+        if constexpr (kLast) {
             // group complete: FP32 rescale of the exact partials
-            const int g = st / SPG;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
 #pragma unroll
@@ -271,15 +313,23 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
                         }
                     }
             }
-#pragma unroll
-            for (int j = 0; j < 4; ++j) sj[j] = sjn[j];
+            load_scales(min(g + 1, ng - 1));
+        }
+        if constexpr (!DUMP) interleave_step<3, 3>();
+        if constexpr ((P + 2) % SPG == 0) {
+            // the group starting at step st + 2
+            const int gn = (st + 2) / SPG;
+            eval_carriers();
+            load_ab(min(gn + 1, ng - 1));
         }
         __syncthreads();
     };
 
-    for (int st = 0; st < nsteps; st += 2) {
-        do_step(st, S1{});
-        if (st + 1 < nsteps) do_step(st + 1, S0{});
+    for (int st = 0; st < nsteps; st += PER) {
+        unroll_positions<0, PER>([&](auto p_c) {
+            constexpr int P = decltype(p_c)::value;
+            if (P == 0 || st + P < nsteps) do_step(st + P, p_c);
+        });
     }
 
 #pragma unroll
