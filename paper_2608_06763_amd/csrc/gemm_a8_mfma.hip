@@ -44,6 +44,10 @@
 
 #include <type_traits>
 
+// the step bodies are large; every lambda of the kernel must be inlined so
+// that register slots stay registers
+#define CQ_INLINE __attribute__((always_inline))
+
 namespace cq {
 
 namespace {
@@ -102,6 +106,10 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
     constexpr int NP = 4 / Q;               // carrier pairs evaluated per thread
     static_assert(SPG >= 1 && G % kKS == 0, "group must be a multiple of the K step");
     static_assert(Q == 2 || Q == 4, "two or four threads per weight row");
+    // code words of step s are requested kCodeSlots steps ahead into slot
+    // s % kCodeSlots (they stream from HBM); with G < 256 the deeper ring
+    // would need a longer unrolled period than the registers allow
+    constexpr int kCodeSlots = SPG >= 4 ? 4 : 2;
     __shared__ __attribute__((aligned(16))) int8_t As[2][TM * kStride];
     __shared__ __attribute__((aligned(16))) int8_t Bs[2][TN * kStride];
 
@@ -150,30 +158,35 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
         tp1[j] = float(ip0[j] + 1) / float(M);
     }
 
-    // Two register slots: step s is loaded into slot s % 2 two steps before it
-    // is decoded, so a load has a whole step of matrix work to arrive.
-    uint32_t cw[2][CPT / 8];
+    // Register slots: the code words of step s go to slot s % kCodeSlots and
+    // its activation bytes to slot s % 2, requested kCodeSlots or two steps
+    // before step s - 1 writes them to LDS.
+    uint32_t cw[kCodeSlots][CPT / 8];
     uint32_t xw[2][XB / 4];
     uint32_t av = 0, bv = 0;  // (a, b) of the next group's row (FP16 bits)
     float sj[4];              // group scales of this lane's four output columns
 
-    auto load_step = [&](int st, auto slot_c) {
+    auto load_codes = [&](int st, auto slot_c) CQ_INLINE {
         constexpr int SL = decltype(slot_c)::value;
         const uint32_t kk = uint32_t(st) * kKS;
         load_words<CPT / 8>(rc, wok ? uint32_t(wrow) * row_bytes + (kk + uint32_t(CPT * lq)) / 2u : kOobOffset,
                             cw[SL]);
+    };
+    auto load_acts = [&](int st, auto slot_c) CQ_INLINE {
+        constexpr int SL = decltype(slot_c)::value;
+        const uint32_t kk = uint32_t(st) * kKS;
         load_words<XB / 4>(rx, xok ? uint32_t(xrow) * uint32_t(k) + kk + uint32_t(xc) : kOobOffset, xw[SL]);
     };
-    auto load_ab = [&](int g) {
+    auto load_ab = [&](int g) CQ_INLINE {
         const uint32_t gi = uint32_t(wrow) * ng + g;
         av = load_u16(ra, wok ? gi * 2u : kOobOffset);
         bv = load_u16(rb, wok ? gi * 2u : kOobOffset);
     };
-    auto load_scales = [&](int g) {
+    auto load_scales = [&](int g) CQ_INLINE {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int col = n0 + wn + 16 * j + (lane & 15);
-            sj[j] = load_f32(rs, col < n ? (uint32_t(col) * ng + g) * 4u : kOobOffset);
+            sj[j] = load_f32(rs, col < n && g < ng ? (uint32_t(col) * ng + g) * 4u : kOobOffset);
         }
     };
 
@@ -181,7 +194,7 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
     // near-tie fallback is a branch, kept at the end of a step); the tables
     // are assembled from them by DPP quad moves, branch-free, when needed.
     uint32_t pr[NP];
-    auto eval_carriers = [&]() {
+    auto eval_carriers = [&]() CQ_INLINE {
         const float a = f16_to_f32(uint16_t(av));
         const float b = f16_to_f32(uint16_t(bv));
         const float c = 1.f - a - b;
@@ -191,7 +204,7 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
             pr[j] = carrier_u8<M>(ip0[j], tp0[j], a, b, c, mg) | (carrier_u8<M>(ip0[j] + 1, tp1[j], a, b, c, mg) << 8);
     };
     uint32_t ta0 = 0, ta1 = 0, tb0 = 0, tb1 = 0;
-    auto build_tables = [&]() {
+    auto build_tables = [&]() CQ_INLINE {
         uint32_t P[4];
         if constexpr (Q == 4) {
             P[0] = quad_bcast<0x00>(pr[0]);
@@ -209,7 +222,15 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
         w4_negative_table(ta0, ta1, tb0, tb1);
     };
 
-    auto store_step = [&](int buf, auto slot_c) {
+    // Activation bytes of a step go to LDS unchanged; code words are decoded
+    // to carriers first.
+    auto store_acts = [&](int buf, auto slot_c) CQ_INLINE {
+        constexpr int SL = decltype(slot_c)::value;
+        int8_t *ap = &As[buf][xr * kStride + xc];
+#pragma unroll
+        for (int q = 0; q < XB / 16; ++q) lds_store16(ap + 16 * q, xw[SL] + 4 * q);
+    };
+    auto store_codes = [&](int buf, auto slot_c) CQ_INLINE {
         constexpr int SL = decltype(slot_c)::value;
         uint32_t cr[CPT / 4];
 #pragma unroll
@@ -217,9 +238,6 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
         int8_t *bp = &Bs[buf][lr * kStride + CPT * lq];
 #pragma unroll
         for (int q = 0; q < CPT / 16; ++q) lds_store16(bp + 16 * q, cr + 4 * q);
-        int8_t *ap = &As[buf][xr * kStride + xc];
-#pragma unroll
-        for (int q = 0; q < XB / 16; ++q) lds_store16(ap + 16 * q, xw[SL] + 4 * q);
     };
 
     i32x4 acc[4][4];
@@ -234,8 +252,12 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
     using S0 = std::integral_constant<int, 0>;
     using S1 = std::integral_constant<int, 1>;
     const int nsteps = k / kKS;
-    load_step(0, S0{});
-    if (nsteps > 1) load_step(1, S1{});
+    unroll_positions<0, kCodeSlots>([&](auto p_c) CQ_INLINE {
+        constexpr int P = decltype(p_c)::value;
+        load_codes(min(P, nsteps - 1), p_c);
+    });
+    load_acts(0, S0{});
+    load_acts(min(1, nsteps - 1), S1{});
     load_ab(0);
     load_scales(0);
     eval_carriers();
@@ -247,25 +269,29 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
         eval_carriers();
         load_ab(min(2, ng - 1));
     }
-    store_step(0, S0{});
+    store_acts(0, S0{});
+    store_codes(0, S0{});
     __syncthreads();
 
     // One K step at position P of the unrolled period: matrix work on LDS
-    // buffer P % 2 (step st), decode of step st + 1 from slot (P + 1) % 2
-    // into the other buffer, and the request for step st + 2 into the slot
-    // step st came from.  At the last step of a group the next group's
+    // buffer P % 2 (step st); step st + 1 goes to the other buffer (its
+    // activations first, then its decoded codes); the slots step st came
+    // from receive the requests for steps st + kCodeSlots (codes) and
+    // st + 2 (activations).  At the last step of a group the next group's
     // tables are assembled (its first step is decoded now), the partials are
     // rescaled and the next group's scales requested.  Two steps before a
     // group starts, its carriers are evaluated at the end of the step, and
     // the (a, b) of the group after it requested.  Requests past the last
     // step or group repeat the last one (in bounds; their data is unused).
-    constexpr int PER = SPG >= 2 ? SPG : 2;  // steps per period (even)
-    auto do_step = [&](int st, auto p_c) {
+    // The last period may be partial (G < 256); its missing steps are skipped.
+    constexpr int PER = SPG >= kCodeSlots ? SPG : kCodeSlots;  // steps per period
+    auto do_step = [&](int st, auto p_c) CQ_INLINE {
         constexpr int P = decltype(p_c)::value;
         constexpr int BUF = P % 2;
         constexpr bool kFirst = P % SPG == 0;
         constexpr bool kLast = P % SPG == SPG - 1;
-        load_step(min(st + 2, nsteps - 1), std::integral_constant<int, BUF>{});
+        load_codes(min(st + kCodeSlots, nsteps - 1), std::integral_constant<int, P % kCodeSlots>{});
+        load_acts(min(st + 2, nsteps - 1), std::integral_constant<int, BUF>{});
         i32x4 af[4], bf[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -273,6 +299,9 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
 #pragma unroll
         for (int j = 0; j < 4; ++j)
             bf[j] = *reinterpret_cast<const i32x4 *>(&Bs[BUF][(wn + 16 * j + (lane & 15)) * kStride + 16 * (lane >> 4)]);
+        // LDS writes are several times slower than reads: the activations of
+        // step st + 1 need no decode and go out before the matrix work
+        store_acts(BUF ^ 1, std::integral_constant<int, BUF ^ 1>{});
         if constexpr (kFirst) {
             // first step of a group: the partials start from zero
             const i32x4 zero = {0, 0, 0, 0};
@@ -289,7 +318,7 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
         }
         const int g = st / SPG;
         if constexpr (kLast) build_tables();  // group g + 1
-        store_step(BUF ^ 1, std::integral_constant<int, BUF ^ 1>{});
+        store_codes(BUF ^ 1, std::integral_constant<int, (P + 1) % kCodeSlots>{});
         if constexpr (kLast) {
             // group complete: FP32 rescale of the exact partials
 #pragma unroll
@@ -313,9 +342,9 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
                         }
                     }
             }
-            load_scales(min(g + 1, ng - 1));
+            load_scales(g + 1);  // reads zero past the last group
         }
-        if constexpr (!DUMP) interleave_step<3, 3>();
+        if constexpr (!DUMP) interleave_step<3, 4>();
         if constexpr ((P + 2) % SPG == 0) {
             // the group starting at step st + 2
             const int gn = (st + 2) / SPG;
@@ -325,12 +354,11 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
         __syncthreads();
     };
 
-    for (int st = 0; st < nsteps; st += PER) {
-        unroll_positions<0, PER>([&](auto p_c) {
-            constexpr int P = decltype(p_c)::value;
-            if (P == 0 || st + P < nsteps) do_step(st + P, p_c);
+    static_assert(PER % kCodeSlots == 0 && PER % SPG == 0 && PER % 2 == 0, "period must hold whole slots");
+    for (int st = 0; st < nsteps; st += PER)
+        unroll_positions<0, PER>([&](auto p_c) CQ_INLINE {
+            if (p_c == 0 || st + p_c < nsteps) do_step(st + p_c, p_c);
         });
-    }
 
 #pragma unroll
     for (int i = 0; i < 4; ++i)
