@@ -65,7 +65,7 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
     extern __shared__ __attribute__((aligned(16))) float tab[];
 
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));  // uniform: rows stay scalar
     const int nwaves = blockDim.x >> 6;  // the host keeps nwaves <= ncb
     float *red = tab + nwaves * RW * NT * 64;
     const int ntiles = (n + RW - 1) / RW;
@@ -98,22 +98,26 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
     // An item is (row tile, column block).  A workgroup walks the tiles
     // blockIdx.x + j * gridDim.x; its wave w takes column blocks w, w + nwaves,
     // ... of each tile.  The codes and metadata of the next item are requested
-    // before the current one is decoded.  Rows and lanes past the matrix load
-    // an out-of-range offset and read zeros (zero scale, so they add nothing).
+    // before the current one is decoded.  Row offsets are wave-uniform (scalar
+    // offsets); rows past the matrix repeat its last row and are never stored;
+    // lanes past the row's units load an out-of-range offset and read zeros.
     uint32_t wn[RW][B];
     float sn[RW];
     uint32_t an[RW], bn[RW];
     auto fetch = [&](int t, int c) {
         const int u = c * 64 + lane;
+        const bool uok = u < units;
+        const uint32_t vc = uok ? uint32_t(u) * (4 * B) : kOobOffset;
+        const uint32_t vm = uok ? uint32_t(u / UPG) * 4u : kOobOffset;
+        const uint32_t vh = uok ? uint32_t(u / UPG) * 2u : kOobOffset;
 #pragma unroll
         for (int r = 0; r < RW; ++r) {
-            const int row = t * RW + r;
-            const bool ok = (u < units) && (row < n);
-            const uint32_t gi = uint32_t(row) * ng + uint32_t(u / UPG);
-            load_words<B>(rc, ok ? uint32_t(row) * row_bytes + uint32_t(u) * (4 * B) : kOobOffset, wn[r]);
-            sn[r] = load_f32(rs, ok ? gi * 4u : kOobOffset);
-            an[r] = load_u16(ra, ok ? gi * 2u : kOobOffset);
-            bn[r] = load_u16(rb, ok ? gi * 2u : kOobOffset);
+            const uint32_t row = uint32_t(min(t * RW + r, n - 1));
+            const uint32_t gi = row * uint32_t(ng);
+            load_words_s<B>(rc, vc, row * row_bytes, wn[r]);
+            sn[r] = load_f32_s(rs, vm, gi * 4u);
+            an[r] = load_u16_s(ra, vh, gi * 2u);
+            bn[r] = load_u16_s(rb, vh, gi * 2u);
         }
     };
 

@@ -47,6 +47,33 @@ __device__ __forceinline__ void load_words(__amdgpu_buffer_rsrc_t r, uint32_t of
     }
 }
 
+// The same with a wave-uniform part of the offset in a scalar register (the
+// caller keeps voff + soff below 2^32; an out-of-range voff still reads zero).
+template <int WORDS>
+__device__ __forceinline__ void load_words_s(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, uint32_t *out) {
+    if constexpr (WORDS >= 4) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+        out[0] = v[0]; out[1] = v[1]; out[2] = v[2]; out[3] = v[3];
+        if constexpr (WORDS > 4) load_words_s<WORDS - 4>(r, voff + 16u, soff, out + 4);
+    } else if constexpr (WORDS == 3) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b96(r, voff, soff, 0);
+        out[0] = v[0]; out[1] = v[1]; out[2] = v[2];
+    } else if constexpr (WORDS == 2) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
+        out[0] = v[0]; out[1] = v[1];
+    } else {
+        out[0] = __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
+    }
+}
+
+__device__ __forceinline__ float load_f32_s(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
+
+__device__ __forceinline__ uint32_t load_u16_s(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    return uint32_t(__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0));
+}
+
 __device__ __forceinline__ float load_f32(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
