@@ -162,6 +162,25 @@ cq_status cq_gemm_a8(const cq_weight *w, const int8_t *x8, const float *dx, int6
                      void *y, cq_dtype y_dtype, int32_t *partials_dbg, void *stream);
 
 /*
+ * cq_gemm_a8_fused -- Dynamic-A8 product from model-dtype activations (device).
+ *
+ * Same result as cq_quantize_act_a8 followed by cq_gemm_a8 (Sec. 5.4): x8 and
+ * dx receive the carriers and d_x, bit-exact; y follows eq. a8-output.  For a
+ * single row (m == 1, B in {1, 2, 4}, K <= 16384) it is one launch: the GEMV
+ * forms the row's carriers itself in a prologue, which removes the separate
+ * encoding pass the paper names as the fixed cost of the single-row A8 path
+ * (Sec. 6).  Other shapes run the two calls in order on the stream.  The FP32
+ * summation order of the single launch can differ from cq_gemm_a8's for the
+ * same row, so y agrees with it to rounding, not bit for bit.
+ *   x        device [M, K] in x_dtype (CQ_BF16 or CQ_FP16).
+ *   x8, dx   device int8 [M, K] and float [M], written (caller-owned).
+ *   y        device [M, N] in y_dtype (CQ_BF16, CQ_FP16 or CQ_FP32).
+ * Errors as cq_quantize_act_a8 and cq_gemm_a8.
+ */
+cq_status cq_gemm_a8_fused(const cq_weight *w, const void *x, cq_dtype x_dtype, int64_t m,
+                           int8_t *x8, float *dx, void *y, cq_dtype y_dtype, void *stream);
+
+/*
  * Row-regime kernel selection (Sec. 5.5-5.6).  Each path picks the GEMV
  * family for m <= its threshold and the tiled GEMM family above it.  The
  * defaults come from measurements on MI355X.  cq_set_gemv_max_rows

@@ -7,7 +7,7 @@ GPU; calling a device entry point does, and a missing library raises.
 
 Entry points (same names as the C ABI):
   cq_pack_groups, cq_decode_ref, cq_gemm_model_dtype, cq_quantize_act_a8,
-  cq_gemm_a8, cq_set_gemv_max_rows, cq_get_gemv_max_rows
+  cq_gemm_a8, cq_gemm_a8_fused, cq_set_gemv_max_rows, cq_get_gemv_max_rows
 """
 from __future__ import annotations
 
@@ -24,7 +24,7 @@ STATUS = {0: "CQ_OK", 1: "CQ_ERR_ARG", 2: "CQ_ERR_SHAPE", 3: "CQ_ERR_ALIGN", 4: 
           5: "CQ_ERR_CODE", 6: "CQ_ERR_DTYPE", 7: "CQ_ERR_HIP", 8: "CQ_ERR_UNSUPPORTED"}
 
 EXPORTS = ("cq_status_str", "cq_pack_groups", "cq_decode_ref", "cq_gemm_model_dtype", "cq_quantize_act_a8",
-           "cq_gemm_a8", "cq_set_gemv_max_rows", "cq_get_gemv_max_rows")
+           "cq_gemm_a8", "cq_gemm_a8_fused", "cq_set_gemv_max_rows", "cq_get_gemv_max_rows")
 
 
 class CQError(RuntimeError):
@@ -63,6 +63,8 @@ def lib() -> ctypes.CDLL:
     L.cq_quantize_act_a8.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp, vp]
     L.cq_gemm_a8.restype = ctypes.c_int
     L.cq_gemm_a8.argtypes = [ctypes.POINTER(cq_weight), vp, vp, i64, vp, ctypes.c_int, vp, vp]
+    L.cq_gemm_a8_fused.restype = ctypes.c_int
+    L.cq_gemm_a8_fused.argtypes = [ctypes.POINTER(cq_weight), vp, ctypes.c_int, i64, vp, vp, vp, ctypes.c_int, vp]
     L.cq_set_gemv_max_rows.restype = ctypes.c_int
     L.cq_set_gemv_max_rows.argtypes = [i32, i64]
     L.cq_get_gemv_max_rows.restype = i64
@@ -213,6 +215,24 @@ def cq_gemm_a8(w: CQWeight, x8, dx, y_dtype=None, want_partials=False, out=None,
                           parts.data_ptr() if parts is not None else None, _stream_ptr(stream))
     _check(st, "cq_gemm_a8")
     return (out, parts) if want_partials else out
+
+
+def cq_gemm_a8_fused(w: CQWeight, x, y_dtype=None, out=None, x8=None, dx=None, stream=None):
+    """Dynamic-A8 product straight from model-dtype activations; returns (y, x8, dx)."""
+    torch = _torch()
+    assert x.dim() == 2 and x.shape[1] == w.k and x.is_contiguous()
+    m = x.shape[0]
+    y_dtype = y_dtype or x.dtype
+    if out is None:
+        out = torch.empty((m, w.n), dtype=y_dtype, device=x.device)
+    if x8 is None:
+        x8 = torch.empty((m, w.k), dtype=torch.int8, device=x.device)
+    if dx is None:
+        dx = torch.empty((m,), dtype=torch.float32, device=x.device)
+    st = lib().cq_gemm_a8_fused(ctypes.byref(w.desc), x.data_ptr(), _dt(x.dtype), m, x8.data_ptr(), dx.data_ptr(),
+                                out.data_ptr(), _dt(out.dtype), _stream_ptr(stream))
+    _check(st, "cq_gemm_a8_fused")
+    return out, x8, dx
 
 
 def cq_set_gemv_max_rows(path: int, max_rows: int):

@@ -176,6 +176,24 @@ cq_status cq_gemm_a8(const cq_weight *w, const int8_t *x8, const float *dx, int6
     return hip_status(cq::launch_gemm_a8(*w, x8, dx, m, y, int(y_dtype), partials_dbg, s));
 }
 
+cq_status cq_gemm_a8_fused(const cq_weight *w, const void *x, cq_dtype x_dtype, int64_t m, int8_t *x8, float *dx,
+                           void *y, cq_dtype y_dtype, void *stream) {
+    const cq_status st = check_weight(w);
+    if (st != CQ_OK) return st;
+    if (!x || !x8 || !dx || !y || m < 1) return CQ_ERR_ARG;
+    if (x_dtype != CQ_BF16 && x_dtype != CQ_FP16) return CQ_ERR_DTYPE;
+    if (y_dtype != CQ_BF16 && y_dtype != CQ_FP16 && y_dtype != CQ_FP32) return CQ_ERR_DTYPE;
+    if (!aligned16(x) || !aligned16(x8) || !aligned16(dx) || !aligned16(y)) return CQ_ERR_ALIGN;
+    if (m > (int64_t(1) << 40) / w->k || m > (int64_t(1) << 40) / w->n) return CQ_ERR_SHAPE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (m <= gemv_max_rows(1) && cq::gemv_a8_fused_supported(*w, m))
+        return hip_status(cq::launch_gemv_a8_fused(*w, x, int(x_dtype), x8, dx, y, int(y_dtype), s));
+    // every other shape: the two calls, in order on the stream
+    const cq_status q = cq_quantize_act_a8(x, x_dtype, m, w->k, x8, dx, stream);
+    if (q != CQ_OK) return q;
+    return cq_gemm_a8(w, x8, dx, m, y, y_dtype, nullptr, stream);
+}
+
 cq_status cq_set_gemv_max_rows(int32_t path, int64_t max_rows) {
     if (path != 0 && path != 1) return CQ_ERR_ARG;
     g_gemv_max_rows[path].store(max_rows < 0 ? -1 : max_rows, std::memory_order_relaxed);

@@ -56,6 +56,9 @@ hipError_t launch_gemv_a8(const cq_weight &w, const int8_t *x8, const float *dx,
 
 // Dynamic-A8 single-row streaming GEMV (m == 1, B in {1, 2, 4}, no partials dump).
 bool gemv_a8_stream_supported(const cq_weight &w, int64_t m);
+bool gemv_a8_fused_supported(const cq_weight &w, int64_t m);
+hipError_t launch_gemv_a8_fused(const cq_weight &w, const void *x, int x_dt, int8_t *x8_out, float *dx_out, void *y,
+                                int y_dt, hipStream_t stream);
 hipError_t launch_gemv_a8_stream(const cq_weight &w, const int8_t *x8, const float *dx, void *y, int y_dt,
                                  hipStream_t stream);
 

@@ -19,10 +19,23 @@
 // are computed once per (row, group): the group's lanes each evaluate two
 // magnitudes and share them through quad DPP moves.  W2 and W1 use constant
 // tables ({0, 127, 0, -127} and {-127, 127}).
+//
+// Fused quantization (FX >= 0): the kernel takes the BF16/FP16 activation row
+// itself and forms its carriers in a prologue, so that a single-row A8 product
+// is one launch (the activation encoding is the fixed cost of the single-row
+// A8 path, Sec. 6).  Every workgroup reduces the whole row to its maximum
+// magnitude (order-free, so every workgroup gets the same d_x): wave w of a
+// workgroup owns column block w for the whole launch, so the 32 activations of
+// each lane's unit, read once, give both the row maximum and the carriers,
+// which are formed with the standalone quantizer's results (a8_quant.h: a
+// reciprocal product, exact division near rounding boundaries) and kept in
+// registers.  The codes of the first tile are requested before the
+// prologue.
 #include "cq_device.h"
 #include "cq_internal.h"
 #include "stream_common.h"
 #include "a8_carriers.h"
+#include "a8_quant.h"
 
 namespace cq {
 
@@ -76,13 +89,21 @@ __device__ __forceinline__ void arrange_x(const uint32_t xw[8], uint32_t xa[8]) 
 
 }  // namespace
 
-template <int B, int UPG, int RW, int YDT>
-__global__ void __launch_bounds__(256) gemv_a8_stream(
+// FX < 0: xin holds the INT8 carriers and dxv their d_x.  FX = 0 / 1: xin is
+// the BF16 / FP16 row, quantized here; block 0 writes the carriers to x8_out
+// (if given) and d_x to dxv.  With FX >= 0 the host launches one wave per
+// column block (at most kMaxFusedWaves).
+constexpr int kMaxFusedWaves = 8;
+
+template <int B, int UPG, int RW, int YDT, int FX>
+__global__ void __launch_bounds__(FX >= 0 ? 64 * kMaxFusedWaves : 256) gemv_a8_stream(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
-    int n, int k, const int8_t *__restrict__ x8, const float *__restrict__ dx, void *__restrict__ y) {
+    int n, int k, const void *__restrict__ xin, float *__restrict__ dxv, int8_t *__restrict__ x8_out,
+    void *__restrict__ y) {
     constexpr int M = max_code(B);
-    __shared__ float red[4 * RW];
+    constexpr bool kFused = FX >= 0;
+    __shared__ float red[kMaxFusedWaves * RW];
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -96,7 +117,7 @@ __global__ void __launch_bounds__(256) gemv_a8_stream(
     const auto rs = make_rsrc(scale, uint32_t(n) * ng * 4u);
     const auto ra = make_rsrc(a16, uint32_t(n) * ng * 2u);
     const auto rb = make_rsrc(b16, uint32_t(n) * ng * 2u);
-    const auto rx = make_rsrc(x8, uint32_t(k));
+    const auto rx = make_rsrc(xin, uint32_t(k) * (kFused ? 2u : 1u));
 
     // W4 carrier pairs evaluated by this lane: pair p covers magnitudes 2p, 2p+1.
     // Q lanes of a quad share a group; lane j of them evaluates pairs j, j+Q, ...
@@ -140,6 +161,52 @@ __global__ void __launch_bounds__(256) gemv_a8_stream(
     int tile = blockIdx.x, cb = wave;
     bool have = tile < ntiles;
     if (have) fetch(tile, cb);
+
+    // fused quantization: d_x of the row and this lane's fixed carriers.  The
+    // waves of a workgroup own all column blocks, so the lanes' own units are
+    // the whole row: one read gives both the maximum and the values.
+    uint32_t xq[8];
+    float fac_fused = 0.f;
+    if constexpr (kFused) {
+        const int u = cb * 64 + lane;
+        const uint32_t xo = u < units ? uint32_t(u) * 64u : kOobOffset;
+        uint4 xv[4];
+        float mx = 0.f;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            uint32_t p[4];
+            load_words<4>(rx, xo + 16u * q, p);
+            xv[q] = make_uint4(p[0], p[1], p[2], p[3]);
+            mx = absmax8<FX>(xv[q], mx);
+        }
+        mx = wave_max(mx);
+        if (lane == 0) red[wave] = mx;
+        __syncthreads();
+        mx = red[0];
+        for (int wv = 1; wv < nwaves; ++wv) mx = fmaxf(mx, red[wv]);
+        __syncthreads();  // red is reused by the tile reduction
+        const float d = a8_row_scale(mx);
+        const float rcp = __fdiv_rn(1.0f, d);
+        fac_fused = d / 127.0f;
+        uint32_t xw[8];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint2 c = quantize8_rcp<FX>(xv[q], d, rcp);
+            xw[2 * q] = c.x;
+            xw[2 * q + 1] = c.y;
+        }
+        if (blockIdx.x == 0) {
+            if (x8_out && u < units) {
+                typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+                u32x4_t *o = reinterpret_cast<u32x4_t *>(x8_out + size_t(u) * 32u);
+                o[0] = u32x4_t{xw[0], xw[1], xw[2], xw[3]};
+                o[1] = u32x4_t{xw[4], xw[5], xw[6], xw[7]};
+            }
+            if (threadIdx.x == 0) dxv[0] = d;
+        }
+        arrange_x<B>(xw, xq);
+    }
+
     while (have) {
         uint32_t w[RW][B];
         float s[RW];
@@ -153,7 +220,7 @@ __global__ void __launch_bounds__(256) gemv_a8_stream(
             bv[r] = bn[r];
         }
         int cb_next = cb + nwaves, tile_next = tile;
-        const bool last_cb = cb_next >= ncb;
+        const bool last_cb = kFused || cb_next >= ncb;
         if (last_cb) {
             cb_next = wave;
             tile_next = tile + int(gridDim.x);
@@ -161,9 +228,12 @@ __global__ void __launch_bounds__(256) gemv_a8_stream(
         const bool have_next = tile_next < ntiles;
         if (have_next) fetch(tile_next, cb_next);
 
-        const int u = cb * 64 + lane;
         uint32_t xa[8];
-        {
+        if constexpr (kFused) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) xa[i] = xq[i];
+        } else {
+            const int u = cb * 64 + lane;
             uint32_t xw[8];
             const uint32_t xo = u < units ? uint32_t(u) * 32u : kOobOffset;
             load_words<4>(rx, xo, xw);
@@ -237,7 +307,7 @@ __global__ void __launch_bounds__(256) gemv_a8_stream(
         }
         if (last_cb) {
             const int row0 = tile * RW;
-            const float fac = dx[0] / 127.0f;
+            const float fac = kFused ? fac_fused : dxv[0] / 127.0f;
             static_assert(RW == 2, "the output store writes row pairs");
             if (nwaves == 1) {
                 const float v0 = wave_sum(acc[0]);
@@ -270,55 +340,80 @@ __global__ void __launch_bounds__(256) gemv_a8_stream(
     }
 }
 
-template <int B, int UPG, int YDT>
-static hipError_t a8_stream_launch(const cq_weight &w, const int8_t *x8, const float *dx, void *y,
+template <int B, int UPG, int YDT, int FX>
+static hipError_t a8_stream_launch(const cq_weight &w, const void *xin, float *dxv, int8_t *x8_out, void *y,
                                    hipStream_t stream) {
     constexpr int RW = 2;
     const int64_t ncb = ((w.k >> 5) + 63) >> 6;
-    // up to two column blocks a single wave per tile is fastest (no LDS
-    // reduction); longer rows split their column blocks over two waves
-    const int nw = ncb > 2 ? 2 : 1;
+    // unfused: up to two column blocks a single wave per tile is fastest (no
+    // LDS reduction); longer rows split their column blocks over two waves.
+    // Fused: one wave per column block.
+    const int nw = FX >= 0 ? int(ncb) : (ncb > 2 ? 2 : 1);
+    if (nw > kMaxFusedWaves) return hipErrorNotSupported;
     const int64_t tiles = (w.n + RW - 1) / RW;
-    int64_t blocks = int64_t(device_cu_count()) * 64;
+    const int64_t cus = device_cu_count();
+    // unfused: one workgroup per tile up to 64 per CU.  Fused: every workgroup
+    // quantizes the whole row once, so fewer, longer-lived workgroups (per CU:
+    // 2 with four or more waves, 4 up to 8192 tiles, 12 beyond; measured on
+    // the Llama-3-8B decode layers)
+    int64_t per_cu = 64;
+    if (FX >= 0) per_cu = nw >= 4 ? 2 : (tiles > 8192 ? 12 : 4);
+    int64_t blocks = cus * per_cu;
     if (blocks > tiles) blocks = tiles;
-    hipLaunchKernelGGL((gemv_a8_stream<B, UPG, RW, YDT>), dim3(unsigned(blocks)), dim3(nw * 64), 0, stream, w.codes,
-                       w.scale, w.a, w.b, int(w.n), int(w.k), x8, dx, y);
+    hipLaunchKernelGGL((gemv_a8_stream<B, UPG, RW, YDT, FX>), dim3(unsigned(blocks)), dim3(nw * 64), 0, stream,
+                       w.codes, w.scale, w.a, w.b, int(w.n), int(w.k), xin, dxv, x8_out, y);
     return hipGetLastError();
 }
 
-template <int B, int YDT>
-static hipError_t a8_stream_group(const cq_weight &w, const int8_t *x8, const float *dx, void *y,
+template <int B, int YDT, int FX>
+static hipError_t a8_stream_group(const cq_weight &w, const void *xin, float *dxv, int8_t *x8_out, void *y,
                                   hipStream_t stream) {
     switch (w.group) {
-        case 32: return a8_stream_launch<B, 1, YDT>(w, x8, dx, y, stream);
-        case 64: return a8_stream_launch<B, 2, YDT>(w, x8, dx, y, stream);
-        case 128: return a8_stream_launch<B, 4, YDT>(w, x8, dx, y, stream);
-        case 256: return a8_stream_launch<B, 8, YDT>(w, x8, dx, y, stream);
-        case 512: return a8_stream_launch<B, 16, YDT>(w, x8, dx, y, stream);
+        case 32: return a8_stream_launch<B, 1, YDT, FX>(w, xin, dxv, x8_out, y, stream);
+        case 64: return a8_stream_launch<B, 2, YDT, FX>(w, xin, dxv, x8_out, y, stream);
+        case 128: return a8_stream_launch<B, 4, YDT, FX>(w, xin, dxv, x8_out, y, stream);
+        case 256: return a8_stream_launch<B, 8, YDT, FX>(w, xin, dxv, x8_out, y, stream);
+        case 512: return a8_stream_launch<B, 16, YDT, FX>(w, xin, dxv, x8_out, y, stream);
     }
     return hipErrorNotSupported;
 }
 
-template <int YDT>
-static hipError_t a8_stream_bits(const cq_weight &w, const int8_t *x8, const float *dx, void *y,
+template <int YDT, int FX>
+static hipError_t a8_stream_bits(const cq_weight &w, const void *xin, float *dxv, int8_t *x8_out, void *y,
                                  hipStream_t stream) {
     switch (w.bits) {
-        case 1: return a8_stream_group<1, YDT>(w, x8, dx, y, stream);
-        case 2: return a8_stream_group<2, YDT>(w, x8, dx, y, stream);
-        case 4: return a8_stream_group<4, YDT>(w, x8, dx, y, stream);
+        case 1: return a8_stream_group<1, YDT, FX>(w, xin, dxv, x8_out, y, stream);
+        case 2: return a8_stream_group<2, YDT, FX>(w, xin, dxv, x8_out, y, stream);
+        case 4: return a8_stream_group<4, YDT, FX>(w, xin, dxv, x8_out, y, stream);
     }
     return hipErrorNotSupported;
+}
+
+template <int FX>
+static hipError_t a8_stream_ydt(const cq_weight &w, const void *xin, float *dxv, int8_t *x8_out, void *y, int y_dt,
+                                hipStream_t stream) {
+    if (y_dt == 0) return a8_stream_bits<0, FX>(w, xin, dxv, x8_out, y, stream);
+    if (y_dt == 1) return a8_stream_bits<1, FX>(w, xin, dxv, x8_out, y, stream);
+    return a8_stream_bits<2, FX>(w, xin, dxv, x8_out, y, stream);
 }
 
 bool gemv_a8_stream_supported(const cq_weight &w, int64_t m) {
     return m == 1 && (w.bits == 1 || w.bits == 2 || w.bits == 4) && stream_fits(w.n, w.k, w.bits, w.group);
 }
 
+bool gemv_a8_fused_supported(const cq_weight &w, int64_t m) {
+    return gemv_a8_stream_supported(w, m) && (((w.k >> 5) + 63) >> 6) <= kMaxFusedWaves;
+}
+
 hipError_t launch_gemv_a8_stream(const cq_weight &w, const int8_t *x8, const float *dx, void *y, int y_dt,
                                  hipStream_t stream) {
-    if (y_dt == 0) return a8_stream_bits<0>(w, x8, dx, y, stream);
-    if (y_dt == 1) return a8_stream_bits<1>(w, x8, dx, y, stream);
-    return a8_stream_bits<2>(w, x8, dx, y, stream);
+    return a8_stream_ydt<-1>(w, x8, const_cast<float *>(dx), nullptr, y, y_dt, stream);
+}
+
+hipError_t launch_gemv_a8_fused(const cq_weight &w, const void *x, int x_dt, int8_t *x8_out, float *dx_out, void *y,
+                                int y_dt, hipStream_t stream) {
+    if (x_dt == 0) return a8_stream_ydt<0>(w, x, dx_out, x8_out, y, y_dt, stream);
+    return a8_stream_ydt<1>(w, x, dx_out, x8_out, y, y_dt, stream);
 }
 
 }  // namespace cq

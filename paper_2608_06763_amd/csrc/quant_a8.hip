@@ -10,50 +10,9 @@
 // 16-byte and 8-byte vectors.
 #include "cq_device.h"
 #include "cq_internal.h"
+#include "a8_quant.h"
 
 namespace cq {
-
-constexpr float kEps = 1e-10f;
-
-// Maximum over the 64 lanes of a wavefront (every lane active), DPP moves
-// within rows of 16 lanes, then readlane across the four rows.
-__device__ __forceinline__ float wave_max(float v) {
-    v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xb1, 0xf, 0xf, false)));
-    v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4e, 0xf, 0xf, false)));
-    v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xf, 0xf, false)));
-    v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xf, 0xf, false)));
-    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
-    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
-    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
-    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
-    return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
-}
-
-template <int XDT>
-__device__ __forceinline__ uint2 quantize8(const uint4 &p, float d) {
-    const uint32_t pw[4] = {p.x, p.y, p.z, p.w};
-    uint32_t out[2] = {0u, 0u};
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        const uint16_t h = (e & 1) ? uint16_t(pw[e >> 1] >> 16) : uint16_t(pw[e >> 1] & 0xffffu);
-        const float q = __fdiv_rn(act_to_f32<XDT>(h), d);
-        float r = roundf(q);  // nearest, halfway cases away from zero
-        r = fminf(fmaxf(r, -127.f), 127.f);
-        out[e >> 2] |= (uint32_t(int(r)) & 0xffu) << (8 * (e & 3));
-    }
-    return make_uint2(out[0], out[1]);
-}
-
-template <int XDT>
-__device__ __forceinline__ float absmax8(const uint4 &p, float mx) {
-    const uint32_t pw[4] = {p.x, p.y, p.z, p.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        mx = fmaxf(mx, fabsf(act_to_f32<XDT>(uint16_t(pw[e] & 0xffffu))));
-        mx = fmaxf(mx, fabsf(act_to_f32<XDT>(uint16_t(pw[e] >> 16))));
-    }
-    return mx;
-}
 
 // NV > 0: every thread holds its (at most NV) 16-byte vectors of the row in
 // registers between the two passes; NV == 0: the second pass re-reads the row.
@@ -84,8 +43,7 @@ __global__ void __launch_bounds__(256) quant_a8_kernel(const uint16_t *__restric
     if ((tid & 63) == 0) red[tid >> 6] = mx;
     __syncthreads();
     mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-    const float xbar = fmaxf(mx, kEps);
-    const float d = __fdiv_rn(xbar, 127.0f);
+    const float d = a8_row_scale(mx);
     if (tid == 0) dx[row] = d;
 
     if constexpr (NV > 0) {

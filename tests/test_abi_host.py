@@ -150,6 +150,7 @@ def test_device_calls_validate_on_host():
         assert L.cq_gemm_model_dtype(ctypes.byref(d), P(ok), 0, 1, P(ok), 0, None) == want
         assert L.cq_gemm_a8(ctypes.byref(d), P(ok), P(ok), 1, P(ok), 0, None, None) == want
         assert L.cq_decode_ref(ctypes.byref(d), P(ok), None, None) == want
+        assert L.cq_gemm_a8_fused(ctypes.byref(d), P(ok), 0, 1, P(ok), P(ok), P(ok), 0, None) == want
     assert L.cq_gemm_model_dtype(None, P(ok), 0, 1, P(ok), 0, None) == 1
     assert L.cq_gemm_model_dtype(ctypes.byref(w), P(ok), 0, 0, P(ok), 0, None) == 1        # m = 0
     assert L.cq_gemm_model_dtype(ctypes.byref(w), P(ok), 2, 1, P(ok), 2, None) == 6        # fp32 x
@@ -158,6 +159,13 @@ def test_device_calls_validate_on_host():
     assert L.cq_gemm_a8(ctypes.byref(w), P(ok), P(ok), 1, P(ok), 7, None, None) == 6
     assert L.cq_gemm_a8(ctypes.byref(w), P(ok), P(ok), 1, P(ok), 0, P(bad_align), None) == 3
     assert L.cq_decode_ref(ctypes.byref(w), None, None, None) == 1
+    fused = L.cq_gemm_a8_fused
+    assert fused(ctypes.byref(w), None, 0, 1, P(ok), P(ok), P(ok), 0, None) == 1            # no x
+    assert fused(ctypes.byref(w), P(ok), 0, 1, None, P(ok), P(ok), 0, None) == 1            # no x8
+    assert fused(ctypes.byref(w), P(ok), 0, 0, P(ok), P(ok), P(ok), 0, None) == 1           # m = 0
+    assert fused(ctypes.byref(w), P(ok), 2, 1, P(ok), P(ok), P(ok), 0, None) == 6           # fp32 x
+    assert fused(ctypes.byref(w), P(ok), 0, 1, P(ok), P(ok), P(ok), 7, None) == 6           # bad y dtype
+    assert fused(ctypes.byref(w), P(ok), 0, 1, P(ok), P(bad_align), P(ok), 0, None) == 3
     assert L.cq_quantize_act_a8(P(ok), 0, 1, 48, P(ok), P(ok), None) == 2                 # k % 32
     assert L.cq_quantize_act_a8(P(ok), 2, 1, 64, P(ok), P(ok), None) == 6
     assert L.cq_quantize_act_a8(P(ok), 0, 0, 64, P(ok), P(ok), None) == 1

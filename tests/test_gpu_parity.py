@@ -400,3 +400,69 @@ def test_narrow_rows_both_paths(torch_dev, group, m):
         assert R.eps_comp(_np(y), y2_ref, "fp32") <= 2e-4
         y16 = cq.cq_gemm_model_dtype(w, _x(torch_dev, xb2, dtype))
         assert R.eps_comp(_np(y16), y2_ref, dtype) <= TOL
+
+
+# ---------------------------------------------------------------- fused single-row A8
+
+
+@pytest.mark.parametrize("bits", [1, 2, 4])
+@pytest.mark.parametrize("group", [32, 128, 512])
+@pytest.mark.parametrize("k", [512, 2048, 4096, 4096 + 2048 + 512, 14336, 16384])
+def test_gemm_a8_fused_single_row(torch_dev, bits, group, k):
+    # m == 1: one launch that quantizes its own activations (one to eight
+    # column blocks, the last one ragged for K = 6656); carriers and d_x are
+    # compared bit for bit, y against the A8 oracle
+    if k % group:
+        pytest.skip("K must be a multiple of G")
+    r = fitted(51, 37, k, bits, group)
+    cq = _cq()
+    w = _weight(r, bits, group)
+    for dtype in ("bf16", "fp16"):
+        xb, xv = act(52, 1, k, dtype)
+        x8_ref, d_ref, y_ref, _ = ref_a8(xv, r, bits, group)
+        say("gemm_a8_fused", bits, group, k, dtype)
+        x = _x(torch_dev, xb, dtype)
+        y, x8, dx = cq.cq_gemm_a8_fused(w, x, y_dtype=torch_dev.float32)
+        assert np.array_equal(x8.cpu().numpy(), x8_ref)
+        assert np.array_equal(dx.cpu().numpy(), d_ref.astype(np.float32))
+        assert R.eps_comp(_np(y), y_ref, "fp32") <= 1e-5
+        y16, _, _ = cq.cq_gemm_a8_fused(w, x)
+        assert R.eps_comp(_np(y16), y_ref, dtype) <= TOL
+        # the two-call path on the same row: same carriers, y equal to rounding
+        y2 = cq.cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32)
+        assert R.eps_comp(_np(y), _np(y2).astype(np.float64), "fp32") <= 1e-6
+
+
+@pytest.mark.parametrize("case", ["rows3", "w3", "k18432", "zero_row", "gemv_rows_0"])
+def test_gemm_a8_fused_fallbacks(torch_dev, case):
+    # shapes the single launch does not take run the two calls; an all-zero
+    # row gives d_x = eps / 127, zero carriers and a zero output
+    cq = _cq()
+    bits, group, k, m, n = 4, 128, 2048, 1, 21
+    if case == "rows3":
+        m = 3
+    elif case == "w3":
+        bits = 3
+    elif case == "k18432":
+        k = 18432
+    r = fitted(61, n, k, bits, group)
+    xb, xv = act(62, m, k)
+    if case == "zero_row":
+        xb = np.zeros_like(xb)
+        xv = np.zeros_like(xv)
+    x8_ref, d_ref, y_ref, _ = ref_a8(xv, r, bits, group)
+    say("gemm_a8_fused fallback", case)
+    w = _weight(r, bits, group)
+    if case == "gemv_rows_0":
+        cq.cq_set_gemv_max_rows(1, 0)
+    try:
+        y, x8, dx = cq.cq_gemm_a8_fused(w, _x(torch_dev, xb, "bf16"), y_dtype=torch_dev.float32)
+    finally:
+        cq.cq_set_gemv_max_rows(1, -1)
+    assert np.array_equal(x8.cpu().numpy(), x8_ref)
+    assert np.array_equal(dx.cpu().numpy(), d_ref.astype(np.float32))
+    if case == "zero_row":
+        assert np.all(y.cpu().numpy() == 0)
+        assert dx.cpu().numpy()[0] == np.float32(np.float32(1e-10) / np.float32(127))
+    else:
+        assert R.eps_comp(_np(y), y_ref, "fp32") <= 1e-5
