@@ -466,3 +466,56 @@ def test_gemm_a8_fused_fallbacks(torch_dev, case):
         assert dx.cpu().numpy()[0] == np.float32(np.float32(1e-10) / np.float32(127))
     else:
         assert R.eps_comp(_np(y), y_ref, "fp32") <= 1e-5
+
+
+def _all_values(dtype):
+    """Every finite non-negative value of the activation dtype (float64)."""
+    if dtype == "bf16":
+        return (np.arange(0, 0x7F80, dtype=np.uint32) << 16).view(np.float32).astype(np.float64)
+    return np.arange(0, 0x7C00, dtype=np.uint16).view(np.float16).astype(np.float64)
+
+
+def _encode(vals, dtype):
+    from workloads import to_bf16_bits, to_f16_bits
+    return to_bf16_bits(vals) if dtype == "bf16" else to_f16_bits(vals)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+def test_gemm_a8_fused_carriers_near_rounding_boundaries(torch_dev, dtype):
+    # the single-row call forms carriers from x * (1/d) and divides only near
+    # a rounding boundary; for 24 random row scales, every representable
+    # activation whose quotient lies within 2^-15 of a half-integer (plus a
+    # random sample of the others), both signs, must give the oracle's
+    # IEEE-division carriers; at xbar = 127 (d = 1) every half-integer is an
+    # exact tie, and there the whole value range is checked
+    from workloads import synthetic_representation
+    allv = _all_values(dtype)
+    rng = np.random.default_rng(81)
+    k = 4096
+    codes, s, a, b = synthetic_representation(72, 5, k, 4, 128)
+    w = _cq().CQWeight.from_codes(codes, s, a, b, 4, 128)
+    cands = allv[(allv >= 0.01) & (allv <= 1000.0)]
+    rows = []
+    for amax in rng.choice(cands, 24, replace=False):
+        d = np.float64(np.float32(np.float32(amax) / np.float32(127.0)))
+        v = allv[allv <= amax]
+        f = np.abs(np.abs(v / d - np.round(v / d)) - 0.5)
+        pick = np.concatenate([v[f < 2.0 ** -15], rng.choice(v, 800)])
+        rows.append((amax, pick))
+    top = allv[allv <= 127.0]
+    for i in range(0, len(top), 2000):
+        rows.append((127.0, top[i:i + 2000]))
+    hits = 0
+    for amax, pick in rows:
+        row = np.zeros((1, k))
+        vals = np.concatenate([pick, -pick])[:k - 1]
+        row[0, 0] = amax
+        row[0, 1:1 + len(vals)] = vals
+        x8_ref, d_ref = A8.quantize_act(row)
+        q = row / np.float64(d_ref[0])
+        hits += int(np.sum(np.abs(np.abs(q - np.round(q)) - 0.5) < 2.0 ** -15))
+        say("fused boundary", dtype, amax, len(vals))
+        _, x8, dx = _cq().cq_gemm_a8_fused(w, _x(torch_dev, _encode(row, dtype), dtype), y_dtype=torch_dev.float32)
+        assert np.array_equal(dx.cpu().numpy(), d_ref.astype(np.float32))
+        assert np.array_equal(x8.cpu().numpy(), x8_ref), (dtype, amax)
+    assert hits >= 48
