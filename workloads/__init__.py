@@ -182,3 +182,29 @@ def synthetic_representation(seed: int, n: int, k: int, bits: int, group: int, s
     a_bits = to_f16_bits(shapes[pick, 0])
     b_bits = to_f16_bits(shapes[pick, 1])
     return codes, scale, a_bits, b_bits
+
+
+# ---------------------------------------------------------------- routed (mixture-of-experts) inputs
+
+# Mixtral-8x7B-shaped expert layers (K, N) with 8 experts, top-2 routing.
+MOE_LAYERS = (("expert_gate_up", 4096, 28672), ("expert_down", 14336, 4096))
+MOE_EXPERTS = 8
+MOE_TOPK = 2
+
+
+def route_map(seed: int, tokens: int, experts: int, topk: int, skew: float = 1.0):
+    """Synthetic route map: every token picks topk distinct experts, drawn
+    with Zipf-like popularity 1 / (rank + 1)^skew over a seeded permutation of
+    the experts (so some experts are busier than others).  Returns int32
+    (route_token, route_expert), token-major."""
+    g = rng(seed)
+    pop = 1.0 / np.arange(1, experts + 1) ** skew
+    perm = g.permutation(experts)
+    p = np.empty(experts)
+    p[perm] = pop / pop.sum()
+    toks, exps = [], []
+    for t in range(tokens):
+        picks = g.choice(experts, size=min(topk, experts), replace=False, p=p)
+        toks.extend([t] * len(picks))
+        exps.extend(picks.tolist())
+    return np.asarray(toks, dtype=np.int32), np.asarray(exps, dtype=np.int32)
