@@ -181,6 +181,36 @@ cq_status cq_gemm_a8_fused(const cq_weight *w, const void *x, cq_dtype x_dtype, 
                            int8_t *x8, float *dx, void *y, cq_dtype y_dtype, void *stream);
 
 /*
+ * cq_gemm_routed_model_dtype -- routed (mixture-of-experts) product (device).
+ *
+ * Sec. 5.5 (workload regimes and routed execution): for every route
+ * r = (route_token[r], route_expert[r]) of a route map supplied by the
+ * caller, y[r] = x[route_token[r]] W_e^T with W_e = expert route_expert[r]
+ * of the bank, in the model-dtype arithmetic of cq_gemm_model_dtype (FP32
+ * products and accumulation).  Outputs are route-major; routing weights and
+ * expert choice stay with the caller.  Routes are grouped by expert on the
+ * device (no host synchronisation), and every decoded weight tile serves all
+ * routes of its expert.
+ *   bank          n_experts experts of equal shape stacked along the rows:
+ *                 bank->n is the row count of ONE expert, and codes, scale, a
+ *                 and b hold n_experts * bank->n rows (expert e first at row
+ *                 e * bank->n).  B <= 5 (otherwise CQ_ERR_UNSUPPORTED).
+ *   x             device [tokens, K] in x_dtype (CQ_BF16 or CQ_FP16).
+ *   route_token   device int32 [routes]; route_expert  device int32 [routes].
+ *                 Routes naming a token outside [0, tokens) or an expert
+ *                 outside [0, n_experts) are dropped: their rows of y are not
+ *                 written.
+ *   workspace     device int32 [n_experts + 1 + routes], caller-owned scratch
+ *                 (expert offsets and the grouped route order).
+ *   y             device [routes, bank->n] in y_dtype: x_dtype or CQ_FP32.
+ * Deterministic: a route's output does not depend on the other routes.
+ */
+cq_status cq_gemm_routed_model_dtype(const cq_weight *bank, int32_t n_experts, const void *x,
+                                     cq_dtype x_dtype, int64_t tokens, const int32_t *route_token,
+                                     const int32_t *route_expert, int64_t routes, int32_t *workspace,
+                                     void *y, cq_dtype y_dtype, void *stream);
+
+/*
  * Row-regime kernel selection (Sec. 5.5-5.6).  Each path picks the GEMV
  * family for m <= its threshold and the tiled GEMM family above it.  The
  * defaults come from measurements on MI355X.  cq_set_gemv_max_rows

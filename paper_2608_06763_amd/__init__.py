@@ -7,7 +7,8 @@ GPU; calling a device entry point does, and a missing library raises.
 
 Entry points (same names as the C ABI):
   cq_pack_groups, cq_decode_ref, cq_gemm_model_dtype, cq_quantize_act_a8,
-  cq_gemm_a8, cq_gemm_a8_fused, cq_set_gemv_max_rows, cq_get_gemv_max_rows
+  cq_gemm_a8, cq_gemm_a8_fused, cq_gemm_routed_model_dtype, cq_set_gemv_max_rows,
+  cq_get_gemv_max_rows
 """
 from __future__ import annotations
 
@@ -24,7 +25,8 @@ STATUS = {0: "CQ_OK", 1: "CQ_ERR_ARG", 2: "CQ_ERR_SHAPE", 3: "CQ_ERR_ALIGN", 4: 
           5: "CQ_ERR_CODE", 6: "CQ_ERR_DTYPE", 7: "CQ_ERR_HIP", 8: "CQ_ERR_UNSUPPORTED"}
 
 EXPORTS = ("cq_status_str", "cq_pack_groups", "cq_decode_ref", "cq_gemm_model_dtype", "cq_quantize_act_a8",
-           "cq_gemm_a8", "cq_gemm_a8_fused", "cq_set_gemv_max_rows", "cq_get_gemv_max_rows")
+           "cq_gemm_a8", "cq_gemm_a8_fused", "cq_gemm_routed_model_dtype", "cq_set_gemv_max_rows",
+           "cq_get_gemv_max_rows")
 
 
 class CQError(RuntimeError):
@@ -65,6 +67,9 @@ def lib() -> ctypes.CDLL:
     L.cq_gemm_a8.argtypes = [ctypes.POINTER(cq_weight), vp, vp, i64, vp, ctypes.c_int, vp, vp]
     L.cq_gemm_a8_fused.restype = ctypes.c_int
     L.cq_gemm_a8_fused.argtypes = [ctypes.POINTER(cq_weight), vp, ctypes.c_int, i64, vp, vp, vp, ctypes.c_int, vp]
+    L.cq_gemm_routed_model_dtype.restype = ctypes.c_int
+    L.cq_gemm_routed_model_dtype.argtypes = [ctypes.POINTER(cq_weight), i32, vp, ctypes.c_int, i64, vp, vp, i64, vp, vp,
+                                             ctypes.c_int, vp]
     L.cq_set_gemv_max_rows.restype = ctypes.c_int
     L.cq_set_gemv_max_rows.argtypes = [i32, i64]
     L.cq_get_gemv_max_rows.restype = i64
@@ -233,6 +238,29 @@ def cq_gemm_a8_fused(w: CQWeight, x, y_dtype=None, out=None, x8=None, dx=None, s
                                 out.data_ptr(), _dt(out.dtype), _stream_ptr(stream))
     _check(st, "cq_gemm_a8_fused")
     return out, x8, dx
+
+
+def cq_gemm_routed_model_dtype(bank: CQWeight, n_experts: int, x, route_token, route_expert, y_dtype=None, out=None,
+                               workspace=None, stream=None):
+    """Route-major routed product; ``bank`` stacks n_experts experts along its rows."""
+    torch = _torch()
+    assert x.dim() == 2 and x.shape[1] == bank.k and x.is_contiguous()
+    assert bank.n % n_experts == 0
+    n = bank.n // n_experts
+    routes = route_token.numel()
+    assert route_expert.numel() == routes and route_token.dtype == torch.int32 and route_expert.dtype == torch.int32
+    y_dtype = y_dtype or x.dtype
+    if out is None:
+        out = torch.empty((routes, n), dtype=y_dtype, device=x.device)
+    if workspace is None:
+        workspace = torch.empty((n_experts + 1 + routes,), dtype=torch.int32, device=x.device)
+    desc = cq_weight(bank.bits, bank.group, n, bank.k, bank.codes.data_ptr(), bank.scale.data_ptr(), bank.a.data_ptr(),
+                     bank.b.data_ptr())
+    st = lib().cq_gemm_routed_model_dtype(ctypes.byref(desc), n_experts, x.data_ptr(), _dt(x.dtype), x.shape[0],
+                                          route_token.data_ptr(), route_expert.data_ptr(), routes, workspace.data_ptr(),
+                                          out.data_ptr(), _dt(out.dtype), _stream_ptr(stream))
+    _check(st, "cq_gemm_routed_model_dtype")
+    return out
 
 
 def cq_set_gemv_max_rows(path: int, max_rows: int):

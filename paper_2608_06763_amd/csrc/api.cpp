@@ -194,6 +194,28 @@ cq_status cq_gemm_a8_fused(const cq_weight *w, const void *x, cq_dtype x_dtype, 
     return cq_gemm_a8(w, x8, dx, m, y, y_dtype, nullptr, stream);
 }
 
+cq_status cq_gemm_routed_model_dtype(const cq_weight *bank, int32_t n_experts, const void *x, cq_dtype x_dtype,
+                                     int64_t tokens, const int32_t *route_token, const int32_t *route_expert,
+                                     int64_t routes, int32_t *workspace, void *y, cq_dtype y_dtype, void *stream) {
+    const cq_status st = check_weight(bank);
+    if (st != CQ_OK) return st;
+    if (n_experts < 1 || tokens < 1 || routes < 0) return CQ_ERR_ARG;
+    if (!x || !route_token || !route_expert || !workspace || !y) return CQ_ERR_ARG;
+    if (x_dtype != CQ_BF16 && x_dtype != CQ_FP16) return CQ_ERR_DTYPE;
+    if (y_dtype != x_dtype && y_dtype != CQ_FP32) return CQ_ERR_DTYPE;
+    if (!aligned16(x) || !aligned16(y)) return CQ_ERR_ALIGN;
+    if ((reinterpret_cast<uintptr_t>(route_token) | reinterpret_cast<uintptr_t>(route_expert) |
+         reinterpret_cast<uintptr_t>(workspace)) % 4)
+        return CQ_ERR_ALIGN;
+    if (bank->n > (int64_t(1) << 40) / bank->k / n_experts) return CQ_ERR_SHAPE;
+    if (tokens > (int64_t(1) << 40) / bank->k || routes > (int64_t(1) << 40) / bank->n) return CQ_ERR_SHAPE;
+    if (!cq::routed_supported(*bank, n_experts, tokens, routes)) return CQ_ERR_UNSUPPORTED;
+    if (routes == 0) return CQ_OK;
+    return hip_status(cq::launch_routed_model_dtype(*bank, n_experts, x, int(x_dtype), tokens, route_token,
+                                                    route_expert, routes, workspace, y, int(y_dtype),
+                                                    static_cast<hipStream_t>(stream)));
+}
+
 cq_status cq_set_gemv_max_rows(int32_t path, int64_t max_rows) {
     if (path != 0 && path != 1) return CQ_ERR_ARG;
     g_gemv_max_rows[path].store(max_rows < 0 ? -1 : max_rows, std::memory_order_relaxed);

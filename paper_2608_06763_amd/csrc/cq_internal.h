@@ -57,6 +57,14 @@ hipError_t launch_gemv_a8(const cq_weight &w, const int8_t *x8, const float *dx,
 // Dynamic-A8 single-row streaming GEMV (m == 1, B in {1, 2, 4}, no partials dump).
 bool gemv_a8_stream_supported(const cq_weight &w, int64_t m);
 bool gemv_a8_fused_supported(const cq_weight &w, int64_t m);
+bool gemv_a16_routed_supported(const cq_weight &w, int64_t tokens);
+hipError_t launch_gemv_a16_routed(const cq_weight &w, int n_experts, const void *x, int x_dt, int64_t tokens,
+                                  const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
+                                  int y_dt, hipStream_t stream);
+bool routed_supported(const cq_weight &w, int64_t n_experts, int64_t tokens, int64_t routes);
+hipError_t launch_routed_model_dtype(const cq_weight &w, int n_experts, const void *x, int x_dt, int64_t tokens,
+                                     const int32_t *token, const int32_t *expert, int64_t routes, int32_t *workspace,
+                                     void *y, int y_dt, hipStream_t stream);
 hipError_t launch_gemv_a8_fused(const cq_weight &w, const void *x, int x_dt, int8_t *x8_out, float *dx_out, void *y,
                                 int y_dt, hipStream_t stream);
 hipError_t launch_gemv_a8_stream(const cq_weight &w, const int8_t *x8, const float *dx, void *y, int y_dt,

@@ -55,7 +55,8 @@ __device__ __forceinline__ void wave_lds_order() {
 // l % 16) and store rows < m of the 16-row strip.
 template <int YDT>
 __device__ __forceinline__ void reduce_store(float (*red)[16][17], const float v[4], int lane, int wave, int nwaves,
-                                             int n0, int n, int m, const float *row_factor, void *y) {
+                                             int n0, int n, int m, const float *row_factor, void *y,
+                                             const int *out_row = nullptr) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) red[wave][4 * (lane >> 4) + i][lane & 15] = v[i];
     __syncthreads();
@@ -65,10 +66,20 @@ __device__ __forceinline__ void reduce_store(float (*red)[16][17], const float v
             float s = 0.f;
             for (int w = 0; w < nwaves; ++w) s += red[w][r][c];
             if (row_factor) s *= row_factor[r];
-            store_out<YDT>(y, int64_t(r) * n + n0 + c, s);
+            store_out<YDT>(y, int64_t(out_row ? out_row[r] : r) * n + n0 + c, s);
         }
     }
 }
+
+// Route map of a routed product, grouped by expert (see routed.hip).  The
+// routed kernel keeps its route chunk state in registers: at most 8 waves.
+constexpr int kMaxRoutedWaves = 8;
+struct route_groups {
+    const int32_t *token;    // [R] activation row of each route
+    const int32_t *order;    // route ids grouped by expert
+    const int32_t *offsets;  // [E + 1] first entry of each expert in order
+    int strips;              // 16-row strips per expert
+};
 
 }  // namespace
 
@@ -172,11 +183,15 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
 
 // ---------------------------------------------------------------- model dtype, B <= 5
 
-template <int B, int UPG, int XDT, int YDT>
-__global__ void __launch_bounds__(1024) gemv_a16_narrow(
+// ROUTED: a bank of experts of n rows each, stacked; block b serves strip
+// b % strips of expert b / strips for all routes of that expert, 16 routes
+// (gathered activation rows) at a time; outputs are route-major rows.  x then
+// has m rows (tokens).
+template <int B, int UPG, int XDT, int YDT, bool ROUTED>
+__global__ void __launch_bounds__(ROUTED ? 64 * kMaxRoutedWaves : 1024) gemv_a16_narrow(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
-    int n, int k, const uint16_t *__restrict__ x, int m, void *__restrict__ y) {
+    int n, int k, const uint16_t *__restrict__ x, int m, void *__restrict__ y, route_groups rg) {
     constexpr int M = max_code(B);
     constexpr int NE = 1 << B;
     constexpr int EPT = NE >= 4 ? NE / 4 : 1;
@@ -184,23 +199,37 @@ __global__ void __launch_bounds__(1024) gemv_a16_narrow(
     __shared__ float red[kMaxWaves][16][17];
     __shared__ uint32_t tab[kMaxWaves][16 * TSTR];
 
+    __shared__ int out_row[16];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int nwaves = blockDim.x >> 6;
-    const int n0 = blockIdx.x * 16;
+    const int ng = k / (32 * UPG);
+    const uint32_t row_bytes = uint32_t(k) * B / 8u;
+    int strip = blockIdx.x, r_begin = 0, r_end = m;
+    if constexpr (ROUTED) {
+        const int e = blockIdx.x / rg.strips;
+        strip = blockIdx.x % rg.strips;
+        r_begin = rg.offsets[e];
+        r_end = rg.offsets[e + 1];
+        codes += size_t(e) * n * row_bytes;
+        scale += size_t(e) * n * ng;
+        a16 += size_t(e) * n * ng;
+        b16 += size_t(e) * n * ng;
+    }
+    const int n0 = strip * 16;
     const int col = lane & 15;
     const int part = lane >> 4;
     const int wrow = n0 + col;
     const bool wok = wrow < n;
-    const bool xok = col < m;
-    const int ng = k / (32 * UPG);
-    const uint32_t row_bytes = uint32_t(k) * B / 8u;
     const auto rc = make_rsrc(codes, uint32_t(n) * row_bytes);
     const auto rs = make_rsrc(scale, uint32_t(n) * ng * 4u);
     const auto ra = make_rsrc(a16, uint32_t(n) * ng * 2u);
     const auto rb = make_rsrc(b16, uint32_t(n) * ng * 2u);
     const auto rx = make_rsrc(x, uint32_t(m) * uint32_t(k) * 2u);
     uint32_t *mytab = tab[wave] + col * TSTR;
+    // activation row of this lane's MFMA row in the current chunk of routes
+    int xrow = col;
+    bool xok = col < m;
 
     // Items are (group, batch of at most four units); a wave walks the items
     // of its groups g = wave, wave + 4, ... and requests the next item's codes,
@@ -240,11 +269,11 @@ __global__ void __launch_bounds__(1024) gemv_a16_narrow(
             const uint32_t byte0 = uint32_t(wrow) * row_bytes + u * (4u * B) + part_byte;
             load_words<2>(rc, wok ? (byte0 & ~3u) : kOobOffset, st.cw[q]);
             uint32_t xv[4];
-            load_words<4>(rx, xok ? (uint32_t(col) * uint32_t(k) + u * 32u + 8u * part) * 2u : kOobOffset, xv);
+            load_words<4>(rx, xok ? (uint32_t(xrow) * uint32_t(k) + u * 32u + 8u * part) * 2u : kOobOffset, xv);
             st.xa[q] = u32x4_t{xv[0], xv[1], xv[2], xv[3]};
         }
     };
-    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    f32x4_t acc;
     auto process = [&](int it, const Stage &st) {
         if (it % NB == 0) {
             // the row's level table: lane part of the row writes fields part, part + 4, ...
@@ -302,17 +331,33 @@ __global__ void __launch_bounds__(1024) gemv_a16_narrow(
             }
         }
     };
-    Stage s0, s1;
-    if (items > 0) load(0, s0);
-    for (int it = 0; it < items; it += 2) {
-        if (it + 1 < items) load(it + 1, s1);
-        process(it, s0);
-        if (it + 1 >= items) break;
-        if (it + 2 < items) load(it + 2, s0);
-        process(it + 1, s1);
+    auto run_rows = [&](int mc) {
+        acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        Stage s0, s1;
+        if (items > 0) load(0, s0);
+        for (int it = 0; it < items; it += 2) {
+            if (it + 1 < items) load(it + 1, s1);
+            process(it, s0);
+            if (it + 1 >= items) break;
+            if (it + 2 < items) load(it + 2, s0);
+            process(it + 1, s1);
+        }
+        const float v[4] = {acc[0], acc[1], acc[2], acc[3]};
+        reduce_store<YDT>(red, v, lane, wave, nwaves, n0, n, mc, nullptr, y, ROUTED ? out_row : nullptr);
+    };
+    if constexpr (ROUTED) {
+        for (int j = r_begin; j < r_end; j += 16) {
+            const int mc = min(16, r_end - j);
+            const int rid = col < mc ? rg.order[j + col] : 0;
+            xrow = col < mc ? rg.token[rid] : 0;
+            xok = col < mc;
+            if (threadIdx.x < 16) out_row[threadIdx.x] = threadIdx.x < mc ? rg.order[j + threadIdx.x] : 0;
+            run_rows(mc);
+            __syncthreads();  // red, the tables and out_row are reused by the next chunk
+        }
+    } else {
+        run_rows(m);
     }
-    const float v[4] = {acc[0], acc[1], acc[2], acc[3]};
-    reduce_store<YDT>(red, v, lane, wave, nwaves, n0, n, m, nullptr, y);
 }
 
 // ---------------------------------------------------------------- launchers
@@ -368,8 +413,9 @@ hipError_t launch_gemv_a8_narrow(const cq_weight &w, const int8_t *x8, const flo
 template <int B, int UPG, int XDT, int YDT>
 static hipError_t a16_narrow_launch(const cq_weight &w, const void *x, int64_t m, void *y, hipStream_t stream) {
     const int64_t blocks = (w.n + 15) / 16;
-    hipLaunchKernelGGL((gemv_a16_narrow<B, UPG, XDT, YDT>), dim3(unsigned(blocks)), dim3(64 * narrow_waves(w)), 0, stream, w.codes,
-                       w.scale, w.a, w.b, int(w.n), int(w.k), static_cast<const uint16_t *>(x), int(m), y);
+    hipLaunchKernelGGL((gemv_a16_narrow<B, UPG, XDT, YDT, false>), dim3(unsigned(blocks)), dim3(64 * narrow_waves(w)), 0,
+                       stream, w.codes, w.scale, w.a, w.b, int(w.n), int(w.k), static_cast<const uint16_t *>(x), int(m), y,
+                       route_groups{});
     return hipGetLastError();
 }
 
@@ -400,6 +446,63 @@ static hipError_t a16_narrow_bits(const cq_weight &w, const void *x, int64_t m, 
 bool gemv_a16_narrow_supported(const cq_weight &w, int64_t m) {
     return m >= 2 && m <= 16 && w.bits <= 5 && stream_fits(w.n, w.k, w.bits, w.group) &&
            m * w.k * 2 < (int64_t(1) << 31);
+}
+
+template <int B, int UPG, int XDT, int YDT>
+static hipError_t a16_routed_launch(const cq_weight &w, int n_experts, const void *x, int64_t tokens,
+                                    const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
+                                    hipStream_t stream) {
+    const int strips = int((w.n + 15) / 16);
+    const int64_t blocks = int64_t(strips) * n_experts;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((gemv_a16_narrow<B, UPG, XDT, YDT, true>), dim3(unsigned(blocks)),
+                       dim3(64 * narrow_waves(w, kMaxRoutedWaves)), 0,
+                       stream, w.codes, w.scale, w.a, w.b, int(w.n), int(w.k), static_cast<const uint16_t *>(x),
+                       int(tokens), y, route_groups{token, order, offsets, strips});
+    return hipGetLastError();
+}
+
+template <int B, int XDT, int YDT>
+static hipError_t a16_routed_group(const cq_weight &w, int n_experts, const void *x, int64_t tokens,
+                                   const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
+                                   hipStream_t stream) {
+    switch (w.group) {
+        case 32: return a16_routed_launch<B, 1, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        case 64: return a16_routed_launch<B, 2, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        case 128: return a16_routed_launch<B, 4, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        case 256: return a16_routed_launch<B, 8, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        case 512: return a16_routed_launch<B, 16, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+    }
+    return hipErrorNotSupported;
+}
+
+template <int XDT, int YDT>
+static hipError_t a16_routed_bits(const cq_weight &w, int n_experts, const void *x, int64_t tokens,
+                                  const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
+                                  hipStream_t stream) {
+    switch (w.bits) {
+        case 1: return a16_routed_group<1, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        case 2: return a16_routed_group<2, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        case 3: return a16_routed_group<3, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        case 4: return a16_routed_group<4, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        case 5: return a16_routed_group<5, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+    }
+    return hipErrorNotSupported;
+}
+
+bool gemv_a16_routed_supported(const cq_weight &w, int64_t tokens) {
+    return w.bits <= 5 && stream_fits(w.n, w.k, w.bits, w.group) && tokens * w.k * 2 < (int64_t(1) << 31);
+}
+
+hipError_t launch_gemv_a16_routed(const cq_weight &w, int n_experts, const void *x, int x_dt, int64_t tokens,
+                                  const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
+                                  int y_dt, hipStream_t stream) {
+    if (x_dt == 0) {
+        if (y_dt == 0) return a16_routed_bits<0, 0>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        return a16_routed_bits<0, 2>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+    }
+    if (y_dt == 1) return a16_routed_bits<1, 1>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+    return a16_routed_bits<1, 2>(w, n_experts, x, tokens, token, order, offsets, y, stream);
 }
 
 hipError_t launch_gemv_a16_narrow(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,

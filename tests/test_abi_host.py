@@ -180,3 +180,23 @@ def test_gemv_threshold_override():
     assert cq.cq_get_gemv_max_rows(0) >= 1
     with pytest.raises(cq.CQError):
         cq.cq_set_gemv_max_rows(2, 1)
+
+
+def test_routed_argument_errors_need_no_gpu():
+    # every argument check of the routed entry returns before any device work
+    L = cq.lib()
+    P = ctypes.c_void_p
+    ok, bad_align = 4096, 4100
+    w = _desc()
+    f = L.cq_gemm_routed_model_dtype
+    assert f(ctypes.byref(_desc(bits=0)), 2, P(ok), 0, 4, P(ok), P(ok), 8, P(ok), P(ok), 0, None) == 1
+    assert f(ctypes.byref(w), 0, P(ok), 0, 4, P(ok), P(ok), 8, P(ok), P(ok), 0, None) == 1      # no experts
+    assert f(ctypes.byref(w), 2, P(ok), 0, 0, P(ok), P(ok), 8, P(ok), P(ok), 0, None) == 1      # no tokens
+    assert f(ctypes.byref(w), 2, P(ok), 0, 4, None, P(ok), 8, P(ok), P(ok), 0, None) == 1       # no route map
+    assert f(ctypes.byref(w), 2, P(ok), 0, 4, P(ok), P(ok), 8, None, P(ok), 0, None) == 1       # no workspace
+    assert f(ctypes.byref(w), 2, P(ok), 2, 4, P(ok), P(ok), 8, P(ok), P(ok), 2, None) == 6      # fp32 x
+    assert f(ctypes.byref(w), 2, P(ok), 0, 4, P(ok), P(ok), 8, P(ok), P(ok), 1, None) == 6      # bf16 -> fp16
+    assert f(ctypes.byref(w), 2, P(bad_align), 0, 4, P(ok), P(ok), 8, P(ok), P(ok), 0, None) == 3
+    assert f(ctypes.byref(w), 2, P(ok), 0, 4, P(ok + 2), P(ok), 8, P(ok), P(ok), 0, None) == 3  # int32 alignment
+    assert f(ctypes.byref(_desc(bits=6)), 2, P(ok), 0, 4, P(ok), P(ok), 8, P(ok), P(ok), 0, None) == 8
+    assert f(ctypes.byref(w), 2, P(ok), 0, 4, P(ok), P(ok), 0, P(ok), P(ok), 0, None) == 0      # no routes

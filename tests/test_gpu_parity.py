@@ -519,3 +519,59 @@ def test_gemm_a8_fused_carriers_near_rounding_boundaries(torch_dev, dtype):
         assert np.array_equal(dx.cpu().numpy(), d_ref.astype(np.float32))
         assert np.array_equal(x8.cpu().numpy(), x8_ref), (dtype, amax)
     assert hits >= 48
+
+
+# ---------------------------------------------------------------- routed (mixture-of-experts) product
+
+
+@pytest.mark.parametrize("bits", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("group", [32, 128])
+@pytest.mark.parametrize("experts,tokens", [(1, 5), (3, 40), (8, 1), (8, 16)])
+def test_routed_model_dtype(torch_dev, bits, group, experts, tokens):
+    # route-major outputs for a skewed top-2 route map (top-1 with one expert);
+    # 37 rows per expert (ragged strip), experts with more than 16 routes run
+    # several chunks; every route against the oracle
+    from oracle import routed as RT
+    from workloads import route_map, synthetic_representation
+    n, k = 37, 1024
+    codes, s, a, b = synthetic_representation(90 + bits, experts * n, k, bits, group)
+    cq = _cq()
+    bank = cq.CQWeight.from_codes(codes, s, a, b, bits, group)
+    tok, exp = route_map(91 + tokens, tokens, experts, 1 if experts == 1 else 2)
+    tt = torch_dev.from_numpy(tok).cuda()
+    te = torch_dev.from_numpy(exp).cuda()
+    for dtype in ("bf16", "fp16"):
+        xb, xv = act(92, tokens, k, dtype)
+        y_ref = RT.routed_model_dtype(xv, tok, exp, codes, bits, group, s, a, b, experts)
+        say("routed", bits, group, experts, tokens, dtype)
+        x = _x(torch_dev, xb, dtype)
+        y = cq.cq_gemm_routed_model_dtype(bank, experts, x, tt, te, y_dtype=torch_dev.float32)
+        assert R.eps_comp(_np(y), y_ref, "fp32") <= 2e-4
+        y16 = cq.cq_gemm_routed_model_dtype(bank, experts, x, tt, te)
+        assert R.eps_comp(_np(y16), y_ref, dtype) <= TOL
+        y2 = cq.cq_gemm_routed_model_dtype(bank, experts, x, tt, te, y_dtype=torch_dev.float32)
+        assert torch_dev.equal(y, y2)
+
+
+def test_routed_invalid_routes_untouched(torch_dev):
+    # routes naming a missing token or expert are dropped; their rows keep
+    # the caller's contents, the others match the oracle
+    from oracle import routed as RT
+    from workloads import synthetic_representation
+    bits, group, experts, n, k, tokens = 4, 128, 4, 20, 512, 6
+    codes, s, a, b = synthetic_representation(95, experts * n, k, bits, group)
+    cq = _cq()
+    bank = cq.CQWeight.from_codes(codes, s, a, b, bits, group)
+    tok = np.array([0, 5, 6, -1, 2, 3, 1], np.int32)
+    exp = np.array([1, 3, 0, 2, 4, -3, 0], np.int32)
+    xb, xv = act(96, tokens, k)
+    y_ref = RT.routed_model_dtype(xv, tok, exp, codes, bits, group, s, a, b, experts)
+    say("routed invalid")
+    y = torch_dev.full((len(tok), n), 7.0, dtype=torch_dev.float32, device="cuda")
+    cq.cq_gemm_routed_model_dtype(bank, experts, _x(torch_dev, xb, "bf16"), torch_dev.from_numpy(tok).cuda(),
+                                  torch_dev.from_numpy(exp).cuda(), out=y)
+    got = _np(y)
+    valid = np.isfinite(y_ref[:, 0])
+    assert list(valid) == [True, True, False, False, False, False, True]
+    assert np.all(got[~valid] == 7.0)
+    assert R.eps_comp(got[valid], y_ref[valid], "fp32") <= 2e-4
