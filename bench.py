@@ -135,6 +135,41 @@ def _cpu_baseline_run(layers_np, bits, group, budget_s, blas_threads):
                       f"product on {blas_threads} BLAS threads"}
 
 
+def routed_sweep(torch, cq, bits=4, group=128, token_counts=(1, 4, 16, 64)):
+    """Routed (mixture-of-experts) product on Mixtral-8x7B-shaped expert layers
+    (8 experts, top-2, skewed synthetic route maps).  The bank replicates one
+    synthetic expert on the device (timing does not depend on the values);
+    effective bytes count the weights of the experts that receive routes."""
+    from workloads import MOE_EXPERTS, MOE_LAYERS, MOE_TOPK, route_map
+    out = []
+    for li, (name, k, n) in enumerate(MOE_LAYERS):
+        w1 = make_weight(cq, 7000 + li, n, k, bits, group)
+        rep = lambda t: t.repeat(MOE_EXPERTS, 1) if t.dim() == 2 else t.repeat(MOE_EXPERTS)
+        banks = [cq.CQWeight(rep(w1.codes), rep(w1.scale), rep(w1.a), rep(w1.b), bits, group, n * MOE_EXPERTS, k)]
+        banks.append(banks[0].clone())  # two banks alternate (together above the 256 MB Infinity Cache)
+        del w1
+        for t in token_counts:
+            tok, exp = route_map(7100 + t, t, MOE_EXPERTS, MOE_TOPK)
+            tt = torch.from_numpy(tok).cuda()
+            te = torch.from_numpy(exp).cuda()
+            x = torch.randn(t, k, device="cuda").to(torch.bfloat16)
+            y = torch.empty((len(tok), n), dtype=torch.bfloat16, device="cuda")
+            ws = torch.empty((MOE_EXPERTS + 1 + len(tok),), dtype=torch.int32, device="cuda")
+            run = lambda i: cq.cq_gemm_routed_model_dtype(banks[i % 2], MOE_EXPERTS, x, tt, te, out=y, workspace=ws)
+            us = graph_timed(torch, run, 8) * 1e3
+            active = len(set(exp.tolist()))
+            eff = active * weight_bytes(n, k, bits, group) + 2 * t * k + 2 * len(tok) * n
+            rec = {"layer": name, "k": k, "n": n, "experts": MOE_EXPERTS, "topk": MOE_TOPK, "tokens": t,
+                   "routes": len(tok), "active_experts": active, "us": round(us, 2),
+                   "effective_gbs": round(eff / us / 1e3, 1), "hbm_frac": round(eff / us / 1e3 / HBM_PEAK_GBS, 4)}
+            out.append(rec)
+            log(f"[routed] {name} T={t} routes={len(tok)} active={active} {us:.2f} us "
+                f"{rec['effective_gbs']:.1f} GB/s")
+        del banks
+        torch.cuda.empty_cache()
+    return out
+
+
 def rows_sweep(torch, cq, bits=4, group=128, k=8192, n=28672, ms=(1, 2, 8, 32, 128, 512, 2048, 8192)):
     from workloads import crossover_act
     w0 = make_weight(cq, 4001, n, k, bits, group)
@@ -382,6 +417,8 @@ def main():
     if not args.no_sweep:
         log("[bench] rows sweep")
         result["rows_sweep"] = rows_sweep(torch, cq)
+        log("[bench] routed sweep")
+        result["routed_sweep"] = routed_sweep(torch, cq)
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
         result["cpu_baseline"] = cpu_baseline(layers_np, bits, group)
