@@ -360,18 +360,19 @@ def main():
                                                  out=y8s[li]), len(copies) * 4)
         # single-row A8 operator in a captured sequence: quantize + GEMV as two
         # launches, and the one-launch call that quantizes inside the GEMV
-        nc = len(copies) * 2
-        tq8 = graph_timed(torch, lambda i: (cq.cq_quantize_act_a8(xs[li], x8s[li], dxs[li]),
-                                            cq.cq_gemm_a8(copies[i % len(copies)][li], x8s[li], dxs[li],
-                                                          out=y8s[li])), nc)
-        tf8 = graph_timed(torch, lambda i: cq.cq_gemm_a8_fused(copies[i % len(copies)][li], xs[li], out=y8s[li],
-                                                               x8=x8s[li], dx=dxs[li]), nc)
         per_layer[name] = {"k": k, "n": n, "model_dtype_us": round(t16 * 1e3, 2),
                            "model_dtype_gbs": round(a16_bytes(m, n, k, bits, group) / t16 / 1e6, 1),
                            "a8_gemv_us": round(t8 * 1e3, 2),
-                           "a8_gemv_gbs": round(a8_bytes(m, n, k, bits, group) / t8 / 1e6, 1),
-                           "a8_quantize_then_gemv_graph_us": round(tq8 * 1e3, 2),
-                           "a8_fused_graph_us": round(tf8 * 1e3, 2)}
+                           "a8_gemv_gbs": round(a8_bytes(m, n, k, bits, group) / t8 / 1e6, 1)}
+        if not args.no_graph:
+            nc = len(copies) * 2
+            tq8 = graph_timed(torch, lambda i: (cq.cq_quantize_act_a8(xs[li], x8s[li], dxs[li]),
+                                                cq.cq_gemm_a8(copies[i % len(copies)][li], x8s[li], dxs[li],
+                                                              out=y8s[li])), nc)
+            tf8 = graph_timed(torch, lambda i: cq.cq_gemm_a8_fused(copies[i % len(copies)][li], xs[li],
+                                                                   out=y8s[li], x8=x8s[li], dx=dxs[li]), nc)
+            per_layer[name]["a8_quantize_then_gemv_graph_us"] = round(tq8 * 1e3, 2)
+            per_layer[name]["a8_fused_graph_us"] = round(tf8 * 1e3, 2)
 
     if args.copy_calibration:
         src = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
