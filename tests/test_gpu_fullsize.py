@@ -174,3 +174,50 @@ def test_fullsize_fitted_slice_partials(torch_dev):
         dx = torch_dev.from_numpy(d_ref).cuda()
         _, parts = cq.cq_gemm_a8(wt, x8, dx, y_dtype=torch_dev.float32, want_partials=True)
         assert np.array_equal(parts.cpu().numpy(), p_ref)
+
+
+@pytest.mark.parametrize("layer", range(4))
+def test_fullsize_fused_a8_decode_layers(torch_dev, layer):
+    # the benchmark's single-row fused A8 call on each decode layer: carriers
+    # and d_x bit-exact, 96 sampled output rows against the A8 oracle
+    name, k, n = LLAMA8B_LAYERS[layer]
+    codes, s, a, b = synthetic_representation(2000 + layer, n, k, 4, 128)
+    cq = _cq()
+    w = cq.CQWeight.from_codes(codes, s, a, b, 4, 128)
+    xb = llama8b_act(1, k, layer)
+    xv = bf16_bits_to_f32(xb).astype(np.float64)
+    rows = _sample(31 + layer, 96, n)
+    say("fused a8", name)
+    y, x8, dx = cq.cq_gemm_a8_fused(w, _dev_x(torch_dev, xb), y_dtype=torch_dev.float32)
+    x8_ref, d_ref = A8.quantize_act(xv)
+    assert np.array_equal(x8.cpu().numpy(), x8_ref)
+    assert np.array_equal(dx.cpu().numpy(), d_ref.astype(np.float32))
+    y_ref, _ = _ref_a8_rows(x8_ref, d_ref, codes, s, a, b, 4, 128, rows)
+    assert _eps(y.cpu().numpy()[:, rows], y_ref, "fp32") <= 1e-5
+
+
+@pytest.mark.parametrize("layer", range(2))
+@pytest.mark.parametrize("tokens", [1, 16, 64])
+def test_fullsize_routed_mixtral_experts(torch_dev, layer, tokens):
+    # the routed sweep's configuration: a bank of 8 copies of one synthetic
+    # expert (as the benchmark builds it), top-2 skewed routes; every route's
+    # output on 48 sampled columns against the oracle
+    from workloads import MOE_EXPERTS, MOE_LAYERS, MOE_TOPK, route_map
+    name, k, n = MOE_LAYERS[layer]
+    codes, s, a, b = synthetic_representation(7000 + layer, n, k, 4, 128)
+    cq = _cq()
+    w1 = cq.CQWeight.from_codes(codes, s, a, b, 4, 128)
+    rep = lambda t: t.repeat(MOE_EXPERTS, 1) if t.dim() == 2 else t.repeat(MOE_EXPERTS)
+    bank = cq.CQWeight(rep(w1.codes), rep(w1.scale), rep(w1.a), rep(w1.b), 4, 128, n * MOE_EXPERTS, k)
+    tok, exp = route_map(7100 + tokens, tokens, MOE_EXPERTS, MOE_TOPK)
+    xb = llama8b_act(tokens, k, 5)
+    xv = bf16_bits_to_f32(xb).astype(np.float64)
+    cols = _sample(41 + tokens, 48, n)
+    say("routed fullsize", name, tokens)
+    y = cq.cq_gemm_routed_model_dtype(bank, MOE_EXPERTS, _dev_x(torch_dev, xb), torch_dev.from_numpy(tok).cuda(),
+                                      torch_dev.from_numpy(exp).cuda(), y_dtype=torch_dev.float32)
+    y_ref = _ref_rows(xv[tok], codes, s, a, b, 4, 128, cols)
+    assert _eps(y.cpu().numpy()[:, cols], y_ref, "fp32") <= 2e-4
+    y16 = cq.cq_gemm_routed_model_dtype(bank, MOE_EXPERTS, _dev_x(torch_dev, xb), torch_dev.from_numpy(tok).cuda(),
+                                        torch_dev.from_numpy(exp).cuda())
+    assert _eps(y16.float().cpu().numpy()[:, cols], y_ref, "bf16") <= TOL
