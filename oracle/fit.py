@@ -1,4 +1,5 @@
-"""Continuous groupwise reference fitter (Sec. 4.1), float64.
+"""Groupwise reference fitters, float64: the continuous fitter (Sec. 4.1) and
+the carrier-aware joint fitter (Sec. 4.3, ``fit_joint``).
 
 TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
 
@@ -69,6 +70,10 @@ def _load():
                                                   ctypes.c_int, ctypes.c_int, p, ctypes.c_int, ctypes.c_int,
                                                   p, p, p]
         lib.cq_oracle_assign_serialized.argtypes = [p, ctypes.c_int64, ctypes.c_int, ctypes.c_int, p, p, p, p, p]
+        lib.cq_oracle_eval_candidates_joint.argtypes = lib.cq_oracle_eval_candidates.argtypes
+        lib.cq_oracle_assign_serialized_joint.argtypes = [p, ctypes.c_int64, ctypes.c_int, ctypes.c_int, p, p, p, p, p,
+                                                          p, p]
+        lib.cq_oracle_carriers.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_double, p]
         _lib = lib
     return _lib
 
@@ -107,9 +112,10 @@ class FitResult:
         return float(np.sqrt(self.sse.sum() / np.sum(w * w)))
 
 
-def _refine(wg, bits, g, inc_a, inc_b, inc_sse, inc_s, step, clips, iters):
+def _refine(wg, bits, g, inc_a, inc_b, inc_sse, inc_s, step, clips, iters, joint=False):
     """One 3x3 local refinement around each group's incumbent."""
     lib = _load()
+    scorer = lib.cq_oracle_eval_candidates_joint if joint else lib.cq_oracle_eval_candidates
     ng = wg.shape[0]
     offs = [(da, db) for da in (-1, 0, 1) for db in (-1, 0, 1) if (da, db) != (0, 0)]
     ca = np.empty((ng, len(offs)))
@@ -124,8 +130,8 @@ def _refine(wg, bits, g, inc_a, inc_b, inc_sse, inc_s, step, clips, iters):
     clips_a = np.asarray(clips, dtype=np.float64)
     ca = np.ascontiguousarray(ca)
     cb = np.ascontiguousarray(cb)
-    lib.cq_oracle_eval_candidates(_ptr(wg), ng, g, bits, _ptr(ca), _ptr(cb), _ptr(valid), len(offs), 0,
-                                  _ptr(clips_a), len(clips_a), iters, _ptr(idx), _ptr(sse), _ptr(s))
+    scorer(_ptr(wg), ng, g, bits, _ptr(ca), _ptr(cb), _ptr(valid), len(offs), 0,
+           _ptr(clips_a), len(clips_a), iters, _ptr(idx), _ptr(sse), _ptr(s))
     better = (idx >= 0) & (sse < inc_sse)
     rows = np.nonzero(better)[0]
     inc_a = inc_a.copy()
@@ -200,3 +206,129 @@ def fit(w, bits: int, group: int, candidates=None, refine_steps=(0.05, 0.02),
     assert np.all(np.abs(codes.astype(np.int64)) <= max_code(bits))
     return FitResult(codes.reshape(n, k), s32.reshape(n, -1), a_bits.reshape(n, -1),
                      b_bits.reshape(n, -1), sse_ser.reshape(n, -1))
+
+
+# ---------------------------------------------------------------- carrier-aware joint fit (Sec. 4.3)
+
+
+@dataclass
+class JointFitResult:
+    codes: np.ndarray      # int8 [N, K]
+    scale: np.ndarray      # float32 [N, K/G]
+    a_bits: np.ndarray     # uint16 [N, K/G]
+    b_bits: np.ndarray     # uint16 [N, K/G]
+    loss_c: np.ndarray     # float64 [N, K/G], L_C of the serialized representation
+    loss_a8: np.ndarray    # float64 [N, K/G], L_A8 of the serialized representation
+
+    def nrmse_joint(self, w) -> float:
+        """eq. carrier-aware-nrmse: sqrt((L_C + L_A8) / (2 sum w^2))."""
+        w = np.asarray(w, dtype=np.float64)
+        return float(np.sqrt((self.loss_c.sum() + self.loss_a8.sum()) / (2.0 * np.sum(w * w))))
+
+    def nrmse_a8(self, w) -> float:
+        """The A8-only diagnostic sqrt(L_A8 / sum w^2)."""
+        w = np.asarray(w, dtype=np.float64)
+        return float(np.sqrt(self.loss_a8.sum() / np.sum(w * w)))
+
+
+def carriers_c(bits: int, a: float, b: float) -> np.ndarray:
+    """The C scorer's integer-exact carriers r(0..M) for one FP16 shape pair."""
+    out = np.empty(max_code(bits) + 1, np.int32)
+    if _load().cq_oracle_carriers(bits, float(a), float(b), _ptr(out)):
+        raise ValueError("bits must be 2..8")
+    return out
+
+
+def joint_loss(w, codes, bits: int, group: int, scale, a_bits, b_bits):
+    """(L_C, L_A8) per group of a given representation (eq. continuous-and-carrier-loss),
+    from the oracle's exact carrier table."""
+    from .a8 import carrier_table
+    from .format import decode
+    w = np.asarray(w, dtype=np.float64)
+    n, k = w.shape
+    wc = decode(codes, bits, group, scale, a_bits, b_bits)
+    m = 1 if bits == 1 else max_code(bits)
+    ng = k // group
+    wa = np.empty_like(wc)
+    cache = {}
+    for r in range(n):
+        for g in range(ng):
+            key = (int(a_bits[r, g]), int(b_bits[r, g]))
+            if key not in cache:
+                cache[key] = carrier_table(bits, *key)
+            tab = cache[key]
+            kk = codes[r, g * group:(g + 1) * group].astype(np.int64)
+            mag = np.abs(kk) if bits > 1 else np.ones_like(kk)
+            car = np.array([tab[i] for i in mag], np.float64)
+            wa[r, g * group:(g + 1) * group] = np.sign(kk) * float(scale[r, g]) * car / 127.0
+    lc = ((w - wc) ** 2).reshape(n, ng, group).sum(axis=2)
+    la = ((w - wa) ** 2).reshape(n, ng, group).sum(axis=2)
+    return lc, la
+
+
+def fit_joint(w, bits: int, group: int, candidates=None, refine_steps=(0.05, 0.02),
+              clips=CLIPS, iters=ITERS) -> JointFitResult:
+    """Carrier-aware joint fit of every [1, G] group (Sec. 4.3): the same
+    candidate traversal as ``fit``, scoring L_C + L_A8 (eq.
+    carrier-aware-objective) with the joint assignment and closed-form scale,
+    then the final joint assignment under the stored FP32 scale, FP16 shapes
+    and their exact carriers.  W1 levels already lie on the carrier grid
+    (L_C = L_A8), so W1 keeps the continuous fit."""
+    from .a8 import carrier_table
+    w = np.ascontiguousarray(np.asarray(w, dtype=np.float32))
+    n, k = w.shape
+    if k % group:
+        raise ValueError("K must be a multiple of G")
+    if bits == 1:
+        r = fit(w, bits, group)
+        return JointFitResult(r.codes, r.scale, r.a_bits, r.b_bits, r.sse, r.sse.copy())
+    ng = n * (k // group)
+    wg = w.reshape(ng, group)
+    zero = np.all(wg == 0, axis=1)
+    lib = _load()
+    if bits == 2:
+        ca, cb = np.array([1.0]), np.array([0.0])
+        steps = ()
+    elif candidates is None:
+        ca, cb = coarse_candidates()
+        steps = refine_steps
+    else:
+        ca, cb = (np.asarray(c, dtype=np.float64) for c in candidates)
+        steps = refine_steps
+    valid = np.ones(len(ca), np.uint8)
+    idx = np.empty(ng, np.int32)
+    loss = np.empty(ng)
+    s = np.empty(ng)
+    clips_a = np.asarray(clips, dtype=np.float64)
+    rc = lib.cq_oracle_eval_candidates_joint(_ptr(wg), ng, group, bits, _ptr(np.ascontiguousarray(ca)),
+                                             _ptr(np.ascontiguousarray(cb)), _ptr(valid), len(ca), 1,
+                                             _ptr(clips_a), len(clips_a), iters, _ptr(idx), _ptr(loss), _ptr(s))
+    if rc:
+        raise RuntimeError("oracle candidate scorer rejected its arguments")
+    inc_a, inc_b = ca[idx], cb[idx]
+    for step in steps:
+        inc_a, inc_b, loss, s = _refine(wg, bits, group, inc_a, inc_b, loss, s, step, clips, iters, joint=True)
+
+    s32 = s.astype(np.float32)
+    s32[zero] = 0
+    inc_a = np.where(zero, 1.0, inc_a)
+    inc_b = np.where(zero, 0.0, inc_b)
+    a_bits = f64_to_f16_bits(inc_a)
+    b_bits = f64_to_f16_bits(inc_b)
+    m = max_code(bits)
+    car = np.empty((ng, m + 1), np.int32)
+    cache = {}
+    for gi in range(ng):
+        key = (int(a_bits[gi]), int(b_bits[gi]))
+        if key not in cache:
+            cache[key] = carrier_table(bits, *key)
+        car[gi] = cache[key]
+    codes = np.empty((ng, group), np.int8)
+    lc = np.empty(ng)
+    la = np.empty(ng)
+    lib.cq_oracle_assign_serialized_joint(_ptr(wg), ng, group, bits, _ptr(s32), _ptr(np.ascontiguousarray(inc_a)),
+                                          _ptr(np.ascontiguousarray(inc_b)), _ptr(car), _ptr(codes), _ptr(lc),
+                                          _ptr(la))
+    assert np.all(np.abs(codes.astype(np.int64)) <= m)
+    return JointFitResult(codes.reshape(n, k), s32.reshape(n, -1), a_bits.reshape(n, -1), b_bits.reshape(n, -1),
+                          lc.reshape(n, -1), la.reshape(n, -1))

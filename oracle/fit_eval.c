@@ -164,3 +164,142 @@ int cq_oracle_assign_serialized(const float *w, int64_t ngroups, int g, int bits
     }
     return 0;
 }
+
+/* ------------------------------------------------------------------ joint
+ * Carrier-aware joint objective (Sec. 4.3, eq. carrier-aware-objective):
+ * L_C + L_A8 with the continuous levels z_i = q(i/M) and the carrier levels
+ * zt_i = RNE(127 z_i) / 127 (eq. carrier-grid), the carrier rounded from the
+ * exact rational value of the FP16 shapes.  Codes take the argmin of
+ * (u - s z_i)^2 + (u - s zt_i)^2 over i (eq. carrier-aware-assignment, ties
+ * to the smaller magnitude), the scale the closed form
+ * s = sum u (z + zt) / sum (z^2 + zt^2) (eq. carrier-aware-scale).
+ */
+
+/* RNE(127 q(i/m)) from FP16 shape values a, b: with A = 2^24 a and
+ * Bq = 2^24 b (integers, FP16 values being multiples of 2^-24) and
+ * C = 2^24 - A - Bq, 127 q(i/m) = 127 (A i m^2 + Bq i^2 m + C i^3) / (2^24 m^3),
+ * an exact rational with an int64 numerator for m <= 127. */
+static int carrier_exact(int i, int m, double a, double b) {
+    const int64_t A = (int64_t)llround(a * 16777216.0), Bq = (int64_t)llround(b * 16777216.0);
+    const int64_t C = ((int64_t)1 << 24) - A - Bq;
+    const int64_t ii = i, mm = m;
+    const int64_t num = 127 * (A * ii * mm * mm + Bq * ii * ii * mm + C * ii * ii * ii);
+    const int64_t den = ((int64_t)1 << 24) * mm * mm * mm;
+    /* nearest integer to num / den, ties to even (num >= 0 for admissible shapes) */
+    int64_t qt = num / den, r = num - qt * den;
+    if (r < 0) { qt -= 1; r += den; }
+    if (2 * r > den || (2 * r == den && (qt & 1))) qt += 1;
+    return (int)qt;
+}
+
+int cq_oracle_carriers(int bits, double a, double b, int32_t *out) {
+    if (bits < 2 || bits > 8) return 1;
+    int m = (1 << (bits - 1)) - 1;
+    for (int i = 0; i <= m; ++i) out[i] = carrier_exact(i, m, a, b);
+    return 0;
+}
+
+static void make_joint_levels(int m, double a, double b, double *z, double *zt) {
+    make_levels(m, a, b, z);
+    for (int i = 0; i <= m; ++i) zt[i] = (double)carrier_exact(i, m, a, b) / 127.0;
+}
+
+static int assign_joint(double u, double s, const double *z, const double *zt, int m) {
+    int best = 0;
+    double bc = INFINITY;
+    for (int i = 0; i <= m; ++i) {
+        double e1 = u - s * z[i], e2 = u - s * zt[i];
+        double c = e1 * e1 + e2 * e2;
+        if (c < bc) { bc = c; best = i; }
+    }
+    return best;
+}
+
+static double score_joint(const double *u, int g, int m, double a, double b, const double *clips, int nclips,
+                          int iters, double umax, double *s_out) {
+    double z[MAXLEV + 1], zt[MAXLEV + 1];
+    make_joint_levels(m, a, b, z, zt);
+    double best = INFINITY, best_s = 0.0;
+    for (int ci = 0; ci < nclips; ++ci) {
+        double s = clips[ci] * umax;
+        for (int it = 0; it <= iters; ++it) {
+            double num = 0.0, den = 0.0, loss = 0.0;
+            for (int j = 0; j < g; ++j) {
+                int i = assign_joint(u[j], s, z, zt, m);
+                num += u[j] * (z[i] + zt[i]);
+                den += z[i] * z[i] + zt[i] * zt[i];
+                double e1 = u[j] - s * z[i], e2 = u[j] - s * zt[i];
+                loss += e1 * e1 + e2 * e2;
+            }
+            if (it == iters) {
+                if (loss < best) { best = loss; best_s = s; }
+            } else if (den > 0.0) {
+                s = num / den;
+            }
+        }
+    }
+    *s_out = best_s;
+    return best;
+}
+
+/* As cq_oracle_eval_candidates, scoring L_C + L_A8. */
+int cq_oracle_eval_candidates_joint(const float *w, int64_t ngroups, int g, int bits,
+                                    const double *cand_a, const double *cand_b,
+                                    const uint8_t *valid, int ncand, int shared,
+                                    const double *clips, int nclips, int iters,
+                                    int32_t *best_idx, double *best_loss, double *best_s) {
+    if (bits < 2 || bits > 8 || g <= 0 || g > 4096) return 1;
+    int m = (1 << (bits - 1)) - 1;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t gi = 0; gi < ngroups; ++gi) {
+        double u[4096];
+        double umax = 0.0;
+        for (int j = 0; j < g; ++j) {
+            u[j] = fabs((double)w[gi * g + j]);
+            if (u[j] > umax) umax = u[j];
+        }
+        int32_t bi = -1;
+        double bl = INFINITY, bs = 0.0;
+        for (int c = 0; c < ncand; ++c) {
+            int64_t off = shared ? c : gi * (int64_t)ncand + c;
+            if (!valid[off]) continue;
+            double s;
+            double l = score_joint(u, g, m, cand_a[off], cand_b[off], clips, nclips, iters, umax, &s);
+            if (l < bl) { bl = l; bs = s; bi = c; }
+        }
+        best_idx[gi] = bi;
+        best_loss[gi] = bl;
+        best_s[gi] = bs;
+    }
+    return 0;
+}
+
+/* Final joint assignment under the stored FP32 scale and FP16 shapes, with the
+ * carriers given per group (carriers[gi * (m + 1) + i], from the caller's
+ * exact carrier table).  Returns the signed codes and, per group, L_C and L_A8. */
+int cq_oracle_assign_serialized_joint(const float *w, int64_t ngroups, int g, int bits,
+                                      const float *s, const double *a, const double *b,
+                                      const int32_t *carriers, int8_t *codes, double *lc_out, double *la8_out) {
+    if (bits < 2 || bits > 8 || g <= 0) return 1;
+    int m = (1 << (bits - 1)) - 1;
+#pragma omp parallel for schedule(static)
+    for (int64_t gi = 0; gi < ngroups; ++gi) {
+        double z[MAXLEV + 1], zt[MAXLEV + 1];
+        make_levels(m, a[gi], b[gi], z);
+        for (int i = 0; i <= m; ++i) zt[i] = (double)carriers[gi * (int64_t)(m + 1) + i] / 127.0;
+        double sc = (double)s[gi], lc = 0.0, la = 0.0;
+        for (int j = 0; j < g; ++j) {
+            double wv = (double)w[gi * g + j];
+            double u = fabs(wv);
+            int i = (sc > 0.0) ? assign_joint(u, sc, z, zt, m) : 0;
+            int k = (wv > 0.0) ? i : (wv < 0.0 ? -i : 0);
+            codes[gi * g + j] = (int8_t)k;
+            double e1 = u - sc * z[i], e2 = u - sc * zt[i];
+            lc += e1 * e1;
+            la += e2 * e2;
+        }
+        lc_out[gi] = lc;
+        la8_out[gi] = la;
+    }
+    return 0;
+}
