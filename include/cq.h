@@ -181,6 +181,33 @@ cq_status cq_gemm_a8_fused(const cq_weight *w, const void *x, cq_dtype x_dtype, 
                            int8_t *x8, float *dx, void *y, cq_dtype y_dtype, void *stream);
 
 /*
+ * cq_build_carriers -- load-time INT8 carrier tables (device).
+ *
+ * Sec. 4.3 eq. carrier, precomputed once per weight (the interior carriers
+ * of Sec. 5.2): for every (row, group) the table holds r(i) = RNE(127 q(i/M))
+ * for i = 0 .. 2^(B-1) - 1, exact from the FP16 shapes (r(0) = 0, r(M) = 127),
+ * one int8 each.  It depends only on (a, b): codes and metadata are unchanged.
+ *   carriers  device int8 [N, K/G, 2^(B-1)], 16-byte aligned (caller-owned).
+ *             W1 has no table (its carriers are +-127): nothing is written and
+ *             carriers may be NULL.
+ */
+cq_status cq_build_carriers(const cq_weight *w, int8_t *carriers, void *stream);
+
+/*
+ * cq_gemm_a8_carriers -- Dynamic-A8 product with load-time carriers (device).
+ *
+ * Same result as cq_gemm_a8 (without the partials dump), bit for bit: the
+ * kernels read the carriers of cq_build_carriers for the same weight instead
+ * of forming them (the many-row W4 matrix-core GEMM and the generic kernels
+ * of the other widths; the W4 single- and narrow-row kernels keep their
+ * register decode, which gives the same carriers).
+ *   carriers  the table of cq_build_carriers (NULL allowed for W1).
+ * Errors as cq_gemm_a8.
+ */
+cq_status cq_gemm_a8_carriers(const cq_weight *w, const int8_t *carriers, const int8_t *x8,
+                              const float *dx, int64_t m, void *y, cq_dtype y_dtype, void *stream);
+
+/*
  * cq_gemm_routed_model_dtype -- routed (mixture-of-experts) product (device).
  *
  * Sec. 5.5 (workload regimes and routed execution): for every route

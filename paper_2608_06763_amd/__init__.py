@@ -7,8 +7,8 @@ GPU; calling a device entry point does, and a missing library raises.
 
 Entry points (same names as the C ABI):
   cq_pack_groups, cq_decode_ref, cq_gemm_model_dtype, cq_quantize_act_a8,
-  cq_gemm_a8, cq_gemm_a8_fused, cq_gemm_routed_model_dtype, cq_set_gemv_max_rows,
-  cq_get_gemv_max_rows
+  cq_gemm_a8, cq_gemm_a8_fused, cq_build_carriers, cq_gemm_a8_carriers,
+  cq_gemm_routed_model_dtype, cq_set_gemv_max_rows, cq_get_gemv_max_rows
 """
 from __future__ import annotations
 
@@ -25,8 +25,8 @@ STATUS = {0: "CQ_OK", 1: "CQ_ERR_ARG", 2: "CQ_ERR_SHAPE", 3: "CQ_ERR_ALIGN", 4: 
           5: "CQ_ERR_CODE", 6: "CQ_ERR_DTYPE", 7: "CQ_ERR_HIP", 8: "CQ_ERR_UNSUPPORTED"}
 
 EXPORTS = ("cq_status_str", "cq_pack_groups", "cq_decode_ref", "cq_gemm_model_dtype", "cq_quantize_act_a8",
-           "cq_gemm_a8", "cq_gemm_a8_fused", "cq_gemm_routed_model_dtype", "cq_set_gemv_max_rows",
-           "cq_get_gemv_max_rows")
+           "cq_gemm_a8", "cq_gemm_a8_fused", "cq_build_carriers", "cq_gemm_a8_carriers",
+           "cq_gemm_routed_model_dtype", "cq_set_gemv_max_rows", "cq_get_gemv_max_rows")
 
 
 class CQError(RuntimeError):
@@ -67,6 +67,10 @@ def lib() -> ctypes.CDLL:
     L.cq_gemm_a8.argtypes = [ctypes.POINTER(cq_weight), vp, vp, i64, vp, ctypes.c_int, vp, vp]
     L.cq_gemm_a8_fused.restype = ctypes.c_int
     L.cq_gemm_a8_fused.argtypes = [ctypes.POINTER(cq_weight), vp, ctypes.c_int, i64, vp, vp, vp, ctypes.c_int, vp]
+    L.cq_build_carriers.restype = ctypes.c_int
+    L.cq_build_carriers.argtypes = [ctypes.POINTER(cq_weight), vp, vp]
+    L.cq_gemm_a8_carriers.restype = ctypes.c_int
+    L.cq_gemm_a8_carriers.argtypes = [ctypes.POINTER(cq_weight), vp, vp, vp, i64, vp, ctypes.c_int, vp]
     L.cq_gemm_routed_model_dtype.restype = ctypes.c_int
     L.cq_gemm_routed_model_dtype.argtypes = [ctypes.POINTER(cq_weight), i32, vp, ctypes.c_int, i64, vp, vp, i64, vp, vp,
                                              ctypes.c_int, vp]
@@ -238,6 +242,30 @@ def cq_gemm_a8_fused(w: CQWeight, x, y_dtype=None, out=None, x8=None, dx=None, s
                                 out.data_ptr(), _dt(out.dtype), _stream_ptr(stream))
     _check(st, "cq_gemm_a8_fused")
     return out, x8, dx
+
+
+def cq_build_carriers(w: CQWeight, out=None, stream=None):
+    """Load-time carrier table int8 [N, K/G, 2^(B-1)] (None for W1)."""
+    torch = _torch()
+    if w.bits == 1:
+        return None
+    if out is None:
+        out = torch.empty((w.n, w.k // w.group, 1 << (w.bits - 1)), dtype=torch.int8, device=w.codes.device)
+    _check(lib().cq_build_carriers(ctypes.byref(w.desc), out.data_ptr(), _stream_ptr(stream)), "cq_build_carriers")
+    return out
+
+
+def cq_gemm_a8_carriers(w: CQWeight, carriers, x8, dx, y_dtype=None, out=None, stream=None):
+    torch = _torch()
+    assert x8.dim() == 2 and x8.shape[1] == w.k and x8.is_contiguous()
+    m = x8.shape[0]
+    y_dtype = y_dtype or torch.bfloat16
+    if out is None:
+        out = torch.empty((m, w.n), dtype=y_dtype, device=x8.device)
+    st = lib().cq_gemm_a8_carriers(ctypes.byref(w.desc), carriers.data_ptr() if carriers is not None else None,
+                                   x8.data_ptr(), dx.data_ptr(), m, out.data_ptr(), _dt(out.dtype), _stream_ptr(stream))
+    _check(st, "cq_gemm_a8_carriers")
+    return out
 
 
 def cq_gemm_routed_model_dtype(bank: CQWeight, n_experts: int, x, route_token, route_expert, y_dtype=None, out=None,

@@ -216,6 +216,30 @@ cq_status cq_gemm_routed_model_dtype(const cq_weight *bank, int32_t n_experts, c
                                                     static_cast<hipStream_t>(stream)));
 }
 
+cq_status cq_build_carriers(const cq_weight *w, int8_t *carriers, void *stream) {
+    const cq_status st = check_weight(w);
+    if (st != CQ_OK) return st;
+    if (w->bits == 1) return CQ_OK;  // W1 carriers are +-127: no table
+    if (!carriers) return CQ_ERR_ARG;
+    if (!aligned16(carriers)) return CQ_ERR_ALIGN;
+    return hip_status(cq::launch_build_carriers(*w, carriers, static_cast<hipStream_t>(stream)));
+}
+
+cq_status cq_gemm_a8_carriers(const cq_weight *w, const int8_t *carriers, const int8_t *x8, const float *dx,
+                              int64_t m, void *y, cq_dtype y_dtype, void *stream) {
+    const cq_status st = check_weight(w);
+    if (st != CQ_OK) return st;
+    if (!x8 || !dx || !y || m < 1 || (w->bits > 1 && !carriers)) return CQ_ERR_ARG;
+    if (y_dtype != CQ_BF16 && y_dtype != CQ_FP16 && y_dtype != CQ_FP32) return CQ_ERR_DTYPE;
+    if (!aligned16(x8) || !aligned16(dx) || !aligned16(y) || (carriers && !aligned16(carriers))) return CQ_ERR_ALIGN;
+    if (m > (int64_t(1) << 40) / w->k || m > (int64_t(1) << 40) / w->n) return CQ_ERR_SHAPE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (m <= gemv_max_rows(1) && m <= cq::kGemvMaxRows)
+        return hip_status(cq::launch_gemv_a8_tab(*w, carriers, x8, dx, m, y, int(y_dtype), s));
+    if (m > int64_t(65535) * 64) return CQ_ERR_SHAPE;
+    return hip_status(cq::launch_gemm_a8_tab(*w, carriers, x8, dx, m, y, int(y_dtype), s));
+}
+
 cq_status cq_set_gemv_max_rows(int32_t path, int64_t max_rows) {
     if (path != 0 && path != 1) return CQ_ERR_ARG;
     g_gemv_max_rows[path].store(max_rows < 0 ? -1 : max_rows, std::memory_order_relaxed);

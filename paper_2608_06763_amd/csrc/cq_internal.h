@@ -62,6 +62,14 @@ hipError_t launch_gemv_a16_routed(const cq_weight &w, int n_experts, const void 
                                   const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
                                   int y_dt, hipStream_t stream);
 bool routed_supported(const cq_weight &w, int64_t n_experts, int64_t tokens, int64_t routes);
+int carrier_table_bytes(int bits);
+hipError_t launch_build_carriers(const cq_weight &w, int8_t *out, hipStream_t stream);
+hipError_t launch_gemv_a8_tab(const cq_weight &w, const int8_t *ctab, const int8_t *x8, const float *dx, int64_t m,
+                              void *y, int y_dt, hipStream_t stream);
+hipError_t launch_gemm_a8_tab(const cq_weight &w, const int8_t *ctab, const int8_t *x8, const float *dx, int64_t m,
+                              void *y, int y_dt, hipStream_t stream);
+hipError_t launch_gemm_a8_mfma_tab(const cq_weight &w, const int8_t *ctab, const int8_t *x8, const float *dx,
+                                   int64_t m, void *y, int y_dt, hipStream_t stream);
 hipError_t launch_routed_model_dtype(const cq_weight &w, int n_experts, const void *x, int x_dt, int64_t tokens,
                                      const int32_t *token, const int32_t *expert, int64_t routes, int32_t *workspace,
                                      void *y, int y_dt, hipStream_t stream);

@@ -31,7 +31,8 @@ __global__ void __launch_bounds__(256) gemm_a8_tiled(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
     int group, int64_t n, int64_t k, const int8_t *__restrict__ x8, const float *__restrict__ dx, int64_t m,
-    void *__restrict__ y, int32_t *__restrict__ partials) {
+    void *__restrict__ y, int32_t *__restrict__ partials, const int8_t *__restrict__ ctab) {
+    // ctab: optional load-time carrier table, 2^(B-1) bytes per (row, group)
     constexpr int M = max_code(B);
     constexpr int STRIDE = KS + 16;  // bytes per LDS row, padded
     __shared__ __attribute__((aligned(16))) int8_t As[BM * STRIDE];
@@ -67,7 +68,8 @@ __global__ void __launch_bounds__(256) gemm_a8_tiled(
                 int c = 0;
                 if (row < n) {
                     const int64_t gi = row * ng + g;
-                    c = exact_carrier(i, M, double(f16_to_f32(a16[gi])), double(f16_to_f32(b16[gi])));
+                    c = ctab ? int(ctab[gi * (M + 1) + i])
+                             : exact_carrier(i, M, double(f16_to_f32(a16[gi])), double(f16_to_f32(b16[gi])));
                     c = c > 127 ? 127 : (c < -127 ? -127 : c);
                 }
                 tab[r * TAB + i] = int8_t(c);
@@ -188,30 +190,30 @@ __global__ void __launch_bounds__(256) gemm_a8_tiled(
 
 template <int B, int YDT>
 static hipError_t run_tiled(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
-                            int32_t *partials, hipStream_t stream) {
+                            int32_t *partials, const int8_t *ctab, hipStream_t stream) {
     const int64_t gx = (w.n + BN - 1) / BN, gy = (m + BM - 1) / BM;
     if (gx > 0x7fffffff || gy > 65535) return hipErrorInvalidValue;
     if (w.group % 64 == 0)
         hipLaunchKernelGGL((gemm_a8_tiled<B, 64, YDT>), dim3(unsigned(gx), unsigned(gy)), dim3(256), 0, stream,
-                           w.codes, w.scale, w.a, w.b, w.group, w.n, w.k, x8, dx, m, y, partials);
+                           w.codes, w.scale, w.a, w.b, w.group, w.n, w.k, x8, dx, m, y, partials, ctab);
     else
         hipLaunchKernelGGL((gemm_a8_tiled<B, 32, YDT>), dim3(unsigned(gx), unsigned(gy)), dim3(256), 0, stream,
-                           w.codes, w.scale, w.a, w.b, w.group, w.n, w.k, x8, dx, m, y, partials);
+                           w.codes, w.scale, w.a, w.b, w.group, w.n, w.k, x8, dx, m, y, partials, ctab);
     return hipGetLastError();
 }
 
 template <int YDT>
 static hipError_t dispatch_bits(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
-                                int32_t *partials, hipStream_t stream) {
+                                int32_t *partials, const int8_t *ctab, hipStream_t stream) {
     switch (w.bits) {
-        case 1: return run_tiled<1, YDT>(w, x8, dx, m, y, partials, stream);
-        case 2: return run_tiled<2, YDT>(w, x8, dx, m, y, partials, stream);
-        case 3: return run_tiled<3, YDT>(w, x8, dx, m, y, partials, stream);
-        case 4: return run_tiled<4, YDT>(w, x8, dx, m, y, partials, stream);
-        case 5: return run_tiled<5, YDT>(w, x8, dx, m, y, partials, stream);
-        case 6: return run_tiled<6, YDT>(w, x8, dx, m, y, partials, stream);
-        case 7: return run_tiled<7, YDT>(w, x8, dx, m, y, partials, stream);
-        case 8: return run_tiled<8, YDT>(w, x8, dx, m, y, partials, stream);
+        case 1: return run_tiled<1, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+        case 2: return run_tiled<2, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+        case 3: return run_tiled<3, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+        case 4: return run_tiled<4, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+        case 5: return run_tiled<5, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+        case 6: return run_tiled<6, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+        case 7: return run_tiled<7, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+        case 8: return run_tiled<8, YDT>(w, x8, dx, m, y, partials, ctab, stream);
     }
     return hipErrorInvalidValue;
 }
@@ -219,9 +221,17 @@ static hipError_t dispatch_bits(const cq_weight &w, const int8_t *x8, const floa
 hipError_t launch_gemm_a8(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
                           int32_t *partials, hipStream_t stream) {
     if (gemm_a8_mfma_supported(w, m)) return launch_gemm_a8_mfma(w, x8, dx, m, y, y_dt, partials, stream);
-    if (y_dt == 0) return dispatch_bits<0>(w, x8, dx, m, y, partials, stream);
-    if (y_dt == 1) return dispatch_bits<1>(w, x8, dx, m, y, partials, stream);
-    return dispatch_bits<2>(w, x8, dx, m, y, partials, stream);
+    if (y_dt == 0) return dispatch_bits<0>(w, x8, dx, m, y, partials, nullptr, stream);
+    if (y_dt == 1) return dispatch_bits<1>(w, x8, dx, m, y, partials, nullptr, stream);
+    return dispatch_bits<2>(w, x8, dx, m, y, partials, nullptr, stream);
+}
+
+hipError_t launch_gemm_a8_tab(const cq_weight &w, const int8_t *ctab, const int8_t *x8, const float *dx, int64_t m,
+                              void *y, int y_dt, hipStream_t stream) {
+    if (gemm_a8_mfma_supported(w, m)) return launch_gemm_a8_mfma_tab(w, ctab, x8, dx, m, y, y_dt, stream);
+    if (y_dt == 0) return dispatch_bits<0>(w, x8, dx, m, y, nullptr, ctab, stream);
+    if (y_dt == 1) return dispatch_bits<1>(w, x8, dx, m, y, nullptr, ctab, stream);
+    return dispatch_bits<2>(w, x8, dx, m, y, nullptr, ctab, stream);
 }
 
 }  // namespace cq

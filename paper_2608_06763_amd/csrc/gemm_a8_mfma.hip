@@ -88,12 +88,16 @@ __device__ __forceinline__ void interleave_step() {
 
 }  // namespace
 
-template <int WM, int WN, int UPG, int YDT, bool DUMP>
+// TB: the carriers come from a load-time table (8 bytes per (row, group),
+// r(0) .. r(7), which is the table TA itself) instead of being evaluated from
+// (a, b); the schedule is unchanged.
+template <int WM, int WN, int UPG, int YDT, bool DUMP, bool TB>
 __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
     int n, int k, const int8_t *__restrict__ x8, const float *__restrict__ dx, int m,
-    void *__restrict__ y, int32_t *__restrict__ partials, int tiles_m, int tiles_n) {
+    void *__restrict__ y, int32_t *__restrict__ partials, int tiles_m, int tiles_n,
+    const int8_t *__restrict__ ctab) {
     constexpr int M = 7;
     constexpr int TM = 64 * WM;             // rows of x per tile
     constexpr int TN = 64 * WN;             // rows of W per tile
@@ -136,6 +140,7 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
     const auto rs = make_rsrc(scale, uint32_t(n) * ng * 4u);
     const auto ra = make_rsrc(a16, uint32_t(n) * ng * 2u);
     const auto rb = make_rsrc(b16, uint32_t(n) * ng * 2u);
+    const auto rt = make_rsrc(ctab, TB ? uint32_t(n) * ng * 8u : 0u);
     const auto rx = make_rsrc(x8, uint32_t(m) * uint32_t(k));
 
     // loader roles: Q adjacent threads (one quad or half quad) share a weight row
@@ -179,8 +184,15 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
     };
     auto load_ab = [&](int g) CQ_INLINE {
         const uint32_t gi = uint32_t(wrow) * ng + g;
-        av = load_u16(ra, wok ? gi * 2u : kOobOffset);
-        bv = load_u16(rb, wok ? gi * 2u : kOobOffset);
+        if constexpr (TB) {
+            uint32_t t[2];
+            load_words<2>(rt, wok ? gi * 8u : kOobOffset, t);
+            av = t[0];  // r0 r1 r2 r3
+            bv = t[1];  // r4 r5 r6 r7
+        } else {
+            av = load_u16(ra, wok ? gi * 2u : kOobOffset);
+            bv = load_u16(rb, wok ? gi * 2u : kOobOffset);
+        }
     };
     auto load_scales = [&](int g) CQ_INLINE {
 #pragma unroll
@@ -194,7 +206,13 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
     // near-tie fallback is a branch, kept at the end of a step); the tables
     // are assembled from them by DPP quad moves, branch-free, when needed.
     uint32_t pr[NP];
+    uint32_t tw0 = 0, tw1 = 0;  // TB: the table words of the group whose tables come next
     auto eval_carriers = [&]() CQ_INLINE {
+        if constexpr (TB) {
+            tw0 = av;
+            tw1 = bv;
+            return;
+        }
         const float a = f16_to_f32(uint16_t(av));
         const float b = f16_to_f32(uint16_t(bv));
         const float c = 1.f - a - b;
@@ -205,6 +223,12 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
     };
     uint32_t ta0 = 0, ta1 = 0, tb0 = 0, tb1 = 0;
     auto build_tables = [&]() CQ_INLINE {
+        if constexpr (TB) {
+            ta0 = tw0;
+            ta1 = tw1;
+            w4_negative_table(ta0, ta1, tb0, tb1);
+            return;
+        }
         uint32_t P[4];
         if constexpr (Q == 4) {
             P[0] = quad_bcast<0x00>(pr[0]);
@@ -375,37 +399,38 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
         }
 }
 
-template <int WM, int WN, int UPG, int YDT, bool DUMP>
+template <int WM, int WN, int UPG, int YDT, bool DUMP, bool TB>
 static hipError_t a8_mfma_launch(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
-                                 int32_t *partials, hipStream_t stream) {
+                                 int32_t *partials, const int8_t *ctab, hipStream_t stream) {
     const int tiles_m = int((m + 64 * WM - 1) / (64 * WM));
     const int tiles_n = int((w.n + 64 * WN - 1) / (64 * WN));
     const int64_t nwg = int64_t(tiles_m) * tiles_n;
     if (nwg > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((gemm_a8_w4_mfma<WM, WN, UPG, YDT, DUMP>), dim3(unsigned(nwg)), dim3(64 * WM * WN), 0, stream, w.codes,
-                       w.scale, w.a, w.b, int(w.n), int(w.k), x8, dx, int(m), y, partials, tiles_m, tiles_n);
+    hipLaunchKernelGGL((gemm_a8_w4_mfma<WM, WN, UPG, YDT, DUMP, TB>), dim3(unsigned(nwg)), dim3(64 * WM * WN), 0, stream,
+                       w.codes, w.scale, w.a, w.b, int(w.n), int(w.k), x8, dx, int(m), y, partials, tiles_m, tiles_n,
+                       ctab);
     return hipGetLastError();
 }
 
-template <int YDT>
+template <int YDT, bool TB>
 static hipError_t a8_mfma_group(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
-                                int32_t *partials, hipStream_t stream) {
+                                int32_t *partials, const int8_t *ctab, hipStream_t stream) {
     // The partials dump (a test path) runs four waves per workgroup, which
     // leaves room for its extra registers; the fast path runs eight.
     if (partials) {
         switch (w.group) {
-            case 64: return a8_mfma_launch<2, 2, 2, YDT, true>(w, x8, dx, m, y, partials, stream);
-            case 128: return a8_mfma_launch<2, 2, 4, YDT, true>(w, x8, dx, m, y, partials, stream);
-            case 256: return a8_mfma_launch<2, 2, 8, YDT, true>(w, x8, dx, m, y, partials, stream);
-            case 512: return a8_mfma_launch<2, 2, 16, YDT, true>(w, x8, dx, m, y, partials, stream);
+            case 64: return a8_mfma_launch<2, 2, 2, YDT, true, TB>(w, x8, dx, m, y, partials, ctab, stream);
+            case 128: return a8_mfma_launch<2, 2, 4, YDT, true, TB>(w, x8, dx, m, y, partials, ctab, stream);
+            case 256: return a8_mfma_launch<2, 2, 8, YDT, true, TB>(w, x8, dx, m, y, partials, ctab, stream);
+            case 512: return a8_mfma_launch<2, 2, 16, YDT, true, TB>(w, x8, dx, m, y, partials, ctab, stream);
         }
         return hipErrorNotSupported;
     }
     switch (w.group) {
-        case 64: return a8_mfma_launch<4, 2, 2, YDT, false>(w, x8, dx, m, y, partials, stream);
-        case 128: return a8_mfma_launch<4, 2, 4, YDT, false>(w, x8, dx, m, y, partials, stream);
-        case 256: return a8_mfma_launch<4, 2, 8, YDT, false>(w, x8, dx, m, y, partials, stream);
-        case 512: return a8_mfma_launch<4, 2, 16, YDT, false>(w, x8, dx, m, y, partials, stream);
+        case 64: return a8_mfma_launch<4, 2, 2, YDT, false, TB>(w, x8, dx, m, y, partials, ctab, stream);
+        case 128: return a8_mfma_launch<4, 2, 4, YDT, false, TB>(w, x8, dx, m, y, partials, ctab, stream);
+        case 256: return a8_mfma_launch<4, 2, 8, YDT, false, TB>(w, x8, dx, m, y, partials, ctab, stream);
+        case 512: return a8_mfma_launch<4, 2, 16, YDT, false, TB>(w, x8, dx, m, y, partials, ctab, stream);
     }
     return hipErrorNotSupported;
 }
@@ -418,9 +443,16 @@ bool gemm_a8_mfma_supported(const cq_weight &w, int64_t m) {
 
 hipError_t launch_gemm_a8_mfma(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
                                int32_t *partials, hipStream_t stream) {
-    if (y_dt == 0) return a8_mfma_group<0>(w, x8, dx, m, y, partials, stream);
-    if (y_dt == 1) return a8_mfma_group<1>(w, x8, dx, m, y, partials, stream);
-    return a8_mfma_group<2>(w, x8, dx, m, y, partials, stream);
+    if (y_dt == 0) return a8_mfma_group<0, false>(w, x8, dx, m, y, partials, nullptr, stream);
+    if (y_dt == 1) return a8_mfma_group<1, false>(w, x8, dx, m, y, partials, nullptr, stream);
+    return a8_mfma_group<2, false>(w, x8, dx, m, y, partials, nullptr, stream);
+}
+
+hipError_t launch_gemm_a8_mfma_tab(const cq_weight &w, const int8_t *ctab, const int8_t *x8, const float *dx,
+                                   int64_t m, void *y, int y_dt, hipStream_t stream) {
+    if (y_dt == 0) return a8_mfma_group<0, true>(w, x8, dx, m, y, nullptr, ctab, stream);
+    if (y_dt == 1) return a8_mfma_group<1, true>(w, x8, dx, m, y, nullptr, ctab, stream);
+    return a8_mfma_group<2, true>(w, x8, dx, m, y, nullptr, ctab, stream);
 }
 
 }  // namespace cq

@@ -20,7 +20,8 @@ __global__ void __launch_bounds__(256) gemv_a8_generic(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
     int group, int64_t n, int64_t k, const int8_t *__restrict__ x8, const float *__restrict__ dx, int m_rows,
-    void *__restrict__ y, int32_t *__restrict__ partials) {
+    void *__restrict__ y, int32_t *__restrict__ partials, const int8_t *__restrict__ ctab) {
+    // ctab: optional load-time carrier table, 2^(B-1) bytes per (row, group)
     constexpr int M = max_code(B);
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -49,7 +50,7 @@ __global__ void __launch_bounds__(256) gemv_a8_generic(
                 gidx = row * ng + u / upg;
                 s = scale[gidx];
                 double a = 1.0, b = 0.0;
-                if constexpr (B > 2) {
+                if (B > 2 && !ctab) {
                     a = double(f16_to_f32(a16[gidx]));
                     b = double(f16_to_f32(b16[gidx]));
                 }
@@ -61,7 +62,9 @@ __global__ void __launch_bounds__(256) gemv_a8_generic(
                         r = code * 127;
                     } else {
                         const int mag = code < 0 ? -code : code;
-                        int c = (B == 2) ? (mag ? 127 : 0) : exact_carrier(mag, M, a, b);
+                        int c;
+                        if constexpr (B == 2) c = mag ? 127 : 0;
+                        else c = ctab ? int(ctab[gidx * (M + 1) + mag]) : exact_carrier(mag, M, a, b);
                         c = c > 127 ? 127 : (c < -127 ? -127 : c);
                         r = code < 0 ? -c : c;
                     }
@@ -102,36 +105,36 @@ __global__ void __launch_bounds__(256) gemv_a8_generic(
 
 template <int B, int MR, int YDT>
 static hipError_t run_generic(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
-                              int32_t *partials, hipStream_t stream) {
+                              int32_t *partials, const int8_t *ctab, hipStream_t stream) {
     int64_t blocks = (w.n + 3) / 4;
     if (blocks > 8192) blocks = 8192;
     hipLaunchKernelGGL((gemv_a8_generic<B, MR, YDT>), dim3(unsigned(blocks)), dim3(256), 0, stream, w.codes,
-                       w.scale, w.a, w.b, w.group, w.n, w.k, x8, dx, int(m), y, partials);
+                       w.scale, w.a, w.b, w.group, w.n, w.k, x8, dx, int(m), y, partials, ctab);
     return hipGetLastError();
 }
 
 template <int B, int YDT>
 static hipError_t dispatch_rows(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
-                                int32_t *partials, hipStream_t stream) {
-    if (m <= 1) return run_generic<B, 1, YDT>(w, x8, dx, m, y, partials, stream);
-    if (m <= 2) return run_generic<B, 2, YDT>(w, x8, dx, m, y, partials, stream);
-    if (m <= 4) return run_generic<B, 4, YDT>(w, x8, dx, m, y, partials, stream);
-    if (m <= 8) return run_generic<B, 8, YDT>(w, x8, dx, m, y, partials, stream);
-    return run_generic<B, 16, YDT>(w, x8, dx, m, y, partials, stream);
+                                int32_t *partials, const int8_t *ctab, hipStream_t stream) {
+    if (m <= 1) return run_generic<B, 1, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+    if (m <= 2) return run_generic<B, 2, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+    if (m <= 4) return run_generic<B, 4, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+    if (m <= 8) return run_generic<B, 8, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+    return run_generic<B, 16, YDT>(w, x8, dx, m, y, partials, ctab, stream);
 }
 
 template <int YDT>
 static hipError_t dispatch_bits(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
-                                int32_t *partials, hipStream_t stream) {
+                                int32_t *partials, const int8_t *ctab, hipStream_t stream) {
     switch (w.bits) {
-        case 1: return dispatch_rows<1, YDT>(w, x8, dx, m, y, partials, stream);
-        case 2: return dispatch_rows<2, YDT>(w, x8, dx, m, y, partials, stream);
-        case 3: return dispatch_rows<3, YDT>(w, x8, dx, m, y, partials, stream);
-        case 4: return dispatch_rows<4, YDT>(w, x8, dx, m, y, partials, stream);
-        case 5: return dispatch_rows<5, YDT>(w, x8, dx, m, y, partials, stream);
-        case 6: return dispatch_rows<6, YDT>(w, x8, dx, m, y, partials, stream);
-        case 7: return dispatch_rows<7, YDT>(w, x8, dx, m, y, partials, stream);
-        case 8: return dispatch_rows<8, YDT>(w, x8, dx, m, y, partials, stream);
+        case 1: return dispatch_rows<1, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+        case 2: return dispatch_rows<2, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+        case 3: return dispatch_rows<3, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+        case 4: return dispatch_rows<4, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+        case 5: return dispatch_rows<5, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+        case 6: return dispatch_rows<6, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+        case 7: return dispatch_rows<7, YDT>(w, x8, dx, m, y, partials, ctab, stream);
+        case 8: return dispatch_rows<8, YDT>(w, x8, dx, m, y, partials, ctab, stream);
     }
     return hipErrorInvalidValue;
 }
@@ -141,9 +144,20 @@ hipError_t launch_gemv_a8(const cq_weight &w, const int8_t *x8, const float *dx,
     if (partials == nullptr && gemv_a8_stream_supported(w, m)) return launch_gemv_a8_stream(w, x8, dx, y, y_dt, stream);
     if (partials == nullptr && gemv_a8_narrow_supported(w, m))
         return launch_gemv_a8_narrow(w, x8, dx, m, y, y_dt, stream);
-    if (y_dt == 0) return dispatch_bits<0>(w, x8, dx, m, y, partials, stream);
-    if (y_dt == 1) return dispatch_bits<1>(w, x8, dx, m, y, partials, stream);
-    return dispatch_bits<2>(w, x8, dx, m, y, partials, stream);
+    if (y_dt == 0) return dispatch_bits<0>(w, x8, dx, m, y, partials, nullptr, stream);
+    if (y_dt == 1) return dispatch_bits<1>(w, x8, dx, m, y, partials, nullptr, stream);
+    return dispatch_bits<2>(w, x8, dx, m, y, partials, nullptr, stream);
+}
+
+hipError_t launch_gemv_a8_tab(const cq_weight &w, const int8_t *ctab, const int8_t *x8, const float *dx, int64_t m,
+                              void *y, int y_dt, hipStream_t stream) {
+    // W4 single- and narrow-row kernels form their carriers from registers
+    // (the same values); the generic kernel reads the table
+    if (gemv_a8_stream_supported(w, m)) return launch_gemv_a8_stream(w, x8, dx, y, y_dt, stream);
+    if (gemv_a8_narrow_supported(w, m)) return launch_gemv_a8_narrow(w, x8, dx, m, y, y_dt, stream);
+    if (y_dt == 0) return dispatch_bits<0>(w, x8, dx, m, y, nullptr, ctab, stream);
+    if (y_dt == 1) return dispatch_bits<1>(w, x8, dx, m, y, nullptr, ctab, stream);
+    return dispatch_bits<2>(w, x8, dx, m, y, nullptr, ctab, stream);
 }
 
 }  // namespace cq

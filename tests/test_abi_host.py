@@ -200,3 +200,21 @@ def test_routed_argument_errors_need_no_gpu():
     assert f(ctypes.byref(w), 2, P(ok), 0, 4, P(ok + 2), P(ok), 8, P(ok), P(ok), 0, None) == 3  # int32 alignment
     assert f(ctypes.byref(_desc(bits=6)), 2, P(ok), 0, 4, P(ok), P(ok), 8, P(ok), P(ok), 0, None) == 8
     assert f(ctypes.byref(w), 2, P(ok), 0, 4, P(ok), P(ok), 0, P(ok), P(ok), 0, None) == 0      # no routes
+
+
+def test_carrier_table_argument_errors_need_no_gpu():
+    L = cq.lib()
+    P = ctypes.c_void_p
+    ok, bad_align = 4096, 4100
+    w = _desc()
+    assert L.cq_build_carriers(ctypes.byref(_desc(bits=0)), P(ok), None) == 1
+    assert L.cq_build_carriers(ctypes.byref(w), None, None) == 1
+    assert L.cq_build_carriers(ctypes.byref(w), P(bad_align), None) == 3
+    assert L.cq_build_carriers(ctypes.byref(_desc(bits=1)), None, None) == 0        # W1: no table
+    f = L.cq_gemm_a8_carriers
+    assert f(ctypes.byref(w), None, P(ok), P(ok), 1, P(ok), 0, None) == 1            # W4 needs a table
+    assert f(ctypes.byref(w), P(ok), None, P(ok), 1, P(ok), 0, None) == 1
+    assert f(ctypes.byref(w), P(ok), P(ok), P(ok), 0, P(ok), 0, None) == 1           # m = 0
+    assert f(ctypes.byref(w), P(ok), P(ok), P(ok), 1, P(ok), 7, None) == 6
+    assert f(ctypes.byref(w), P(bad_align), P(ok), P(ok), 1, P(ok), 0, None) == 3
+    assert f(ctypes.byref(_desc(group=48)), P(ok), P(ok), P(ok), 1, P(ok), 0, None) == 1

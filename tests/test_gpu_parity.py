@@ -575,3 +575,55 @@ def test_routed_invalid_routes_untouched(torch_dev):
     assert list(valid) == [True, True, False, False, False, False, True]
     assert np.all(got[~valid] == 7.0)
     assert R.eps_comp(got[valid], y_ref[valid], "fp32") <= 2e-4
+
+
+# ---------------------------------------------------------------- load-time carrier tables
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4, 5, 6, 7, 8])
+def test_build_carriers_exact(torch_dev, bits):
+    # every (row, group) entry against the oracle's exact table, on fitted
+    # weights and on shapes searched to sit next to a carrier tie
+    from tests._cases import near_tie_shapes
+    r = fitted(101, 24, 1024, bits, 128)
+    a_bits, b_bits = r.a_bits.copy(), r.b_bits.copy()
+    if bits >= 3:
+        ties = near_tie_shapes(bits, count=16)
+        for i, (a, b) in enumerate(ties):
+            a_bits.flat[i] = a
+            b_bits.flat[i] = b
+    cq = _cq()
+    w = cq.CQWeight.from_codes(r.codes, r.scale, a_bits, b_bits, bits, 128)
+    say("build_carriers", bits)
+    tab = cq.cq_build_carriers(w).cpu().numpy()
+    assert tab.shape == (24, 8, 1 << (bits - 1))
+    cache = {}
+    for row in range(24):
+        for g in range(8):
+            key = (int(a_bits[row, g]), int(b_bits[row, g]))
+            if key not in cache:
+                cache[key] = A8.carrier_table(bits, *key)
+            assert list(tab[row, g].astype(np.int64)) == cache[key], (row, g)
+
+
+@pytest.mark.parametrize("bits", WIDTHS)
+@pytest.mark.parametrize("group", [32, 128, 256])
+@pytest.mark.parametrize("m", [1, 5, 16, 70, 300])
+def test_gemm_a8_carriers_equals_gemm_a8(torch_dev, bits, group, m):
+    # the table-fed product is the same computation: bit-equal to cq_gemm_a8
+    # on every family, and within the A8 bar of the oracle
+    r = fitted(102, 67, 1024, bits, group)
+    xb, xv = act(103 + m, m, 1024)
+    x8_ref, d_ref, y_ref, _ = ref_a8(xv, r, bits, group)
+    cq = _cq()
+    w = _weight(r, bits, group)
+    x8 = torch_dev.from_numpy(x8_ref).cuda()
+    dx = torch_dev.from_numpy(d_ref).cuda()
+    say("gemm_a8_carriers", bits, group, m)
+    tab = cq.cq_build_carriers(w)
+    y = cq.cq_gemm_a8_carriers(w, tab, x8, dx, y_dtype=torch_dev.float32)
+    y0 = cq.cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32)
+    assert torch_dev.equal(y, y0)
+    assert R.eps_comp(_np(y), y_ref, "fp32") <= 1e-5
+    y16 = cq.cq_gemm_a8_carriers(w, tab, x8, dx)
+    assert R.eps_comp(_np(y16), y_ref, "bf16") <= TOL
