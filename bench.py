@@ -174,6 +174,7 @@ def rows_sweep(torch, cq, bits=4, group=128, k=8192, n=28672, ms=(1, 2, 8, 32, 1
     from workloads import crossover_act
     w0 = make_weight(cq, 4001, n, k, bits, group)
     copies = [w0] + [w0.clone() for _ in range(max(1, math.ceil((1 << 30) / w0.nbytes)))]
+    tabs = [cq.cq_build_carriers(c) for c in copies]  # load-time carrier tables, one per copy
     out = []
     for m in ms:
         x = torch.from_numpy(crossover_act(m, k).view(np.int16)).cuda().view(torch.bfloat16)
@@ -184,13 +185,16 @@ def rows_sweep(torch, cq, bits=4, group=128, k=8192, n=28672, ms=(1, 2, 8, 32, 1
         a16 = lambda i: cq.cq_gemm_model_dtype(copies[i % len(copies)], x, out=y)
         quant = lambda i: cq.cq_quantize_act_a8(x, x8, dx)
         a8g = lambda i: cq.cq_gemm_a8(copies[i % len(copies)], x8, dx, out=y)
-        a16(0); quant(0); a8g(0)
+        a8t = lambda i: cq.cq_gemm_a8_carriers(copies[i % len(copies)], tabs[i % len(copies)], x8, dx, out=y)
+        a16(0); quant(0); a8g(0); a8t(0)
         torch.cuda.synchronize()
         t16 = timed(torch, a16, it)
         tq = timed(torch, quant, it)
         t8 = timed(torch, a8g, it)
+        t8t = timed(torch, a8t, it)
         flops = 2.0 * m * n * k
         rec = {"m": m, "a16_ms": t16, "a8_gemm_ms": t8, "a8_quant_ms": tq, "a8_op_ms": t8 + tq,
+               "a8_gemm_tables_ms": t8t, "a8_tables_tops": flops / t8t / 1e9,
                "a16_tflops": flops / t16 / 1e9, "a8_tops": flops / t8 / 1e9,
                "a16_gbs": a16_bytes(m, n, k, bits, group) / t16 / 1e6,
                "a8_gbs": a8_bytes(m, n, k, bits, group) / t8 / 1e6}
@@ -198,9 +202,10 @@ def rows_sweep(torch, cq, bits=4, group=128, k=8192, n=28672, ms=(1, 2, 8, 32, 1
         ai8 = flops / a8_bytes(m, n, k, bits, group)
         rec["a16_roofline_frac"] = (flops / t16 / 1e9) / min(BF16_PEAK_TFLOPS, ai16 * HBM_PEAK_GBS / 1e3)
         rec["a8_roofline_frac"] = (flops / t8 / 1e9) / min(INT8_PEAK_TOPS, ai8 * HBM_PEAK_GBS / 1e3)
+        rec["a8_tables_roofline_frac"] = (flops / t8t / 1e9) / min(INT8_PEAK_TOPS, ai8 * HBM_PEAK_GBS / 1e3)
         out.append(rec)
         log(f"[sweep] m={m} a16 {t16:.3f} ms ({rec['a16_tflops']:.1f} TF) a8 {t8:.3f}+{tq:.3f} ms "
-            f"({rec['a8_tops']:.1f} TOPS)")
+            f"({rec['a8_tops']:.1f} TOPS; {rec['a8_tables_tops']:.1f} with load-time carriers)")
         del x, y, x8, dx
     cross = next((r["m"] for r in out if r["a8_op_ms"] < r["a16_ms"]), None)
     return {"shape": {"k": k, "n": n, "bits": bits, "group": group}, "rows": out, "a8_faster_from_m": cross}
