@@ -88,17 +88,23 @@ __device__ __forceinline__ void interleave_step() {
 
 }  // namespace
 
-// TB: the carriers come from a load-time table (8 bytes per (row, group),
-// r(0) .. r(7), which is the table TA itself) instead of being evaluated from
-// (a, b); the schedule is unchanged.
-template <int WM, int WN, int UPG, int YDT, bool DUMP, bool TB>
-__global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
+// B = 4 or 3.  TB: the carriers come from a load-time table (2^(B-1) bytes per
+// (row, group), r(0) .. r(2^(B-1) - 1), which is the table TA itself) instead
+// of being evaluated from (a, b); the schedule is unchanged.
+//
+// W3: a 3-bit field f indexes the 8-byte pair TA = [r0 r1 r2 r3], TB = [0 -r3
+// -r2 -r1] (f = 4 is the reserved pattern, f = 5..7 are -3..-1) directly, so
+// one byte permute serves four fields once they are spread into bytes.  The
+// 16 codes of a thread per step are 6 bytes, read from an aligned 8-byte
+// window; every thread evaluates the two interior carriers itself.
+template <int B, int WM, int WN, int UPG, int YDT, bool DUMP, bool TB>
+__global__ void __launch_bounds__(64 * WM * WN) gemm_a8_mfma(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
     int n, int k, const int8_t *__restrict__ x8, const float *__restrict__ dx, int m,
     void *__restrict__ y, int32_t *__restrict__ partials, int tiles_m, int tiles_n,
     const int8_t *__restrict__ ctab) {
-    constexpr int M = 7;
+    constexpr int M = max_code(B);
     constexpr int TM = 64 * WM;             // rows of x per tile
     constexpr int TN = 64 * WN;             // rows of W per tile
     constexpr int NT = 64 * WM * WN;        // threads
@@ -110,6 +116,7 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
     constexpr int NP = 4 / Q;               // carrier pairs evaluated per thread
     static_assert(SPG >= 1 && G % kKS == 0, "group must be a multiple of the K step");
     static_assert(Q == 2 || Q == 4, "two or four threads per weight row");
+    static_assert(B == 4 || (B == 3 && Q == 4), "W3 takes four threads per weight row");
     // code words of step s are requested kCodeSlots steps ahead into slot
     // s % kCodeSlots (they stream from HBM); with G < 256 the deeper ring
     // would need a longer unrolled period than the registers allow
@@ -135,12 +142,12 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
     const int wn = (wave % WN) * 64;
 
     const int ng = k / G;
-    const uint32_t row_bytes = uint32_t(k) / 2u;
+    const uint32_t row_bytes = uint32_t(k) * B / 8u;
     const auto rc = make_rsrc(codes, uint32_t(n) * row_bytes);
     const auto rs = make_rsrc(scale, uint32_t(n) * ng * 4u);
     const auto ra = make_rsrc(a16, uint32_t(n) * ng * 2u);
     const auto rb = make_rsrc(b16, uint32_t(n) * ng * 2u);
-    const auto rt = make_rsrc(ctab, TB ? uint32_t(n) * ng * 8u : 0u);
+    const auto rt = make_rsrc(ctab, TB ? uint32_t(n) * ng * (1u << (B - 1)) : 0u);
     const auto rx = make_rsrc(x8, uint32_t(m) * uint32_t(k));
 
     // loader roles: Q adjacent threads (one quad or half quad) share a weight row
@@ -174,8 +181,14 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
     auto load_codes = [&](int st, auto slot_c) CQ_INLINE {
         constexpr int SL = decltype(slot_c)::value;
         const uint32_t kk = uint32_t(st) * kKS;
-        load_words<CPT / 8>(rc, wok ? uint32_t(wrow) * row_bytes + (kk + uint32_t(CPT * lq)) / 2u : kOobOffset,
-                            cw[SL]);
+        if constexpr (B == 4) {
+            load_words<CPT / 8>(rc, wok ? uint32_t(wrow) * row_bytes + (kk + uint32_t(CPT * lq)) / 2u : kOobOffset,
+                                cw[SL]);
+        } else {
+            // the 6 code bytes of this thread inside an aligned 8-byte window
+            const uint32_t off = uint32_t(st) * (kKS * 3 / 8) + ((6u * uint32_t(lq)) & ~3u);
+            load_words<2>(rc, wok ? uint32_t(wrow) * row_bytes + off : kOobOffset, cw[SL]);
+        }
     };
     auto load_acts = [&](int st, auto slot_c) CQ_INLINE {
         constexpr int SL = decltype(slot_c)::value;
@@ -184,11 +197,13 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
     };
     auto load_ab = [&](int g) CQ_INLINE {
         const uint32_t gi = uint32_t(wrow) * ng + g;
-        if constexpr (TB) {
+        if constexpr (TB && B == 4) {
             uint32_t t[2];
             load_words<2>(rt, wok ? gi * 8u : kOobOffset, t);
             av = t[0];  // r0 r1 r2 r3
             bv = t[1];  // r4 r5 r6 r7
+        } else if constexpr (TB) {
+            av = __builtin_amdgcn_raw_buffer_load_b32(rt, wok ? gi * 4u : kOobOffset, 0, 0);  // r0 r1 r2 r3
         } else {
             av = load_u16(ra, wok ? gi * 2u : kOobOffset);
             bv = load_u16(rb, wok ? gi * 2u : kOobOffset);
@@ -217,12 +232,23 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
         const float b = f16_to_f32(uint16_t(bv));
         const float c = 1.f - a - b;
         const float mg = carrier_margin(a, b, c);
+        if constexpr (B == 3) {
+            // r1, r2 (r0 = 0, r3 = 127)
+            pr[0] = carrier_u8<M>(1, 1.f / 3.f, a, b, c, mg) | (carrier_u8<M>(2, 2.f / 3.f, a, b, c, mg) << 8);
+            return;
+        }
 #pragma unroll
         for (int j = 0; j < NP; ++j)
             pr[j] = carrier_u8<M>(ip0[j], tp0[j], a, b, c, mg) | (carrier_u8<M>(ip0[j] + 1, tp1[j], a, b, c, mg) << 8);
     };
     uint32_t ta0 = 0, ta1 = 0, tb0 = 0, tb1 = 0;
     auto build_tables = [&]() CQ_INLINE {
+        if constexpr (B == 3) {
+            ta0 = TB ? tw0 : ((pr[0] << 8) | 0x7f000000u);  // r0 r1 r2 r3
+            const uint32_t neg = (0x80808080u - ta0) ^ 0x80808080u;  // 0 -r1 -r2 -r3
+            tb0 = perm(neg, neg, 0x01020300u);                      // 0 -r3 -r2 -r1
+            return;
+        }
         if constexpr (TB) {
             ta0 = tw0;
             ta1 = tw1;
@@ -257,8 +283,18 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
     auto store_codes = [&](int buf, auto slot_c) CQ_INLINE {
         constexpr int SL = decltype(slot_c)::value;
         uint32_t cr[CPT / 4];
+        if constexpr (B == 4) {
 #pragma unroll
-        for (int i = 0; i < CPT / 8; ++i) w4_word_carriers(cw[SL][i], ta0, ta1, tb0, tb1, cr[2 * i], cr[2 * i + 1]);
+            for (int i = 0; i < CPT / 8; ++i) w4_word_carriers(cw[SL][i], ta0, ta1, tb0, tb1, cr[2 * i], cr[2 * i + 1]);
+        } else {
+            const uint64_t win = ((uint64_t(cw[SL][1]) << 32) | cw[SL][0]) >> (8u * ((6u * uint32_t(lq)) & 3u));
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t x = uint32_t(win >> (12 * q)) & 0xfffu;  // four 3-bit fields
+                const uint32_t sel = (x & 7u) | ((x << 5) & 0x700u) | ((x << 10) & 0x70000u) | ((x << 15) & 0x7000000u);
+                cr[q] = perm(tb0, ta0, sel);
+            }
+        }
         int8_t *bp = &Bs[buf][lr * kStride + CPT * lq];
 #pragma unroll
         for (int q = 0; q < CPT / 16; ++q) lds_store16(bp + 16 * q, cr + 4 * q);
@@ -399,60 +435,73 @@ __global__ void __launch_bounds__(64 * WM * WN) gemm_a8_w4_mfma(
         }
 }
 
-template <int WM, int WN, int UPG, int YDT, bool DUMP, bool TB>
+template <int B, int WM, int WN, int UPG, int YDT, bool DUMP, bool TB>
 static hipError_t a8_mfma_launch(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
                                  int32_t *partials, const int8_t *ctab, hipStream_t stream) {
     const int tiles_m = int((m + 64 * WM - 1) / (64 * WM));
     const int tiles_n = int((w.n + 64 * WN - 1) / (64 * WN));
     const int64_t nwg = int64_t(tiles_m) * tiles_n;
     if (nwg > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((gemm_a8_w4_mfma<WM, WN, UPG, YDT, DUMP, TB>), dim3(unsigned(nwg)), dim3(64 * WM * WN), 0, stream,
+    hipLaunchKernelGGL((gemm_a8_mfma<B, WM, WN, UPG, YDT, DUMP, TB>), dim3(unsigned(nwg)), dim3(64 * WM * WN), 0, stream,
                        w.codes, w.scale, w.a, w.b, int(w.n), int(w.k), x8, dx, int(m), y, partials, tiles_m, tiles_n,
                        ctab);
     return hipGetLastError();
 }
 
-template <int YDT, bool TB>
+template <int B, int YDT, bool TB>
 static hipError_t a8_mfma_group(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
                                 int32_t *partials, const int8_t *ctab, hipStream_t stream) {
     // The partials dump (a test path) runs four waves per workgroup, which
     // leaves room for its extra registers; the fast path runs eight.
     if (partials) {
+        if constexpr (B != 4) {
+            return hipErrorNotSupported;  // W3 partials: the 64x64 kernel
+        } else {
         switch (w.group) {
-            case 64: return a8_mfma_launch<2, 2, 2, YDT, true, TB>(w, x8, dx, m, y, partials, ctab, stream);
-            case 128: return a8_mfma_launch<2, 2, 4, YDT, true, TB>(w, x8, dx, m, y, partials, ctab, stream);
-            case 256: return a8_mfma_launch<2, 2, 8, YDT, true, TB>(w, x8, dx, m, y, partials, ctab, stream);
-            case 512: return a8_mfma_launch<2, 2, 16, YDT, true, TB>(w, x8, dx, m, y, partials, ctab, stream);
+            case 64: return a8_mfma_launch<B, 2, 2, 2, YDT, true, TB>(w, x8, dx, m, y, partials, ctab, stream);
+            case 128: return a8_mfma_launch<B, 2, 2, 4, YDT, true, TB>(w, x8, dx, m, y, partials, ctab, stream);
+            case 256: return a8_mfma_launch<B, 2, 2, 8, YDT, true, TB>(w, x8, dx, m, y, partials, ctab, stream);
+            case 512: return a8_mfma_launch<B, 2, 2, 16, YDT, true, TB>(w, x8, dx, m, y, partials, ctab, stream);
         }
         return hipErrorNotSupported;
+        }
     }
     switch (w.group) {
-        case 64: return a8_mfma_launch<4, 2, 2, YDT, false, TB>(w, x8, dx, m, y, partials, ctab, stream);
-        case 128: return a8_mfma_launch<4, 2, 4, YDT, false, TB>(w, x8, dx, m, y, partials, ctab, stream);
-        case 256: return a8_mfma_launch<4, 2, 8, YDT, false, TB>(w, x8, dx, m, y, partials, ctab, stream);
-        case 512: return a8_mfma_launch<4, 2, 16, YDT, false, TB>(w, x8, dx, m, y, partials, ctab, stream);
+        case 64: return a8_mfma_launch<B, 4, 2, 2, YDT, false, TB>(w, x8, dx, m, y, partials, ctab, stream);
+        case 128: return a8_mfma_launch<B, 4, 2, 4, YDT, false, TB>(w, x8, dx, m, y, partials, ctab, stream);
+        case 256: return a8_mfma_launch<B, 4, 2, 8, YDT, false, TB>(w, x8, dx, m, y, partials, ctab, stream);
+        case 512: return a8_mfma_launch<B, 4, 2, 16, YDT, false, TB>(w, x8, dx, m, y, partials, ctab, stream);
     }
     return hipErrorNotSupported;
 }
 
 bool gemm_a8_mfma_supported(const cq_weight &w, int64_t m) {
     const int64_t lim = int64_t(1) << 31;
-    return w.bits == 4 && w.group >= 64 && m * w.k < lim && stream_fits(w.n, w.k, w.bits, w.group) &&
-           w.n < lim && m < lim;
+    return (w.bits == 4 || w.bits == 3) && w.group >= 64 && m * w.k < lim &&
+           stream_fits(w.n, w.k, w.bits, w.group) && w.n < lim && m < lim;
+}
+
+template <bool TB>
+static hipError_t a8_mfma_dispatch(const cq_weight &w, const int8_t *ctab, const int8_t *x8, const float *dx,
+                                   int64_t m, void *y, int y_dt, int32_t *partials, hipStream_t stream) {
+    if (w.bits == 3) {
+        if (y_dt == 0) return a8_mfma_group<3, 0, TB>(w, x8, dx, m, y, partials, ctab, stream);
+        if (y_dt == 1) return a8_mfma_group<3, 1, TB>(w, x8, dx, m, y, partials, ctab, stream);
+        return a8_mfma_group<3, 2, TB>(w, x8, dx, m, y, partials, ctab, stream);
+    }
+    if (y_dt == 0) return a8_mfma_group<4, 0, TB>(w, x8, dx, m, y, partials, ctab, stream);
+    if (y_dt == 1) return a8_mfma_group<4, 1, TB>(w, x8, dx, m, y, partials, ctab, stream);
+    return a8_mfma_group<4, 2, TB>(w, x8, dx, m, y, partials, ctab, stream);
 }
 
 hipError_t launch_gemm_a8_mfma(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
                                int32_t *partials, hipStream_t stream) {
-    if (y_dt == 0) return a8_mfma_group<0, false>(w, x8, dx, m, y, partials, nullptr, stream);
-    if (y_dt == 1) return a8_mfma_group<1, false>(w, x8, dx, m, y, partials, nullptr, stream);
-    return a8_mfma_group<2, false>(w, x8, dx, m, y, partials, nullptr, stream);
+    return a8_mfma_dispatch<false>(w, nullptr, x8, dx, m, y, y_dt, partials, stream);
 }
 
 hipError_t launch_gemm_a8_mfma_tab(const cq_weight &w, const int8_t *ctab, const int8_t *x8, const float *dx,
                                    int64_t m, void *y, int y_dt, hipStream_t stream) {
-    if (y_dt == 0) return a8_mfma_group<0, true>(w, x8, dx, m, y, nullptr, ctab, stream);
-    if (y_dt == 1) return a8_mfma_group<1, true>(w, x8, dx, m, y, nullptr, ctab, stream);
-    return a8_mfma_group<2, true>(w, x8, dx, m, y, nullptr, ctab, stream);
+    return a8_mfma_dispatch<true>(w, ctab, x8, dx, m, y, y_dt, nullptr, stream);
 }
 
 }  // namespace cq
