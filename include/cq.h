@@ -166,7 +166,7 @@ cq_status cq_gemm_a8(const cq_weight *w, const int8_t *x8, const float *dx, int6
  *
  * Same result as cq_quantize_act_a8 followed by cq_gemm_a8 (Sec. 5.4): x8 and
  * dx receive the carriers and d_x, bit-exact; y follows eq. a8-output.  For a
- * single row (m == 1, B in {1, 2, 4}, K <= 16384) it is one launch: the GEMV
+ * single row (m == 1, B <= 4, K <= 16384) it is one launch: the GEMV
  * forms the row's carriers itself in a prologue, which removes the separate
  * encoding pass the paper names as the fixed cost of the single-row A8 path
  * (Sec. 6).  Other shapes run the two calls in order on the stream.  The FP32

@@ -54,7 +54,7 @@ hipError_t launch_quant_a8(const void *x, int x_dt, int64_t m, int64_t k, int8_t
 hipError_t launch_gemv_a8(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
                           int32_t *partials, hipStream_t stream);
 
-// Dynamic-A8 single-row streaming GEMV (m == 1, B in {1, 2, 4}, no partials dump).
+// Dynamic-A8 single-row streaming GEMV (m == 1, B <= 4, no partials dump).
 bool gemv_a8_stream_supported(const cq_weight &w, int64_t m);
 bool gemv_a8_fused_supported(const cq_weight &w, int64_t m);
 bool gemv_a16_routed_supported(const cq_weight &w, int64_t tokens);

@@ -151,8 +151,8 @@ hipError_t launch_gemv_a8(const cq_weight &w, const int8_t *x8, const float *dx,
 
 hipError_t launch_gemv_a8_tab(const cq_weight &w, const int8_t *ctab, const int8_t *x8, const float *dx, int64_t m,
                               void *y, int y_dt, hipStream_t stream) {
-    // W4 single- and narrow-row kernels form their carriers from registers
-    // (the same values); the generic kernel reads the table
+    // the single-row (B <= 4) and W4 narrow-row kernels form their carriers
+    // in registers (the same values); the generic kernel reads the table
     if (gemv_a8_stream_supported(w, m)) return launch_gemv_a8_stream(w, x8, dx, y, y_dt, stream);
     if (gemv_a8_narrow_supported(w, m)) return launch_gemv_a8_narrow(w, x8, dx, m, y, y_dt, stream);
     if (y_dt == 0) return dispatch_bits<0>(w, x8, dx, m, y, nullptr, ctab, stream);

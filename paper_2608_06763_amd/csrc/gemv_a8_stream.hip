@@ -1,5 +1,5 @@
 // Dynamic-A8 single-row GEMV, streaming byte-permute family (Sec. 5.4) for
-// m == 1 and B in {1, 2, 4}.
+// m == 1 and B in {1, 2, 3, 4}.
 //
 // Numerics are those of eq. a8-output: every weight contributes the INT8
 // carrier r(k) = sign(k) RNE(127 q(|k|/M)) (eq. carrier, Appendix A item 7)
@@ -17,7 +17,10 @@
 // in registers and looked up with byte permutes (a8_carriers.h), multiplied
 // with four activations at a time by v_dot4_i32_i8.  The carriers of a group
 // are computed once per (row, group): the group's lanes each evaluate two
-// magnitudes and share them through quad DPP moves.  W2 and W1 use constant
+// magnitudes and share them through quad DPP moves.  W3: every lane evaluates
+// the two interior carriers itself; a field indexes the 8-byte pair
+// [r0 r1 r2 r3 | 0 -r3 -r2 -r1] directly once four fields are spread into
+// bytes, and the carriers come out in field order.  W2 and W1 use constant
 // tables ({0, 127, 0, -127} and {-127, 127}).
 //
 // Fused quantization (FX >= 0): the kernel takes the BF16/FP16 activation row
@@ -58,7 +61,11 @@ __device__ __forceinline__ void transpose4(const uint32_t in[4], uint32_t out[4]
 // order in which the decode produces carriers.
 template <int B>
 __device__ __forceinline__ void arrange_x(const uint32_t xw[8], uint32_t xa[8]) {
-    if constexpr (B == 4) {
+    if constexpr (B == 3) {
+        // carriers come out in field order
+#pragma unroll
+        for (int i = 0; i < 8; ++i) xa[i] = xw[i];
+    } else if constexpr (B == 4) {
         // word i of codes holds fields 8i..8i+7; the even fields come out as
         // bytes (8i, 8i+2, 8i+4, 8i+6), the odd ones as (8i+1, ...)
 #pragma unroll
@@ -148,7 +155,7 @@ __global__ void __launch_bounds__(FX >= 0 ? 64 * kMaxFusedWaves : 256) gemv_a8_s
             const uint32_t gi = uint32_t(row) * ng + uint32_t(u / UPG);
             load_words<B>(rc, ok ? uint32_t(row) * row_bytes + uint32_t(u) * (4 * B) : kOobOffset, wn[r]);
             sn[r] = load_f32(rs, ok ? gi * 4u : kOobOffset);
-            if constexpr (B == 4) {
+            if constexpr (B == 4 || B == 3) {
                 an[r] = load_u16(ra, ok ? gi * 2u : kOobOffset);
                 bn[r] = load_u16(rb, ok ? gi * 2u : kOobOffset);
             }
@@ -283,6 +290,27 @@ __global__ void __launch_bounds__(FX >= 0 ? 64 * kMaxFusedWaves : 256) gemv_a8_s
                         p = __builtin_amdgcn_sdot4(int(w4_lookup(f2[h], ta0, ta1, tb0, tb1)), int(xa[2 * i + h]), p,
                                                    false);
                 }
+            } else if constexpr (B == 3) {
+                const float a = f16_to_f32(uint16_t(av[r]));
+                const float b = f16_to_f32(uint16_t(bv[r]));
+                const float c = 1.f - a - b;
+                const float margin = carrier_margin(a, b, c);
+                const uint32_t r12 = carrier_u8<M>(1, 1.f / 3.f, a, b, c, margin) |
+                                     (carrier_u8<M>(2, 2.f / 3.f, a, b, c, margin) << 8);
+                const uint32_t ta = (r12 << 8) | 0x7f000000u;             // r0 r1 r2 r3
+                const uint32_t neg = (0x80808080u - ta) ^ 0x80808080u;  // 0 -r1 -r2 -r3
+                const uint32_t tb = perm(neg, neg, 0x01020300u);        // 0 -r3 -r2 -r1
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const int bit = 12 * q, wi = bit >> 5, sh = bit & 31;
+                    uint32_t x;
+                    if (sh + 12 <= 32) x = w[r][wi] >> sh;
+                    else x = __builtin_amdgcn_alignbit(w[r][wi + 1], w[r][wi], sh);
+                    x &= 0xfffu;  // fields 4q .. 4q + 3
+                    const uint32_t sel =
+                        (x & 7u) | ((x << 5) & 0x700u) | ((x << 10) & 0x70000u) | ((x << 15) & 0x7000000u);
+                    p = __builtin_amdgcn_sdot4(int(perm(tb, ta, sel)), int(xa[q]), p, false);
+                }
             } else if constexpr (B == 2) {
                 // fields 0 -> 0, 1 -> +127, 2 (reserved) -> 0, 3 -> -127
                 constexpr uint32_t T = 0x81007f00u;
@@ -384,6 +412,7 @@ static hipError_t a8_stream_bits(const cq_weight &w, const void *xin, float *dxv
     switch (w.bits) {
         case 1: return a8_stream_group<1, YDT, FX>(w, xin, dxv, x8_out, y, stream);
         case 2: return a8_stream_group<2, YDT, FX>(w, xin, dxv, x8_out, y, stream);
+        case 3: return a8_stream_group<3, YDT, FX>(w, xin, dxv, x8_out, y, stream);
         case 4: return a8_stream_group<4, YDT, FX>(w, xin, dxv, x8_out, y, stream);
     }
     return hipErrorNotSupported;
@@ -398,7 +427,7 @@ static hipError_t a8_stream_ydt(const cq_weight &w, const void *xin, float *dxv,
 }
 
 bool gemv_a8_stream_supported(const cq_weight &w, int64_t m) {
-    return m == 1 && (w.bits == 1 || w.bits == 2 || w.bits == 4) && stream_fits(w.n, w.k, w.bits, w.group);
+    return m == 1 && w.bits <= 4 && stream_fits(w.n, w.k, w.bits, w.group);
 }
 
 bool gemv_a8_fused_supported(const cq_weight &w, int64_t m) {

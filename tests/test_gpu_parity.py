@@ -301,7 +301,7 @@ def test_edge_shapes(torch_dev, n, k, g, m):
 # ---------------------------------------------------------------- single-row A8 streaming family
 
 
-@pytest.mark.parametrize("bits", [1, 2, 4])
+@pytest.mark.parametrize("bits", [1, 2, 3, 4])
 @pytest.mark.parametrize("group", GROUPS)
 @pytest.mark.parametrize("k", [768, 4096 + 2048 + 512])
 def test_gemv_a8_stream(torch_dev, bits, group, k):
@@ -405,7 +405,7 @@ def test_narrow_rows_both_paths(torch_dev, group, m):
 # ---------------------------------------------------------------- fused single-row A8
 
 
-@pytest.mark.parametrize("bits", [1, 2, 4])
+@pytest.mark.parametrize("bits", [1, 2, 3, 4])
 @pytest.mark.parametrize("group", [32, 128, 512])
 @pytest.mark.parametrize("k", [512, 2048, 4096, 4096 + 2048 + 512, 14336, 16384])
 def test_gemm_a8_fused_single_row(torch_dev, bits, group, k):
@@ -433,7 +433,7 @@ def test_gemm_a8_fused_single_row(torch_dev, bits, group, k):
         assert R.eps_comp(_np(y), _np(y2).astype(np.float64), "fp32") <= 1e-6
 
 
-@pytest.mark.parametrize("case", ["rows3", "w3", "k18432", "zero_row", "gemv_rows_0"])
+@pytest.mark.parametrize("case", ["rows3", "w6", "k18432", "zero_row", "gemv_rows_0"])
 def test_gemm_a8_fused_fallbacks(torch_dev, case):
     # shapes the single launch does not take run the two calls; an all-zero
     # row gives d_x = eps / 127, zero carriers and a zero output
@@ -441,8 +441,8 @@ def test_gemm_a8_fused_fallbacks(torch_dev, case):
     bits, group, k, m, n = 4, 128, 2048, 1, 21
     if case == "rows3":
         m = 3
-    elif case == "w3":
-        bits = 3
+    elif case == "w6":
+        bits = 6
     elif case == "k18432":
         k = 18432
     r = fitted(61, n, k, bits, group)
