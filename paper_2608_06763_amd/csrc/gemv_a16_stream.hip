@@ -11,20 +11,23 @@
 // of a wave always owns unit l of its column block, so one wavefront load of a
 // row reads 64 * 4B contiguous bytes.  A workgroup owns RW rows; its waves take
 // different column blocks of those rows and are reduced through LDS at the
-// end.  A wave requests the codes and metadata of all RW rows of a column
-// block before it decodes any of them, and the activations of its column block
-// stay in registers (FP32) for all RW rows.
+// end.  A wave requests the codes, metadata and activations of its next item
+// (RW rows of one column block) before it decodes the current one, and the
+// activations of an item are converted to FP32 once for all RW rows.
 //
 // Decode.  The UPG = G/32 lanes that share a group share its level table:
 // every lane writes some of the 2^B signed normalised levels (0 for the
 // reserved pattern) into the table columns of all lanes of its group with
 // 128-bit LDS stores, then reads one entry per weight from its own column at
 // byte (field << 8) + lane * 4 + wave base, which is free of bank conflicts.
-// For W4 the address is assembled by one byte permute per weight.  B >= 6
+// For W4 the address is assembled by one byte permute per weight, and the
+// reads are issued 16 weights ahead of the products that consume them.  B >= 6
 // evaluates the cubic in registers instead of keeping a 64..256-entry table.
 #include "cq_device.h"
 #include "cq_internal.h"
 #include "stream_common.h"
+
+#define CQ_INLINE __attribute__((always_inline))
 
 namespace cq {
 
@@ -97,73 +100,53 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
 
     // An item is (row tile, column block).  A workgroup walks the tiles
     // blockIdx.x + j * gridDim.x; its wave w takes column blocks w, w + nwaves,
-    // ... of each tile.  The codes and metadata of the next item are requested
-    // before the current one is decoded.  Row offsets are wave-uniform (scalar
-    // offsets); rows past the matrix repeat its last row and are never stored;
-    // lanes past the row's units load an out-of-range offset and read zeros.
-    uint32_t wn[RW][B];
-    float sn[RW];
-    uint32_t an[RW], bn[RW];
-    auto fetch = [&](int t, int c) {
+    // ... of each tile.  Row offsets are wave-uniform (scalar offsets); rows
+    // past the matrix repeat its last row and are never stored; lanes past the
+    // row's units load an out-of-range offset and read zeros.
+    //
+    // Two register sets alternate: the codes, metadata and activations of the
+    // next item are requested into one set before the item in the other set
+    // is decoded, so every wait is for loads issued a whole item earlier
+    // (vector-memory loads complete in issue order for the wait counter).
+    struct Item {
+        uint32_t w[RW][B];
+        float s[RW];
+        uint32_t a[RW], b[RW];
+        uint32_t x[16];
+    };
+    // An item past the last tile (ok false) still issues its loads, at an
+    // out-of-range offset that reads zeros: every path through the loop then
+    // has the same loads in flight, and the waits stay exact.
+    auto fetch = [&](Item &it, int t, int c, bool ok) CQ_INLINE {
         const int u = c * 64 + lane;
-        const bool uok = u < units;
+        const bool uok = ok && u < units;
         const uint32_t vc = uok ? uint32_t(u) * (4 * B) : kOobOffset;
         const uint32_t vm = uok ? uint32_t(u / UPG) * 4u : kOobOffset;
         const uint32_t vh = uok ? uint32_t(u / UPG) * 2u : kOobOffset;
+        const uint32_t xo = uok ? uint32_t(u) * 64u : kOobOffset;
 #pragma unroll
         for (int r = 0; r < RW; ++r) {
-            const uint32_t row = uint32_t(min(t * RW + r, n - 1));
+            const uint32_t row = uint32_t(min(t * RW + r, n - 1));  // t may be past the last tile
             const uint32_t gi = row * uint32_t(ng);
-            load_words_s<B>(rc, vc, row * row_bytes, wn[r]);
-            sn[r] = load_f32_s(rs, vm, gi * 4u);
-            an[r] = load_u16_s(ra, vh, gi * 2u);
-            bn[r] = load_u16_s(rb, vh, gi * 2u);
+            load_words_s<B>(rc, vc, row * row_bytes, it.w[r]);
+            it.s[r] = load_f32_s(rs, vm, gi * 4u);
+            it.a[r] = load_u16_s(ra, vh, gi * 2u);
+            it.b[r] = load_u16_s(rb, vh, gi * 2u);
         }
+        load_words<16>(rx, xo, it.x);
     };
 
     float acc[RW];
 #pragma unroll
     for (int i = 0; i < RW; ++i) acc[i] = 0.f;
-    int tile = blockIdx.x, cb = wave;
-    bool have = tile < ntiles;
-    if (have) fetch(tile, cb);
-    while (have) {
-        uint32_t w[RW][B];
-        float s[RW];
-        uint32_t av[RW], bv[RW];
-#pragma unroll
-        for (int r = 0; r < RW; ++r) {
-#pragma unroll
-            for (int i = 0; i < B; ++i) w[r][i] = wn[r][i];
-            s[r] = sn[r];
-            av[r] = an[r];
-            bv[r] = bn[r];
-        }
-        int cb_next = cb + nwaves, tile_next = tile;
-        const bool last_cb = cb_next >= ncb;
-        if (last_cb) {
-            cb_next = wave;
-            tile_next = tile + int(gridDim.x);
-        }
-        const bool have_next = tile_next < ntiles;
-        if (have_next) fetch(tile_next, cb_next);
-        const int u = cb * 64 + lane;
+
+    auto process = [&](const Item &it, int tile, bool last_cb) CQ_INLINE {
         // ---- activations of this unit, FP32 in registers
         float xf[32];
-        {
-            const uint32_t xo = u < units ? uint32_t(u) * 64u : kOobOffset;
-            uint32_t xv[4][4];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) load_words<4>(rx, xo + 16u * q, xv[q]);
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const uint32_t *vw = xv[q];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    xf[q * 8 + 2 * e] = act_to_f32<XDT>(uint16_t(vw[e] & 0xffffu));
-                    xf[q * 8 + 2 * e + 1] = act_to_f32<XDT>(uint16_t(vw[e] >> 16));
-                }
-            }
+        for (int e = 0; e < 16; ++e) {
+            xf[2 * e] = act_to_f32<XDT>(uint16_t(it.x[e] & 0xffffu));
+            xf[2 * e + 1] = act_to_f32<XDT>(uint16_t(it.x[e] >> 16));
         }
         // ---- level tables of all rows of the tile first (one slot per row), so
         // that the LDS writes of one row overlap the reads of the previous one
@@ -173,8 +156,8 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
         for (int r = 0; r < RW; ++r) {
             float a = 1.f, b = 0.f;
             if constexpr (B >= 3) {
-                a = f16_to_f32(uint16_t(av[r]));
-                b = f16_to_f32(uint16_t(bv[r]));
+                a = f16_to_f32(uint16_t(it.a[r]));
+                b = f16_to_f32(uint16_t(it.b[r]));
             }
             const float cc = 1.f - a - b;
             al_r[r] = a * (1.0f / float(M));
@@ -217,35 +200,67 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
             }
         }
         if constexpr (LUT) wave_lds_fence();
-        // ---- decode row by row
+        // ---- decode
+        if constexpr (B == 4) {
+            // The 64 weights of the item (both rows) in chunks of 16: the table
+            // reads of chunk c + 1 are issued before the products of chunk c, so
+            // a wave keeps 16 to 32 LDS reads in flight.
+            constexpr int BT = 16;
+            constexpr int CH = RW * 32 / BT;
+            float lvb[2][BT];
+            float pp[RW][2];
 #pragma unroll
-        for (int r = 0; r < RW; ++r) {
-            const uint32_t colr = col + uint32_t(r) * (NT * 256u);
-            const uint32_t wtagr = wtag + uint32_t(r) * 0x10101010u;
-            const float al = al_r[r], be = be_r[r], ga = ga_r[r];
-            float p0 = 0.f, p1 = 0.f;
+            for (int r = 0; r < RW; ++r) pp[r][0] = pp[r][1] = 0.f;
+            auto reads = [&](int c, float *dst) CQ_INLINE {
 #pragma unroll
-            for (int i8 = 0; i8 < 4; ++i8) {
-                float lv[8];
-                if constexpr (B == 4) {
-                    const uint32_t wd = w[r][i8];
-                    const uint32_t ev = (wd & 0x0f0f0f0fu) | wtagr;
-                    const uint32_t od = ((wd >> 4) & 0x0f0f0f0fu) | wtagr;
+                for (int e = 0; e < BT; ++e) {
+                    // weight i of row r: byte i / 2 % 4 of code word i / 8, low
+                    // nibble for even i
+                    const int wi = c * BT + e;
+                    const int r = wi / 32, i = wi % 32;
+                    const uint32_t wd = it.w[r][i / 8];
+                    const uint32_t nib =
+                        ((i & 1) ? ((wd >> 4) & 0x0f0f0f0fu) : (wd & 0x0f0f0f0fu)) | (wtag + uint32_t(r) * 0x10101010u);
+                    const uint32_t sel = 0x03020000u | (uint32_t(4 + (i % 8) / 2) << 8);
+                    dst[e] = lds_ld(__builtin_amdgcn_perm(nib, col + uint32_t(r) * (NT * 256u), sel));
+                }
+            };
+            auto products = [&](int c, const float *src) CQ_INLINE {
 #pragma unroll
-                    for (int jj = 0; jj < 4; ++jj) {
-                        const uint32_t sel = 0x03020000u | (uint32_t(4 + jj) << 8);
-                        lv[2 * jj] = lds_ld(__builtin_amdgcn_perm(ev, colr, sel));
-                        lv[2 * jj + 1] = lds_ld(__builtin_amdgcn_perm(od, colr, sel));
-                    }
-                } else {
+                for (int e = 0; e < BT; ++e) {
+                    const int wi = c * BT + e;
+                    const int r = wi / 32, i = wi % 32;
+                    pp[r][i & 1] = __builtin_fmaf(xf[i], src[e], pp[r][i & 1]);
+                }
+            };
+            reads(0, lvb[0]);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                if (c + 1 < CH) reads(c + 1, lvb[(c + 1) & 1]);
+                __builtin_amdgcn_sched_barrier(0);
+                products(c, lvb[c & 1]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+#pragma unroll
+            for (int r = 0; r < RW; ++r) acc[r] = __builtin_fmaf(it.s[r], pp[r][0] + pp[r][1], acc[r]);
+        } else {
+#pragma unroll
+            for (int r = 0; r < RW; ++r) {
+                const uint32_t colr = col + uint32_t(r) * (NT * 256u);
+                const float al = al_r[r], be = be_r[r], ga = ga_r[r];
+                float p0 = 0.f, p1 = 0.f;
+#pragma unroll
+                for (int i8 = 0; i8 < 4; ++i8) {
+                    float lv[8];
 #pragma unroll
                     for (int e = 0; e < 8; ++e) {
                         const int i = i8 * 8 + e;
                         const int bit = i * B;
                         const int wd = bit >> 5, sh = bit & 31;
                         uint32_t v;
-                        if (sh + B <= 32) v = w[r][wd] >> sh;
-                        else v = __builtin_amdgcn_alignbit(w[r][wd + 1], w[r][wd], sh);
+                        if (sh + B <= 32) v = it.w[r][wd] >> sh;
+                        else v = __builtin_amdgcn_alignbit(it.w[r][wd + 1], it.w[r][wd], sh);
                         if constexpr (LUT) {
                             lv[e] = lds_ld(((v & uint32_t(NT - 1)) << 8) + colr);
                         } else {
@@ -256,14 +271,14 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                             lv[e] = (kk == -(1 << (B - 1))) ? 0.f : lvv;
                         }
                     }
-                }
 #pragma unroll
-                for (int e = 0; e < 8; e += 2) {
-                    p0 = __builtin_fmaf(xf[i8 * 8 + e], lv[e], p0);
-                    p1 = __builtin_fmaf(xf[i8 * 8 + e + 1], lv[e + 1], p1);
+                    for (int e = 0; e < 8; e += 2) {
+                        p0 = __builtin_fmaf(xf[i8 * 8 + e], lv[e], p0);
+                        p1 = __builtin_fmaf(xf[i8 * 8 + e + 1], lv[e + 1], p1);
+                    }
                 }
+                acc[r] = __builtin_fmaf(it.s[r], p0 + p1, acc[r]);
             }
-            acc[r] = __builtin_fmaf(s[r], p0 + p1, acc[r]);
         }
         if (last_cb) {
             const int row0 = tile * RW;
@@ -293,9 +308,39 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                 __syncthreads();  // red is reused by the next tile
             }
         }
-        tile = tile_next;
-        cb = cb_next;
-        have = have_next;
+    };
+
+    // the item after (tile, cb): the wave's next column block of the tile,
+    // else its first column block of the workgroup's next tile
+    auto advance = [&](int &tile, int &cb) CQ_INLINE {
+        cb += nwaves;
+        if (cb >= ncb) {
+            cb = wave;
+            tile += int(gridDim.x);
+        }
+    };
+
+    Item ia, ib;
+    int tile = blockIdx.x, cb = wave;
+    if (tile >= ntiles) return;
+    fetch(ia, tile, cb, true);
+    while (true) {
+        int t1 = tile, c1 = cb;
+        advance(t1, c1);
+        const bool last0 = t1 != tile;
+        const bool have1 = t1 < ntiles;
+        fetch(ib, t1, c1, have1);
+        process(ia, tile, last0);
+        if (!have1) break;
+        int t2 = t1, c2 = c1;
+        advance(t2, c2);
+        const bool last1 = t2 != t1;
+        const bool have2 = t2 < ntiles;
+        fetch(ia, t2, c2, have2);
+        process(ib, t1, last1);
+        if (!have2) break;
+        tile = t2;
+        cb = c2;
     }
 }
 
@@ -304,9 +349,10 @@ static hipError_t stream_waves(const cq_weight &w, const void *x, void *y, hipSt
     const int64_t ncb = ((w.k >> 5) + 63) >> 6;
     constexpr int NT = B <= 5 ? (1 << B) : 1;
     constexpr int kMaxW = NT >= 32 ? 2 : 4;  // keep the tables within 32 KB and the W4 slot tag in 4 bits
-    // Two waves split the column blocks of a tile; more waves per workgroup
-    // only add tile-reduction cost (measured on Llama-3-8B layer shapes).
-    int nw = ncb >= 2 ? 2 : 1;
+    // Rows of up to two column blocks: one wave per tile walks them in turn
+    // (no cross-wave reduction); longer rows split their column blocks over two
+    // waves (measured on the Llama-3-8B layer shapes).
+    int nw = ncb > 2 ? 2 : 1;
     if (nw > kMaxW) nw = kMaxW;
     const size_t lds = sizeof(float) * (size_t(nw) * RW * NT * 64 + size_t(nw) * RW);
     const int64_t tiles = (w.n + RW - 1) / RW;
