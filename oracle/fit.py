@@ -16,8 +16,7 @@ admissible shape (a, b):
   * NRMSE_C = sqrt(sum (w - w_hat)^2 / sum w^2) (eq. nrmse).
 
 The paper leaves the candidate grid, the clipping candidates and the iteration
-counts open.  This oracle fixes them (the same constants are the defaults of
-the product-side fitter, which is tested against this one):
+counts open.  This oracle fixes them:
   * coarse grid a in {0.10, 0.20, ..., 1.50} x b in {-1.20, -1.10, ..., 0.40},
     each value rounded to FP16 first, kept when m(a, b) >= 1e-3;
   * two 3x3 local refinements around the incumbent, steps 0.05 then 0.02,
