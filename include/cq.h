@@ -248,6 +248,98 @@ cq_status cq_gemm_routed_model_dtype(const cq_weight *bank, int32_t n_experts, c
 cq_status cq_set_gemv_max_rows(int32_t path, int64_t max_rows);
 int64_t cq_get_gemv_max_rows(int32_t path);
 
+/*
+ * Measured shape- and device-dependent kernel selection (Sec. 5.6).
+ *
+ * The paper treats the choice of kernel family as an optimisation over the
+ * operator signature (B, G, M, N, K, activation dtype) on the measured device:
+ * candidates are filtered by width, dtype and structural constraints, the
+ * valid ones are timed on representative row counts, and the winner is a
+ * deterministic function of signature and device.  Selection changes neither
+ * codes nor metadata.  These calls expose the families (for a tuner to time
+ * them) and a process-wide table that the dispatcher of cq_gemm_model_dtype
+ * and cq_gemm_a8 consults before its built-in rules.
+ *
+ * Paths: CQ_PATH_MODEL_DTYPE (cq_gemm_model_dtype), CQ_PATH_A8 (cq_gemm_a8).
+ * Families (CQ_FAMILY_AUTO = the built-in rules):
+ *   GEMV_STREAM   single-row streaming GEMV (m == 1; A8: B <= 4)
+ *   GEMV_LUT      model dtype only, per-wave level tables (m <= 4, G <= 128;
+ *                 m == 1 at G == 256)
+ *   GEMV_NARROW   matrix-core narrow-row GEMV (2 <= m <= 16; model dtype
+ *                 B <= 5, A8 W4 with G >= 64)
+ *   GEMV_GENERIC  conservative one-wave-per-row GEMV (m <= 16, every B, G)
+ *   GEMM_MFMA     tiled matrix-core GEMM (model dtype B <= 5; A8 W3/W4 with
+ *                 G >= 64)
+ *   GEMM_TILED    conservative 64 x 64 tiled GEMM (every B, G)
+ * Families that read 32-bit buffer offsets also need tensors below 2 GiB.
+ */
+typedef enum { CQ_PATH_MODEL_DTYPE = 0, CQ_PATH_A8 = 1 } cq_path;
+typedef enum {
+    CQ_FAMILY_AUTO = 0,
+    CQ_FAMILY_GEMV_STREAM = 1,
+    CQ_FAMILY_GEMV_LUT = 2,
+    CQ_FAMILY_GEMV_NARROW = 3,
+    CQ_FAMILY_GEMV_GENERIC = 4,
+    CQ_FAMILY_GEMM_MFMA = 5,
+    CQ_FAMILY_GEMM_TILED = 6
+} cq_family;
+
+/*
+ * 1 if `family` can run `path` for this weight and row count, else 0 (also 0
+ * for invalid arguments).  Host only: reads the descriptor's fields, never
+ * its device memory.
+ */
+int32_t cq_family_supported(int32_t path, int32_t family, const cq_weight *w, int64_t m);
+
+/*
+ * cq_gemm_model_dtype / cq_gemm_a8 forced onto one family (for timing and
+ * for checking that every family computes the same product).  Arguments and
+ * results as in those calls (no partials dump); CQ_ERR_UNSUPPORTED, before
+ * anything is launched, when cq_family_supported would return 0.
+ * CQ_FAMILY_AUTO runs the ordinary dispatch.
+ */
+cq_status cq_gemm_model_dtype_family(const cq_weight *w, const void *x, cq_dtype x_dtype, int64_t m,
+                                     void *y, cq_dtype y_dtype, int32_t family, void *stream);
+cq_status cq_gemm_a8_family(const cq_weight *w, const int8_t *x8, const float *dx, int64_t m, void *y,
+                            cq_dtype y_dtype, int32_t family, void *stream);
+
+/*
+ * One row of the selection table: calls on `path` with exactly this (bits,
+ * group, n, k), activation dtype x_dtype (CQ_BF16 or CQ_FP16; -1 matches
+ * both; A8 entries take -1) and m_lo <= m <= m_hi run `family`.
+ */
+typedef struct {
+    int32_t path, family;
+    int32_t bits, group;
+    int64_t n, k;
+    int64_t m_lo, m_hi;
+    int32_t x_dtype;
+    int32_t reserved; /* must be 0 */
+} cq_select_entry;
+
+/*
+ * Replace the process-wide table with a copy of entries[0 .. count) (count 0
+ * clears it).  Host only.  CQ_ERR_ARG, with the previous table kept, if an
+ * entry is malformed (unknown path or family, CQ_FAMILY_AUTO, the LUT family
+ * on the A8 path, bits outside 1..8, a group that is not a multiple of 32 in
+ * 32..512, n or k < 1, m_lo < 1 or m_hi < m_lo, a bad x_dtype, reserved != 0)
+ * or if two entries of the same path, shape and dtype overlap in m; count
+ * above 65536 is CQ_ERR_ARG too.  The first matching entry wins; when its
+ * family cannot take the call (cq_family_supported is 0) the built-in rules
+ * decide.  The table does not apply to a cq_gemm_a8 call that asks for the
+ * partials dump, nor to cq_gemm_a8_fused, cq_gemm_a8_carriers or the routed
+ * product.  Safe to call while other threads launch products; a call already
+ * past its dispatch is not affected.
+ */
+cq_status cq_select_set(const cq_select_entry *entries, int64_t count);
+
+/*
+ * The family the dispatcher would run for this call (table first, then the
+ * built-in rules, including the cq_set_gemv_max_rows threshold), written to
+ * *family.  Host only.
+ */
+cq_status cq_select_query(int32_t path, const cq_weight *w, cq_dtype x_dtype, int64_t m, int32_t *family);
+
 #ifdef __cplusplus
 }
 #endif

@@ -8,7 +8,11 @@ GPU; calling a device entry point does, and a missing library raises.
 Entry points (same names as the C ABI):
   cq_pack_groups, cq_decode_ref, cq_gemm_model_dtype, cq_quantize_act_a8,
   cq_gemm_a8, cq_gemm_a8_fused, cq_build_carriers, cq_gemm_a8_carriers,
-  cq_gemm_routed_model_dtype, cq_set_gemv_max_rows, cq_get_gemv_max_rows
+  cq_gemm_routed_model_dtype, cq_set_gemv_max_rows, cq_get_gemv_max_rows,
+  cq_family_supported, cq_gemm_model_dtype_family, cq_gemm_a8_family,
+  cq_select_set, cq_select_query
+The measured kernel-selection tuner that fills the selection table is in
+``selection.py``.
 """
 from __future__ import annotations
 
@@ -26,7 +30,14 @@ STATUS = {0: "CQ_OK", 1: "CQ_ERR_ARG", 2: "CQ_ERR_SHAPE", 3: "CQ_ERR_ALIGN", 4: 
 
 EXPORTS = ("cq_status_str", "cq_pack_groups", "cq_decode_ref", "cq_gemm_model_dtype", "cq_quantize_act_a8",
            "cq_gemm_a8", "cq_gemm_a8_fused", "cq_build_carriers", "cq_gemm_a8_carriers",
-           "cq_gemm_routed_model_dtype", "cq_set_gemv_max_rows", "cq_get_gemv_max_rows")
+           "cq_gemm_routed_model_dtype", "cq_set_gemv_max_rows", "cq_get_gemv_max_rows",
+           "cq_family_supported", "cq_gemm_model_dtype_family", "cq_gemm_a8_family", "cq_select_set",
+           "cq_select_query")
+
+CQ_PATH_MODEL_DTYPE, CQ_PATH_A8 = 0, 1
+FAMILIES = {"auto": 0, "gemv_stream": 1, "gemv_lut": 2, "gemv_narrow": 3, "gemv_generic": 4, "gemm_mfma": 5,
+            "gemm_tiled": 6}
+FAMILY_NAMES = {v: k for k, v in FAMILIES.items()}
 
 
 class CQError(RuntimeError):
@@ -39,6 +50,12 @@ class cq_weight(ctypes.Structure):
     _fields_ = [("bits", ctypes.c_int32), ("group", ctypes.c_int32), ("n", ctypes.c_int64),
                 ("k", ctypes.c_int64), ("codes", ctypes.c_void_p), ("scale", ctypes.c_void_p),
                 ("a", ctypes.c_void_p), ("b", ctypes.c_void_p)]
+
+
+class cq_select_entry(ctypes.Structure):
+    _fields_ = [("path", ctypes.c_int32), ("family", ctypes.c_int32), ("bits", ctypes.c_int32),
+                ("group", ctypes.c_int32), ("n", ctypes.c_int64), ("k", ctypes.c_int64), ("m_lo", ctypes.c_int64),
+                ("m_hi", ctypes.c_int64), ("x_dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 _lib = None
@@ -78,6 +95,17 @@ def lib() -> ctypes.CDLL:
     L.cq_set_gemv_max_rows.argtypes = [i32, i64]
     L.cq_get_gemv_max_rows.restype = i64
     L.cq_get_gemv_max_rows.argtypes = [i32]
+    L.cq_family_supported.restype = i32
+    L.cq_family_supported.argtypes = [i32, i32, ctypes.POINTER(cq_weight), i64]
+    L.cq_gemm_model_dtype_family.restype = ctypes.c_int
+    L.cq_gemm_model_dtype_family.argtypes = [ctypes.POINTER(cq_weight), vp, ctypes.c_int, i64, vp, ctypes.c_int, i32,
+                                             vp]
+    L.cq_gemm_a8_family.restype = ctypes.c_int
+    L.cq_gemm_a8_family.argtypes = [ctypes.POINTER(cq_weight), vp, vp, i64, vp, ctypes.c_int, i32, vp]
+    L.cq_select_set.restype = ctypes.c_int
+    L.cq_select_set.argtypes = [ctypes.POINTER(cq_select_entry), i64]
+    L.cq_select_query.restype = ctypes.c_int
+    L.cq_select_query.argtypes = [i32, ctypes.POINTER(cq_weight), ctypes.c_int, i64, ctypes.POINTER(i32)]
     _lib = L
     return L
 
@@ -297,3 +325,63 @@ def cq_set_gemv_max_rows(path: int, max_rows: int):
 
 def cq_get_gemv_max_rows(path: int) -> int:
     return int(lib().cq_get_gemv_max_rows(path))
+
+
+# ---------------------------------------------------------------- kernel families and the selection table
+
+
+def _family(f) -> int:
+    return FAMILIES[f] if isinstance(f, str) else int(f)
+
+
+def _desc(w):
+    return w.desc if isinstance(w, CQWeight) else w
+
+
+def cq_family_supported(path: int, family, w, m: int) -> bool:
+    """Whether a family can take this call; w is a CQWeight or a cq_weight descriptor."""
+    return bool(lib().cq_family_supported(path, _family(family), ctypes.byref(_desc(w)), m))
+
+
+def cq_gemm_model_dtype_family(w: CQWeight, x, family, y_dtype=None, out=None, stream=None):
+    """cq_gemm_model_dtype on one kernel family."""
+    torch = _torch()
+    assert x.dim() == 2 and x.shape[1] == w.k and x.is_contiguous()
+    y_dtype = y_dtype or x.dtype
+    if out is None:
+        out = torch.empty((x.shape[0], w.n), dtype=y_dtype, device=x.device)
+    st = lib().cq_gemm_model_dtype_family(ctypes.byref(w.desc), x.data_ptr(), _dt(x.dtype), x.shape[0],
+                                          out.data_ptr(), _dt(out.dtype), _family(family), _stream_ptr(stream))
+    _check(st, "cq_gemm_model_dtype_family")
+    return out
+
+
+def cq_gemm_a8_family(w: CQWeight, x8, dx, family, y_dtype=None, out=None, stream=None):
+    """cq_gemm_a8 on one kernel family (no partials dump)."""
+    torch = _torch()
+    assert x8.dim() == 2 and x8.shape[1] == w.k and x8.is_contiguous()
+    m = x8.shape[0]
+    y_dtype = y_dtype or torch.bfloat16
+    if out is None:
+        out = torch.empty((m, w.n), dtype=y_dtype, device=x8.device)
+    st = lib().cq_gemm_a8_family(ctypes.byref(w.desc), x8.data_ptr(), dx.data_ptr(), m, out.data_ptr(),
+                                 _dt(out.dtype), _family(family), _stream_ptr(stream))
+    _check(st, "cq_gemm_a8_family")
+    return out
+
+
+def cq_select_set(entries):
+    """Install the selection table: a list of dicts with keys path, family, bits,
+    group, n, k, m_lo, m_hi and optionally x_dtype (-1 = any)."""
+    arr = (cq_select_entry * max(1, len(entries)))()
+    for i, e in enumerate(entries):
+        arr[i] = cq_select_entry(int(e["path"]), _family(e["family"]), int(e["bits"]), int(e["group"]), int(e["n"]),
+                                 int(e["k"]), int(e["m_lo"]), int(e["m_hi"]), int(e.get("x_dtype", -1)), 0)
+    _check(lib().cq_select_set(arr, len(entries)), "cq_select_set")
+
+
+def cq_select_query(path: int, w, m: int, x_dtype: int = CQ_BF16) -> str:
+    """Name of the family the dispatcher would run for this call."""
+    out = ctypes.c_int32(-1)
+    _check(lib().cq_select_query(path, ctypes.byref(_desc(w)), x_dtype, m, ctypes.byref(out)), "cq_select_query")
+    return FAMILY_NAMES[out.value]

@@ -56,6 +56,16 @@ cq_status check_weight(const cq_weight *w) {
 
 cq_status hip_status(hipError_t e) { return e == hipSuccess ? CQ_OK : CQ_ERR_HIP; }
 
+// Table entry if it names a family that can take the call, else the built-in
+// rules (a partials dump always takes the built-in rules).
+int choose_family(int path, const cq_weight &w, int x_dt, int64_t m, bool partials) {
+    if (!partials) {
+        const int f = cq::table_family(path, w, x_dt, m);
+        if (f != CQ_FAMILY_AUTO && cq::family_supported(path, f, w, m)) return f;
+    }
+    return cq::default_family(path, w, m, gemv_max_rows(path), partials);
+}
+
 }  // namespace
 
 extern "C" {
@@ -143,11 +153,10 @@ cq_status cq_gemm_model_dtype(const cq_weight *w, const void *x, cq_dtype x_dtyp
     if (y_dtype != x_dtype && y_dtype != CQ_FP32) return CQ_ERR_DTYPE;
     if (!aligned16(x) || !aligned16(y)) return CQ_ERR_ALIGN;
     if (m > (int64_t(1) << 40) / w->k || m > (int64_t(1) << 40) / w->n) return CQ_ERR_SHAPE;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    const int xd = int(x_dtype), yd = int(y_dtype);
-    if (m <= gemv_max_rows(0) && m <= cq::kGemvMaxRows) return hip_status(cq::launch_gemv_a16(*w, x, xd, m, y, yd, s));
     if (m > int64_t(65535) * 64) return CQ_ERR_SHAPE;
-    return hip_status(cq::launch_gemm_a16(*w, x, xd, m, y, yd, s));
+    const int family = choose_family(CQ_PATH_MODEL_DTYPE, *w, int(x_dtype), m, false);
+    return hip_status(
+        cq::run_family_a16(family, *w, x, int(x_dtype), m, y, int(y_dtype), static_cast<hipStream_t>(stream)));
 }
 
 cq_status cq_quantize_act_a8(const void *x, cq_dtype x_dtype, int64_t m, int64_t k, int8_t *x8, float *dx,
@@ -169,11 +178,10 @@ cq_status cq_gemm_a8(const cq_weight *w, const int8_t *x8, const float *dx, int6
     if (!aligned16(x8) || !aligned16(dx) || !aligned16(y) || (partials_dbg && !aligned16(partials_dbg)))
         return CQ_ERR_ALIGN;
     if (m > (int64_t(1) << 40) / w->k || m > (int64_t(1) << 40) / w->n) return CQ_ERR_SHAPE;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    if (m <= gemv_max_rows(1) && m <= cq::kGemvMaxRows)
-        return hip_status(cq::launch_gemv_a8(*w, x8, dx, m, y, int(y_dtype), partials_dbg, s));
     if (m > int64_t(65535) * 64) return CQ_ERR_SHAPE;
-    return hip_status(cq::launch_gemm_a8(*w, x8, dx, m, y, int(y_dtype), partials_dbg, s));
+    const int family = choose_family(CQ_PATH_A8, *w, -1, m, partials_dbg != nullptr);
+    return hip_status(cq::run_family_a8(family, *w, x8, dx, m, y, int(y_dtype), partials_dbg,
+                                        static_cast<hipStream_t>(stream)));
 }
 
 cq_status cq_gemm_a8_fused(const cq_weight *w, const void *x, cq_dtype x_dtype, int64_t m, int8_t *x8, float *dx,
@@ -249,6 +257,63 @@ cq_status cq_set_gemv_max_rows(int32_t path, int64_t max_rows) {
 int64_t cq_get_gemv_max_rows(int32_t path) {
     if (path != 0 && path != 1) return -1;
     return gemv_max_rows(path);
+}
+
+int32_t cq_family_supported(int32_t path, int32_t family, const cq_weight *w, int64_t m) {
+    if (check_weight(w) != CQ_OK) return 0;
+    return cq::family_supported(path, family, *w, m) ? 1 : 0;
+}
+
+cq_status cq_gemm_model_dtype_family(const cq_weight *w, const void *x, cq_dtype x_dtype, int64_t m, void *y,
+                                     cq_dtype y_dtype, int32_t family, void *stream) {
+    if (family == CQ_FAMILY_AUTO) return cq_gemm_model_dtype(w, x, x_dtype, m, y, y_dtype, stream);
+    const cq_status st = check_weight(w);
+    if (st != CQ_OK) return st;
+    if (!x || !y || m < 1) return CQ_ERR_ARG;
+    if (x_dtype != CQ_BF16 && x_dtype != CQ_FP16) return CQ_ERR_DTYPE;
+    if (y_dtype != x_dtype && y_dtype != CQ_FP32) return CQ_ERR_DTYPE;
+    if (!aligned16(x) || !aligned16(y)) return CQ_ERR_ALIGN;
+    if (m > (int64_t(1) << 40) / w->k || m > (int64_t(1) << 40) / w->n) return CQ_ERR_SHAPE;
+    if (!cq::family_supported(CQ_PATH_MODEL_DTYPE, family, *w, m)) return CQ_ERR_UNSUPPORTED;
+    const hipError_t e =
+        cq::run_family_a16(family, *w, x, int(x_dtype), m, y, int(y_dtype), static_cast<hipStream_t>(stream));
+    return e == hipErrorNotSupported ? CQ_ERR_UNSUPPORTED : hip_status(e);
+}
+
+cq_status cq_gemm_a8_family(const cq_weight *w, const int8_t *x8, const float *dx, int64_t m, void *y,
+                            cq_dtype y_dtype, int32_t family, void *stream) {
+    if (family == CQ_FAMILY_AUTO) return cq_gemm_a8(w, x8, dx, m, y, y_dtype, nullptr, stream);
+    const cq_status st = check_weight(w);
+    if (st != CQ_OK) return st;
+    if (!x8 || !dx || !y || m < 1) return CQ_ERR_ARG;
+    if (y_dtype != CQ_BF16 && y_dtype != CQ_FP16 && y_dtype != CQ_FP32) return CQ_ERR_DTYPE;
+    if (!aligned16(x8) || !aligned16(dx) || !aligned16(y)) return CQ_ERR_ALIGN;
+    if (m > (int64_t(1) << 40) / w->k || m > (int64_t(1) << 40) / w->n) return CQ_ERR_SHAPE;
+    if (!cq::family_supported(CQ_PATH_A8, family, *w, m)) return CQ_ERR_UNSUPPORTED;
+    const hipError_t e = cq::run_family_a8(family, *w, x8, dx, m, y, int(y_dtype), nullptr,
+                                           static_cast<hipStream_t>(stream));
+    return e == hipErrorNotSupported ? CQ_ERR_UNSUPPORTED : hip_status(e);
+}
+
+cq_status cq_select_set(const cq_select_entry *entries, int64_t count) {
+    if (count < 0 || count > 65536 || (count > 0 && !entries)) return CQ_ERR_ARG;
+    std::vector<cq_select_entry> t(entries, entries + count);
+    for (int64_t i = 0; i < count; ++i) {
+        if (!cq::select_entry_valid(t[i])) return CQ_ERR_ARG;
+        for (int64_t j = 0; j < i; ++j)
+            if (cq::select_entries_overlap(t[i], t[j])) return CQ_ERR_ARG;
+    }
+    cq::select_install(std::move(t));
+    return CQ_OK;
+}
+
+cq_status cq_select_query(int32_t path, const cq_weight *w, cq_dtype x_dtype, int64_t m, int32_t *family) {
+    const cq_status st = check_weight(w);
+    if (st != CQ_OK) return st;
+    if (!family || m < 1 || (path != CQ_PATH_MODEL_DTYPE && path != CQ_PATH_A8)) return CQ_ERR_ARG;
+    if (path == CQ_PATH_MODEL_DTYPE && x_dtype != CQ_BF16 && x_dtype != CQ_FP16) return CQ_ERR_DTYPE;
+    *family = choose_family(path, *w, path == CQ_PATH_A8 ? -1 : int(x_dtype), m, false);
+    return CQ_OK;
 }
 
 }  // extern "C"

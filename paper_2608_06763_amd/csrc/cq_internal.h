@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "../../include/cq.h"
 
 namespace cq {
@@ -12,15 +14,12 @@ namespace cq {
 
 hipError_t launch_decode_ref(const cq_weight &w, int8_t *codes_out, float *w_out, hipStream_t stream);
 
-// Model-dtype narrow-row GEMV family (m <= 16).
-hipError_t launch_gemv_a16(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
-                           hipStream_t stream);
-
 // Conservative model-dtype GEMV (every B and G, m <= 16).
 hipError_t launch_gemv_a16_generic(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                                    hipStream_t stream);
 
 // Model-dtype single-row streaming GEMV (m == 1, every B, G <= 512).
+bool gemv_a16_stream_supported(const cq_weight &w, int64_t m);
 hipError_t launch_gemv_a16_stream(const cq_weight &w, const void *x, int x_dt, void *y, int y_dt,
                                   hipStream_t stream);
 
@@ -37,10 +36,6 @@ bool gemv_a8_narrow_supported(const cq_weight &w, int64_t m);
 hipError_t launch_gemv_a8_narrow(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
                                  hipStream_t stream);
 
-// Model-dtype tiled matrix-core GEMM family.
-hipError_t launch_gemm_a16(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
-                           hipStream_t stream);
-
 // Model-dtype many-row GEMM for B <= 5 (tensors below 2 GiB).
 bool gemm_a16_mfma_supported(const cq_weight &w, int64_t m);
 hipError_t launch_gemm_a16_mfma(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
@@ -49,10 +44,6 @@ hipError_t launch_gemm_a16_mfma(const cq_weight &w, const void *x, int x_dt, int
 // Dynamic-A8 activation quantizer.
 hipError_t launch_quant_a8(const void *x, int x_dt, int64_t m, int64_t k, int8_t *x8, float *dx,
                            hipStream_t stream);
-
-// Dynamic-A8 narrow-row GEMV family (m <= 16).
-hipError_t launch_gemv_a8(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
-                          int32_t *partials, hipStream_t stream);
 
 // Dynamic-A8 single-row streaming GEMV (m == 1, B <= 4, no partials dump).
 bool gemv_a8_stream_supported(const cq_weight &w, int64_t m);
@@ -78,16 +69,35 @@ hipError_t launch_gemv_a8_fused(const cq_weight &w, const void *x, int x_dt, int
 hipError_t launch_gemv_a8_stream(const cq_weight &w, const int8_t *x8, const float *dx, void *y, int y_dt,
                                  hipStream_t stream);
 
-// Dynamic-A8 tiled int8 matrix-core GEMM family.
-hipError_t launch_gemm_a8(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
-                          int32_t *partials, hipStream_t stream);
-
-// Dynamic-A8 many-row GEMM for W4, G >= 64 (tensors below 2 GiB).
+// Dynamic-A8 many-row GEMM for W3 and W4, G >= 64 (tensors below 2 GiB).
 bool gemm_a8_mfma_supported(const cq_weight &w, int64_t m);
 hipError_t launch_gemm_a8_mfma(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
                                int32_t *partials, hipStream_t stream);
 
 // Largest row count each GEMV family accepts.
 constexpr int64_t kGemvMaxRows = 16;
+
+// Single families, for the measured kernel selection.
+hipError_t launch_gemm_a16_tiled(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                                 hipStream_t stream);
+hipError_t launch_gemm_a8_tiled(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
+                                int32_t *partials, hipStream_t stream);
+hipError_t launch_gemv_a8_generic(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
+                                  int32_t *partials, hipStream_t stream);
+
+// Family predicates, defaults and launches (select.cpp).  Families are the
+// CQ_FAMILY_* values; path 0 = model dtype, 1 = Dynamic A8.
+bool family_supported(int path, int family, const cq_weight &w, int64_t m);
+int default_family(int path, const cq_weight &w, int64_t m, int64_t gemv_max_rows, bool partials);
+// table entry for this call, or CQ_FAMILY_AUTO
+int table_family(int path, const cq_weight &w, int x_dt, int64_t m);
+hipError_t run_family_a16(int family, const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                          hipStream_t stream);
+hipError_t run_family_a8(int family, const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
+                         int y_dt, int32_t *partials, hipStream_t stream);
+bool select_entry_valid(const cq_select_entry &e);
+bool select_entries_overlap(const cq_select_entry &a, const cq_select_entry &b);
+// replace the table (empty clears it)
+void select_install(std::vector<cq_select_entry> entries);
 
 }  // namespace cq

@@ -174,9 +174,8 @@ static hipError_t dispatch_bits(const cq_weight &w, const void *x, int64_t m, vo
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_gemm_a16(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
-                           hipStream_t stream) {
-    if (gemm_a16_mfma_supported(w, m)) return launch_gemm_a16_mfma(w, x, x_dt, m, y, y_dt, stream);
+hipError_t launch_gemm_a16_tiled(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                                 hipStream_t stream) {
     if (x_dt == 0) {
         if (y_dt == 0) return dispatch_bits<0, 0>(w, x, m, y, stream);
         return dispatch_bits<0, 2>(w, x, m, y, stream);

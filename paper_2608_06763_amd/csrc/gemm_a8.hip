@@ -218,11 +218,8 @@ static hipError_t dispatch_bits(const cq_weight &w, const int8_t *x8, const floa
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_gemm_a8(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
-                          int32_t *partials, hipStream_t stream) {
-    // W3 partials dumps stay on the 64x64 kernel
-    if (gemm_a8_mfma_supported(w, m) && (w.bits == 4 || !partials))
-        return launch_gemm_a8_mfma(w, x8, dx, m, y, y_dt, partials, stream);
+hipError_t launch_gemm_a8_tiled(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
+                                int32_t *partials, hipStream_t stream) {
     if (y_dt == 0) return dispatch_bits<0>(w, x8, dx, m, y, partials, nullptr, stream);
     if (y_dt == 1) return dispatch_bits<1>(w, x8, dx, m, y, partials, nullptr, stream);
     return dispatch_bits<2>(w, x8, dx, m, y, partials, nullptr, stream);

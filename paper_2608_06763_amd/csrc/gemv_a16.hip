@@ -112,20 +112,6 @@ static hipError_t dispatch_bits(const cq_weight &w, const void *x, int64_t m, vo
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_gemv_a16(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
-                           hipStream_t stream) {
-    if (m == 1 && stream_fits(w.n, w.k, w.bits, w.group)) return launch_gemv_a16_stream(w, x, x_dt, y, y_dt, stream);
-    // 2..4 rows: the table-decode family streams each weight once per row set
-    // with FP32 products and measured faster there; more rows go to the
-    // matrix-core narrow-row family
-    if (gemv_a16_lut_supported(w, m)) {
-        const hipError_t e = launch_gemv_a16_lut(w, x, x_dt, m, y, y_dt, stream);
-        if (e != hipErrorNotSupported) return e;
-    }
-    if (gemv_a16_narrow_supported(w, m)) return launch_gemv_a16_narrow(w, x, x_dt, m, y, y_dt, stream);
-    return launch_gemv_a16_generic(w, x, x_dt, m, y, y_dt, stream);
-}
-
 hipError_t launch_gemv_a16_generic(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                                    hipStream_t stream) {
     if (x_dt == 0) {

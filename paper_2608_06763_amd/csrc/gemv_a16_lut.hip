@@ -283,12 +283,14 @@ __global__ void __launch_bounds__(THREADS) gemv_a16_lut(
     }
 }
 
+constexpr size_t lut_lds_bytes_of(int B, int UPG, int R, int MR) {
+    return sizeof(float) * ((B <= 5 ? (size_t(1) << B) * THREADS : THREADS) +
+                            size_t(WAVES) * MR * (64 / R) * (UPG * 32 + 4) + size_t(WAVES) * R * MR);
+}
+
 template <int B, int UPG, int R, int MR>
 constexpr size_t lut_lds_bytes() {
-    constexpr int G = UPG * 32;
-    constexpr int P = 64 / R;
-    return sizeof(float) * ((B <= 5 ? (size_t(1) << B) * THREADS : THREADS) + size_t(WAVES) * MR * P * (G + 4) +
-                            size_t(WAVES) * R * MR);
+    return lut_lds_bytes_of(B, UPG, R, MR);
 }
 
 template <int B, int UPG, int R, int MR, int XDT, int YDT>
@@ -342,7 +344,12 @@ static hipError_t lut_bits(const cq_weight &w, const void *x, int64_t m, void *y
 }
 
 bool gemv_a16_lut_supported(const cq_weight &w, int64_t m) {
-    return w.group <= 128 ? m <= 4 : (w.group == 256 && m <= 1);
+    if (!(w.group <= 128 ? m <= 4 : (w.group == 256 && m <= 1))) return false;
+    // the (R, MR) configuration lut_rows picks must fit 64 KB of LDS
+    const int upg = w.group / 32;
+    const int r = upg >= 8 ? 16 : (m <= 1 ? 8 : 16);
+    const int mr = upg >= 8 ? 1 : (m <= 1 ? 1 : (m <= 2 ? 2 : 4));
+    return lut_lds_bytes_of(w.bits, upg, r, mr) <= 65536;
 }
 
 hipError_t launch_gemv_a16_lut(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,

@@ -398,6 +398,10 @@ static hipError_t stream_bits(const cq_weight &w, const void *x, void *y, hipStr
     return hipErrorNotSupported;
 }
 
+bool gemv_a16_stream_supported(const cq_weight &w, int64_t m) {
+    return m == 1 && stream_fits(w.n, w.k, w.bits, w.group);
+}
+
 hipError_t launch_gemv_a16_stream(const cq_weight &w, const void *x, int x_dt, void *y, int y_dt,
                                   hipStream_t stream) {
     if (x_dt == 0) {

@@ -139,11 +139,8 @@ static hipError_t dispatch_bits(const cq_weight &w, const int8_t *x8, const floa
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_gemv_a8(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
-                          int32_t *partials, hipStream_t stream) {
-    if (partials == nullptr && gemv_a8_stream_supported(w, m)) return launch_gemv_a8_stream(w, x8, dx, y, y_dt, stream);
-    if (partials == nullptr && gemv_a8_narrow_supported(w, m))
-        return launch_gemv_a8_narrow(w, x8, dx, m, y, y_dt, stream);
+hipError_t launch_gemv_a8_generic(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
+                                  int32_t *partials, hipStream_t stream) {
     if (y_dt == 0) return dispatch_bits<0>(w, x8, dx, m, y, partials, nullptr, stream);
     if (y_dt == 1) return dispatch_bits<1>(w, x8, dx, m, y, partials, nullptr, stream);
     return dispatch_bits<2>(w, x8, dx, m, y, partials, nullptr, stream);

@@ -1,0 +1,142 @@
+// Kernel-family predicates, the built-in row-regime rules and the measured
+// selection table (Sec. 5.5-5.6).  Host code only: nothing here touches device
+// memory, so the choice for a call can be queried without a GPU.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <memory>
+#include <mutex>
+#include <vector>
+
+#include "cq_internal.h"
+
+namespace cq {
+
+bool family_supported(int path, int family, const cq_weight &w, int64_t m) {
+    if (m < 1) return false;
+    if (path == CQ_PATH_MODEL_DTYPE) {
+        switch (family) {
+            case CQ_FAMILY_GEMV_STREAM: return gemv_a16_stream_supported(w, m);
+            case CQ_FAMILY_GEMV_LUT: return gemv_a16_lut_supported(w, m);
+            case CQ_FAMILY_GEMV_NARROW: return gemv_a16_narrow_supported(w, m);
+            case CQ_FAMILY_GEMV_GENERIC: return m <= kGemvMaxRows;
+            case CQ_FAMILY_GEMM_MFMA: return gemm_a16_mfma_supported(w, m);
+            case CQ_FAMILY_GEMM_TILED: return m <= int64_t(65535) * 64;
+        }
+        return false;
+    }
+    if (path == CQ_PATH_A8) {
+        switch (family) {
+            case CQ_FAMILY_GEMV_STREAM: return gemv_a8_stream_supported(w, m);
+            case CQ_FAMILY_GEMV_NARROW: return gemv_a8_narrow_supported(w, m);
+            case CQ_FAMILY_GEMV_GENERIC: return m <= kGemvMaxRows;
+            case CQ_FAMILY_GEMM_MFMA: return gemm_a8_mfma_supported(w, m);
+            case CQ_FAMILY_GEMM_TILED: return m <= int64_t(65535) * 64;
+        }
+        return false;
+    }
+    return false;
+}
+
+int default_family(int path, const cq_weight &w, int64_t m, int64_t gemv_max_rows, bool partials) {
+    const bool gemv = m <= gemv_max_rows && m <= kGemvMaxRows;
+    if (path == CQ_PATH_MODEL_DTYPE) {
+        if (gemv) {
+            if (gemv_a16_stream_supported(w, m)) return CQ_FAMILY_GEMV_STREAM;
+            // 2..4 rows: the table-decode family streams each weight once per
+            // row set with FP32 products and measured faster there; more rows
+            // go to the matrix-core narrow-row family
+            if (gemv_a16_lut_supported(w, m)) return CQ_FAMILY_GEMV_LUT;
+            if (gemv_a16_narrow_supported(w, m)) return CQ_FAMILY_GEMV_NARROW;
+            return CQ_FAMILY_GEMV_GENERIC;
+        }
+        return gemm_a16_mfma_supported(w, m) ? CQ_FAMILY_GEMM_MFMA : CQ_FAMILY_GEMM_TILED;
+    }
+    // Dynamic A8: a partials dump is written by the generic GEMV, the W4
+    // matrix-core GEMM and the 64 x 64 GEMM only
+    if (gemv) {
+        if (!partials && gemv_a8_stream_supported(w, m)) return CQ_FAMILY_GEMV_STREAM;
+        if (!partials && gemv_a8_narrow_supported(w, m)) return CQ_FAMILY_GEMV_NARROW;
+        return CQ_FAMILY_GEMV_GENERIC;
+    }
+    return gemm_a8_mfma_supported(w, m) && (w.bits == 4 || !partials) ? CQ_FAMILY_GEMM_MFMA : CQ_FAMILY_GEMM_TILED;
+}
+
+hipError_t run_family_a16(int family, const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                          hipStream_t stream) {
+    switch (family) {
+        case CQ_FAMILY_GEMV_STREAM: return launch_gemv_a16_stream(w, x, x_dt, y, y_dt, stream);
+        case CQ_FAMILY_GEMV_LUT: return launch_gemv_a16_lut(w, x, x_dt, m, y, y_dt, stream);
+        case CQ_FAMILY_GEMV_NARROW: return launch_gemv_a16_narrow(w, x, x_dt, m, y, y_dt, stream);
+        case CQ_FAMILY_GEMV_GENERIC: return launch_gemv_a16_generic(w, x, x_dt, m, y, y_dt, stream);
+        case CQ_FAMILY_GEMM_MFMA: return launch_gemm_a16_mfma(w, x, x_dt, m, y, y_dt, stream);
+        case CQ_FAMILY_GEMM_TILED: return launch_gemm_a16_tiled(w, x, x_dt, m, y, y_dt, stream);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t run_family_a8(int family, const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
+                         int y_dt, int32_t *partials, hipStream_t stream) {
+    switch (family) {
+        case CQ_FAMILY_GEMV_STREAM: return launch_gemv_a8_stream(w, x8, dx, y, y_dt, stream);
+        case CQ_FAMILY_GEMV_NARROW: return launch_gemv_a8_narrow(w, x8, dx, m, y, y_dt, stream);
+        case CQ_FAMILY_GEMV_GENERIC: return launch_gemv_a8_generic(w, x8, dx, m, y, y_dt, partials, stream);
+        case CQ_FAMILY_GEMM_MFMA: return launch_gemm_a8_mfma(w, x8, dx, m, y, y_dt, partials, stream);
+        case CQ_FAMILY_GEMM_TILED: return launch_gemm_a8_tiled(w, x8, dx, m, y, y_dt, partials, stream);
+    }
+    return hipErrorInvalidValue;
+}
+
+// ---------------------------------------------------------------- selection table
+
+namespace {
+
+using Table = std::vector<cq_select_entry>;
+
+std::mutex g_table_mutex;               // serialises writers
+std::shared_ptr<const Table> g_table;   // read with std::atomic_load
+std::atomic<bool> g_table_nonempty{false};
+
+bool entry_matches(const cq_select_entry &e, int path, const cq_weight &w, int x_dt, int64_t m) {
+    return e.path == path && e.bits == w.bits && e.group == w.group && e.n == w.n && e.k == w.k &&
+           (e.x_dtype < 0 || e.x_dtype == x_dt) && m >= e.m_lo && m <= e.m_hi;
+}
+
+}  // namespace
+
+int table_family(int path, const cq_weight &w, int x_dt, int64_t m) {
+    if (!g_table_nonempty.load(std::memory_order_acquire)) return CQ_FAMILY_AUTO;
+    const std::shared_ptr<const Table> t = std::atomic_load(&g_table);
+    if (!t) return CQ_FAMILY_AUTO;
+    for (const cq_select_entry &e : *t)
+        if (entry_matches(e, path, w, x_dt, m)) return e.family;
+    return CQ_FAMILY_AUTO;
+}
+
+bool select_entry_valid(const cq_select_entry &e) {
+    if (e.path != CQ_PATH_MODEL_DTYPE && e.path != CQ_PATH_A8) return false;
+    if (e.family < CQ_FAMILY_GEMV_STREAM || e.family > CQ_FAMILY_GEMM_TILED) return false;
+    if (e.path == CQ_PATH_A8 && e.family == CQ_FAMILY_GEMV_LUT) return false;
+    if (e.bits < 1 || e.bits > 8) return false;
+    if (e.group < 32 || e.group > 512 || e.group % 32) return false;
+    if (e.n < 1 || e.k < 1) return false;
+    if (e.m_lo < 1 || e.m_hi < e.m_lo) return false;
+    if (e.x_dtype < -1 || e.x_dtype > 1 || (e.path == CQ_PATH_A8 && e.x_dtype != -1)) return false;
+    return e.reserved == 0;
+}
+
+bool select_entries_overlap(const cq_select_entry &a, const cq_select_entry &b) {
+    const bool dtypes_meet = a.x_dtype < 0 || b.x_dtype < 0 || a.x_dtype == b.x_dtype;
+    return a.path == b.path && a.bits == b.bits && a.group == b.group && a.n == b.n && a.k == b.k && dtypes_meet &&
+           a.m_lo <= b.m_hi && b.m_lo <= a.m_hi;
+}
+
+void select_install(std::vector<cq_select_entry> entries) {
+    std::lock_guard<std::mutex> lock(g_table_mutex);
+    const bool nonempty = !entries.empty();
+    std::shared_ptr<const Table> t = nonempty ? std::make_shared<const Table>(std::move(entries)) : nullptr;
+    std::atomic_store(&g_table, t);
+    g_table_nonempty.store(nonempty, std::memory_order_release);
+}
+
+}  // namespace cq

@@ -218,3 +218,161 @@ def test_carrier_table_argument_errors_need_no_gpu():
     assert f(ctypes.byref(w), P(ok), P(ok), P(ok), 1, P(ok), 7, None) == 6
     assert f(ctypes.byref(w), P(bad_align), P(ok), P(ok), 1, P(ok), 0, None) == 3
     assert f(ctypes.byref(_desc(group=48)), P(ok), P(ok), P(ok), 1, P(ok), 0, None) == 1
+
+
+# ---------------------------------------------------------------- kernel selection (host logic only)
+
+
+def _fake(bits, group, n, k):
+    # descriptor with aligned placeholder addresses: the selection calls read
+    # only its fields
+    return cq.cq_weight(bits, group, n, k, 256, 512, 768, 1024)
+
+
+@pytest.fixture
+def clean_table():
+    cq.cq_select_set([])
+    yield
+    cq.cq_select_set([])
+    cq.cq_set_gemv_max_rows(0, -1)
+    cq.cq_set_gemv_max_rows(1, -1)
+
+
+@pytest.mark.parametrize("bits,group,m,md,a8", [
+    (4, 128, 1, "gemv_stream", "gemv_stream"),
+    (4, 128, 3, "gemv_lut", "gemv_narrow"),
+    (4, 256, 3, "gemv_narrow", "gemv_narrow"),
+    (4, 128, 8, "gemv_narrow", "gemv_narrow"),
+    (4, 32, 8, "gemv_narrow", "gemv_generic"),
+    (3, 128, 1, "gemv_stream", "gemv_stream"),
+    (3, 128, 8, "gemv_narrow", "gemv_generic"),
+    (6, 128, 1, "gemv_stream", "gemv_generic"),
+    (6, 128, 8, "gemv_generic", "gemv_generic"),
+    (4, 128, 17, "gemm_mfma", "gemm_mfma"),
+    (3, 64, 300, "gemm_mfma", "gemm_mfma"),
+    (3, 32, 300, "gemm_mfma", "gemm_tiled"),
+    (6, 128, 300, "gemm_tiled", "gemm_tiled"),
+])
+def test_builtin_rules(clean_table, bits, group, m, md, a8):
+    d = _fake(bits, group, 4096, 4096)
+    assert cq.cq_select_query(cq.CQ_PATH_MODEL_DTYPE, d, m) == md
+    assert cq.cq_select_query(cq.CQ_PATH_A8, d, m) == a8
+    assert cq.cq_family_supported(cq.CQ_PATH_MODEL_DTYPE, md, d, m)
+    assert cq.cq_family_supported(cq.CQ_PATH_A8, a8, d, m)
+
+
+def test_builtin_rules_follow_gemv_threshold(clean_table):
+    d = _fake(4, 128, 4096, 4096)
+    cq.cq_set_gemv_max_rows(0, 0)
+    assert cq.cq_select_query(cq.CQ_PATH_MODEL_DTYPE, d, 1) == "gemm_mfma"
+    assert cq.cq_select_query(cq.CQ_PATH_A8, d, 1) == "gemv_stream"
+
+
+def test_family_predicates():
+    d = _fake(4, 128, 4096, 4096)
+    md, a8 = cq.CQ_PATH_MODEL_DTYPE, cq.CQ_PATH_A8
+    assert not cq.cq_family_supported(md, "gemv_stream", d, 2)
+    assert not cq.cq_family_supported(md, "gemv_lut", d, 5)
+    assert not cq.cq_family_supported(md, "gemv_narrow", d, 1)
+    assert not cq.cq_family_supported(md, "gemv_generic", d, 17)
+    assert cq.cq_family_supported(md, "gemm_tiled", d, 1)
+    assert cq.cq_family_supported(md, "gemm_mfma", d, 1)
+    assert not cq.cq_family_supported(a8, "gemv_lut", d, 2)
+    assert not cq.cq_family_supported(a8, "auto", d, 2)
+    assert not cq.cq_family_supported(7, "gemm_tiled", d, 2)
+    # 32-bit buffer offsets: the streaming and matrix-core families stop below 2 GiB
+    big = _fake(8, 128, 1 << 18, 8192)
+    assert not cq.cq_family_supported(md, "gemv_stream", big, 1)
+    assert not cq.cq_family_supported(md, "gemm_mfma", big, 64)
+    assert cq.cq_family_supported(md, "gemv_generic", big, 1)
+    assert cq.cq_family_supported(md, "gemm_tiled", big, 64)
+
+
+def _entry(**kw):
+    e = {"path": 0, "family": "gemv_generic", "bits": 4, "group": 128, "n": 4096, "k": 4096, "m_lo": 1,
+         "m_hi": 16, "x_dtype": -1}
+    e.update(kw)
+    return e
+
+
+def test_table_overrides_and_falls_back(clean_table):
+    d = _fake(4, 128, 4096, 4096)
+    other = _fake(4, 128, 4096, 8192)
+    cq.cq_select_set([_entry(m_lo=1, m_hi=4, family="gemv_generic"),
+                      _entry(m_lo=5, m_hi=1000, family="gemm_tiled"),
+                      _entry(path=1, m_lo=1, m_hi=1, family="gemm_mfma"),
+                      # narrow cannot take one row: the built-in rules decide there
+                      _entry(path=1, m_lo=2, m_hi=8, family="gemv_generic"),
+                      _entry(path=1, m_lo=9, m_hi=16, family="gemv_narrow", group=32)])
+    md, a8 = cq.CQ_PATH_MODEL_DTYPE, cq.CQ_PATH_A8
+    assert cq.cq_select_query(md, d, 1) == "gemv_generic"
+    assert cq.cq_select_query(md, d, 4) == "gemv_generic"
+    assert cq.cq_select_query(md, d, 5) == "gemm_tiled"
+    assert cq.cq_select_query(md, d, 1000) == "gemm_tiled"
+    assert cq.cq_select_query(md, d, 1001) == "gemm_mfma"
+    assert cq.cq_select_query(md, other, 1) == "gemv_stream"
+    assert cq.cq_select_query(a8, d, 1) == "gemm_mfma"
+    assert cq.cq_select_query(a8, d, 8) == "gemv_generic"
+    assert cq.cq_select_query(a8, d, 12) == "gemv_narrow"
+    # an entry whose family cannot take the call is skipped
+    cq.cq_select_set([_entry(m_lo=1, m_hi=16, family="gemv_narrow")])
+    assert cq.cq_select_query(md, d, 1) == "gemv_stream"
+    assert cq.cq_select_query(md, d, 2) == "gemv_narrow"
+    cq.cq_select_set([])
+    assert cq.cq_select_query(md, d, 4) == "gemv_lut"
+
+
+def test_table_matches_activation_dtype(clean_table):
+    d = _fake(4, 128, 4096, 4096)
+    cq.cq_select_set([_entry(x_dtype=cq.CQ_FP16, family="gemv_generic")])
+    assert cq.cq_select_query(0, d, 1, cq.CQ_FP16) == "gemv_generic"
+    assert cq.cq_select_query(0, d, 1, cq.CQ_BF16) == "gemv_stream"
+
+
+@pytest.mark.parametrize("bad", [
+    dict(path=2), dict(family="auto"), dict(family=7), dict(path=1, family="gemv_lut"), dict(bits=0),
+    dict(bits=9), dict(group=48), dict(group=1024), dict(n=0), dict(k=0), dict(m_lo=0), dict(m_lo=5, m_hi=4),
+    dict(x_dtype=2), dict(path=1, x_dtype=0)])
+def test_table_rejects_malformed_entries(clean_table, bad):
+    d = _fake(4, 128, 4096, 4096)
+    cq.cq_select_set([_entry(family="gemv_generic")])
+    with pytest.raises(cq.CQError) as e:
+        cq.cq_select_set([_entry(m_lo=20, m_hi=30, family="gemm_tiled"), _entry(**bad)])
+    assert e.value.status == 1
+    # the previous table stays
+    assert cq.cq_select_query(0, d, 1) == "gemv_generic"
+
+
+def test_table_rejects_overlaps_and_reserved(clean_table):
+    with pytest.raises(cq.CQError):
+        cq.cq_select_set([_entry(m_lo=1, m_hi=8), _entry(m_lo=8, m_hi=9, family="gemm_tiled")])
+    with pytest.raises(cq.CQError):
+        cq.cq_select_set([_entry(x_dtype=-1), _entry(x_dtype=cq.CQ_BF16)])
+    # different dtypes, shapes or paths do not overlap
+    cq.cq_select_set([_entry(x_dtype=cq.CQ_FP16), _entry(x_dtype=cq.CQ_BF16), _entry(k=8192), _entry(path=1)])
+    L = cq.lib()
+    arr = (cq.cq_select_entry * 1)()
+    arr[0] = cq.cq_select_entry(0, 4, 4, 128, 4096, 4096, 1, 2, -1, 1)
+    assert L.cq_select_set(arr, 1) == 1
+    assert L.cq_select_set(None, 1) == 1
+    assert L.cq_select_set(arr, -1) == 1
+    assert L.cq_select_set(arr, 65537) == 1
+
+
+def test_forced_family_errors_need_no_gpu():
+    d = _fake(4, 128, 4096, 4096)
+    L = cq.lib()
+    buf = 4096
+    # unsupported family for the shape: rejected before any launch
+    assert L.cq_gemm_model_dtype_family(ctypes.byref(d), buf, 0, 2, buf, 0, cq.FAMILIES["gemv_stream"], None) == 8
+    assert L.cq_gemm_a8_family(ctypes.byref(d), buf, buf, 2, buf, 0, cq.FAMILIES["gemv_lut"], None) == 8
+    assert L.cq_gemm_a8_family(ctypes.byref(d), buf, buf, 1, buf, 0, 99, None) == 8
+    # argument checks come first
+    assert L.cq_gemm_model_dtype_family(ctypes.byref(d), None, 0, 2, buf, 0, 6, None) == 1
+    assert L.cq_gemm_model_dtype_family(ctypes.byref(d), buf, 2, 2, buf, 2, 6, None) == 6
+    assert L.cq_gemm_a8_family(ctypes.byref(d), buf + 4, buf, 2, buf, 0, 6, None) == 3
+    out = ctypes.c_int32(-1)
+    assert L.cq_select_query(3, ctypes.byref(d), 0, 1, ctypes.byref(out)) == 1
+    assert L.cq_select_query(0, ctypes.byref(d), 2, 1, ctypes.byref(out)) == 6
+    assert L.cq_select_query(0, ctypes.byref(d), 0, 0, ctypes.byref(out)) == 1
+    assert L.cq_family_supported(0, 1, None, 1) == 0

@@ -627,3 +627,122 @@ def test_gemm_a8_carriers_equals_gemm_a8(torch_dev, bits, group, m):
     assert R.eps_comp(_np(y), y_ref, "fp32") <= 1e-5
     y16 = cq.cq_gemm_a8_carriers(w, tab, x8, dx)
     assert R.eps_comp(_np(y16), y_ref, "bf16") <= TOL
+
+
+# ---------------------------------------------------------------- kernel families and the selection table
+
+MD_FAMILIES = ("gemv_stream", "gemv_lut", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_tiled")
+A8_FAMILIES = ("gemv_stream", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_tiled")
+
+
+@pytest.mark.parametrize("bits,group", [(4, 128), (3, 64), (6, 32), (2, 256)])
+@pytest.mark.parametrize("m", [1, 3, 8, 24])
+def test_every_family_matches_oracle(torch_dev, bits, group, m):
+    # every admissible family of both paths computes the oracle's product; the
+    # matrix-core model-dtype families carry the level as a BF16 hi + lo pair
+    # (16 significant bits), hence 2e-4 on their FP32 output
+    n, k = 131, 1024
+    r = fitted(140 + bits, n, k, bits, group)
+    xb, xv = act(141, m, k)
+    y16_ref = ref_model_dtype(xv, r, bits, group)
+    x8_ref, d_ref, y8_ref, _ = ref_a8(xv, r, bits, group)
+    cq = _cq()
+    w = _weight(r, bits, group)
+    x = _x(torch_dev, xb, "bf16")
+    x8 = torch_dev.from_numpy(x8_ref).cuda()
+    dx = torch_dev.from_numpy(d_ref).cuda()
+    ran = 0
+    for f in MD_FAMILIES:
+        if not cq.cq_family_supported(cq.CQ_PATH_MODEL_DTYPE, f, w, m):
+            with pytest.raises(cq.CQError):
+                cq.cq_gemm_model_dtype_family(w, x, f)
+            continue
+        say("family model dtype", f, bits, group, m)
+        y = cq.cq_gemm_model_dtype_family(w, x, f, y_dtype=torch_dev.float32)
+        assert R.eps_comp(_np(y), y16_ref, "fp32") <= 2e-4, f
+        assert R.eps_comp(_np(cq.cq_gemm_model_dtype_family(w, x, f)), y16_ref, "bf16") <= TOL, f
+        ran += 1
+    for f in A8_FAMILIES:
+        if not cq.cq_family_supported(cq.CQ_PATH_A8, f, w, m):
+            continue
+        say("family a8", f, bits, group, m)
+        y = cq.cq_gemm_a8_family(w, x8, dx, f, y_dtype=torch_dev.float32)
+        assert R.eps_comp(_np(y), y8_ref, "fp32") <= 1e-5, f
+        ran += 1
+    assert ran >= 2
+
+
+def test_selection_table_drives_dispatch(torch_dev):
+    # with a table installed the ordinary calls run the named family: their
+    # outputs equal the forced-family call bit for bit; clearing restores the
+    # built-in rules
+    cq = _cq()
+    n, k, bits, group = 300, 2048, 4, 128
+    r = fitted(150, n, k, bits, group)
+    w = _weight(r, bits, group)
+    md, a8 = cq.CQ_PATH_MODEL_DTYPE, cq.CQ_PATH_A8
+    table = [{"path": md, "family": "gemv_generic", "bits": bits, "group": group, "n": n, "k": k, "m_lo": 1,
+              "m_hi": 4, "x_dtype": cq.CQ_BF16},
+             {"path": md, "family": "gemm_tiled", "bits": bits, "group": group, "n": n, "k": k, "m_lo": 5,
+              "m_hi": 100},
+             {"path": a8, "family": "gemm_tiled", "bits": bits, "group": group, "n": n, "k": k, "m_lo": 1,
+              "m_hi": 100}]
+    try:
+        for m in (1, 3, 40):
+            xb, _ = act(151 + m, m, k)
+            x = _x(torch_dev, xb, "bf16")
+            x8, dx = cq.cq_quantize_act_a8(x)
+            say("selection table", m)
+            cq.cq_select_set([])
+            base_md = cq.cq_select_query(md, w, m)
+            y_default = cq.cq_gemm_model_dtype(w, x, y_dtype=torch_dev.float32)
+            assert torch_dev.equal(y_default, cq.cq_gemm_model_dtype_family(w, x, base_md, y_dtype=torch_dev.float32))
+            cq.cq_select_set(table)
+            f_md = cq.cq_select_query(md, w, m)
+            assert f_md == ("gemv_generic" if m <= 4 else "gemm_tiled")
+            y = cq.cq_gemm_model_dtype(w, x, y_dtype=torch_dev.float32)
+            assert torch_dev.equal(y, cq.cq_gemm_model_dtype_family(w, x, f_md, y_dtype=torch_dev.float32))
+            assert cq.cq_select_query(a8, w, m) == "gemm_tiled"
+            y8 = cq.cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32)
+            assert torch_dev.equal(y8, cq.cq_gemm_a8_family(w, x8, dx, "gemm_tiled", y_dtype=torch_dev.float32))
+            # the partials dump keeps the built-in rules and the same product
+            y8p, parts = cq.cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32, want_partials=True)
+            assert torch_dev.allclose(y8p, y8, rtol=1e-5, atol=1e-6)
+            # fp16 activations do not match the bf16-only entry for m <= 4
+            assert cq.cq_select_query(md, w, m, cq.CQ_FP16) == ("gemm_tiled" if m > 4 else base_md)
+    finally:
+        cq.cq_select_set([])
+    assert cq.cq_select_query(md, w, 1) == "gemv_stream"
+
+
+def test_tuner_selects_valid_families(torch_dev):
+    # the measured selection on a small shape: every timed family agreed with
+    # the built-in choice, the winner at each row count is the fastest one, the
+    # regimes cover every row count, and installing the table makes the
+    # dispatcher follow it
+    cq = _cq()
+    from paper_2608_06763_amd import selection as S
+    n, k, bits, group = 512, 2048, 4, 128
+    r = fitted(160, n, k, bits, group)
+    w = _weight(r, bits, group)
+    ms = [1, 3, 24]
+    try:
+        tables = []
+        for path in (cq.CQ_PATH_MODEL_DTYPE, cq.CQ_PATH_A8):
+            say("tuner", path)
+            t = S.tune(w, path, ms, target_ms=0.5, max_calls=8)
+            assert not t["rejected"]
+            for m in ms:
+                assert t["choice"][m] == min(t["timings"][m], key=t["timings"][m].get)
+                assert len(t["timings"][m]) >= 2
+            e = t["entries"]
+            assert e[0]["m_lo"] == 1 and e[-1]["m_hi"] == S.M_MAX
+            assert all(a["m_hi"] + 1 == b["m_lo"] for a, b in zip(e[:-1], e[1:]))
+            tables.append(t)
+        S.install(tables)
+        for t in tables:
+            path = t["signature"]["path"]
+            for m in ms:
+                assert cq.cq_select_query(path, w, m) == t["choice"][m]
+    finally:
+        S.clear()
