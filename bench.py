@@ -211,6 +211,30 @@ def rows_sweep(torch, cq, bits=4, group=128, k=8192, n=28672, ms=(1, 2, 8, 32, 1
     return {"shape": {"k": k, "n": n, "bits": bits, "group": group}, "rows": out, "a8_faster_from_m": cross}
 
 
+def selection_sweep(torch, cq, bits=4, group=128, k=8192, n=28672, ms=(1, 2, 8, 32, 128, 512, 2048, 8192)):
+    """Measured kernel selection on the crossover shape: every admissible family
+    of both paths timed at each row count; the table is reported, not kept."""
+    from paper_2608_06763_amd import selection as S
+    from workloads import crossover_act
+    w0 = make_weight(cq, 4001, n, k, bits, group)
+    act = lambda m: torch.from_numpy(crossover_act(m, k).view(np.int16)).cuda().view(torch.bfloat16)
+    out = {}
+    for path, name in ((cq.CQ_PATH_MODEL_DTYPE, "model_dtype"), (cq.CQ_PATH_A8, "a8")):
+        t = S.tune(w0, path, ms, activations=act, log=log)
+        S.clear()
+        builtin = {m: cq.cq_select_query(path, w0, m) for m in ms}
+        out[name] = {
+            "choice": {str(m): t["choice"][m] for m in ms},
+            "builtin": {str(m): builtin[m] for m in ms},
+            "timings_us": {str(m): {f: round(v, 2) for f, v in t["timings"][m].items()} for m in ms},
+            "speedup_vs_builtin": {str(m): round(t["timings"][m][builtin[m]] / t["timings"][m][t["choice"][m]], 3)
+                                   for m in ms},
+            "entries": [{k2: v for k2, v in e.items() if k2 != "bits" and k2 != "group"} for e in t["entries"]],
+            "rejected": {str(m): v for m, v in t["rejected"].items()},
+        }
+    return {"shape": {"k": k, "n": n, "bits": bits, "group": group}, "device": S.device_signature(), **out}
+
+
 # sources the dominant kernel is built from (its counter summary is keyed to them)
 KERNEL_SOURCES = ("paper_2608_06763_amd/csrc/gemv_a16_stream.hip", "paper_2608_06763_amd/csrc/stream_common.h",
                   "paper_2608_06763_amd/csrc/cq_device.h")
@@ -423,6 +447,7 @@ def main():
     if not args.no_sweep:
         log("[bench] rows sweep")
         result["rows_sweep"] = rows_sweep(torch, cq)
+        result["selection"] = selection_sweep(torch, cq)
         log("[bench] routed sweep")
         result["routed_sweep"] = routed_sweep(torch, cq)
     if not args.no_cpu_baseline:
