@@ -235,6 +235,44 @@ def selection_sweep(torch, cq, bits=4, group=128, k=8192, n=28672, ms=(1, 2, 8, 
     return {"shape": {"k": k, "n": n, "bits": bits, "group": group}, "device": S.device_signature(), **out}
 
 
+def measured_ceilings(torch):
+    """Measured ceilings beside the published peaks: a pure HBM read (the
+    library's streaming read probe over two alternating 1 GiB buffers,
+    together eight times the Infinity Cache) and the vendor library's dense
+    bf16 and int8 GEMMs at 8192^3 (hipBLASLt through torch; int8 only where
+    torch offers it)."""
+    import paper_2608_06763_amd as cq
+    out = {}
+    bufs = [torch.ones((1 << 28,), dtype=torch.float32, device="cuda") for _ in range(2)]
+    sink = torch.zeros((4,), dtype=torch.int32, device="cuda")
+    for b in bufs:
+        cq.cq_probe_read(b, sink)
+    torch.cuda.synchronize()
+    t = timed(torch, lambda i: cq.cq_probe_read(bufs[i % 2], sink), 20)
+    out["hbm_read_gbs"] = round((1 << 30) / t / 1e6, 1)
+    del bufs
+    n = 8192
+    a = torch.randn((n, n), device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    b = torch.randn((n, n), device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    torch.matmul(a, b)
+    torch.cuda.synchronize()
+    t = timed(torch, lambda i: torch.matmul(a, b), 10)
+    out["bf16_gemm_tflops"] = round(2.0 * n ** 3 / t / 1e9, 1)
+    del a, b
+    try:
+        a8 = torch.randint(-127, 128, (n, n), device="cuda", dtype=torch.int8)
+        b8 = torch.randint(-127, 128, (n, n), device="cuda", dtype=torch.int8)
+        torch._int_mm(a8, b8)
+        torch.cuda.synchronize()
+        t = timed(torch, lambda i: torch._int_mm(a8, b8), 10)
+        out["int8_gemm_tops"] = round(2.0 * n ** 3 / t / 1e9, 1)
+    except (RuntimeError, AttributeError) as e:
+        out["int8_gemm_tops"] = None
+        out["int8_note"] = f"torch int8 GEMM unavailable: {str(e).splitlines()[0][:120]}"
+    torch.cuda.synchronize()
+    return out
+
+
 # sources the dominant kernel is built from (its counter summary is keyed to them)
 KERNEL_SOURCES = ("paper_2608_06763_amd/csrc/gemv_a16_stream.hip", "paper_2608_06763_amd/csrc/stream_common.h",
                   "paper_2608_06763_amd/csrc/cq_device.h")
@@ -412,6 +450,8 @@ def main():
         log("[bench] copy calibration: 3 x 256 MiB device copies")
 
     traffic, traffic_note = measured_traffic()
+    ceil = measured_ceilings(torch)
+    log(f"[bench] measured ceilings: {ceil}")
     result = {
         "metric": "W4G128 GEMV effective HBM GB/s (M=1) + GEMM TFLOPS/TOPS vs rows M, % roofline",
         "value": round(value, 2),
@@ -442,11 +482,17 @@ def main():
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "avg_launch_us": round(gemv_ms * 1e3, 3),
                      "timing": "HIP events around K back-to-back passes of its four launches",
                      "bytes_per_launch": round(bytes_a16 / nl, 1), "traffic": traffic,
-                     "traffic_note": traffic_note, "kernel_source_sha256": kernel_source_hash()},
+                     "traffic_note": traffic_note, "kernel_source_sha256": kernel_source_hash(),
+                     "frac_of_measured_hbm_read": round(achieved / ceil["hbm_read_gbs"], 4)},
+        "measured_ceilings": ceil,
     }
     if not args.no_sweep:
         log("[bench] rows sweep")
         result["rows_sweep"] = rows_sweep(torch, cq)
+        for r in result["rows_sweep"]["rows"]:
+            r["a16_frac_of_measured_bf16_gemm"] = r["a16_tflops"] / ceil["bf16_gemm_tflops"]
+            if ceil.get("int8_gemm_tops"):
+                r["a8_frac_of_measured_int8_gemm"] = r["a8_tops"] / ceil["int8_gemm_tops"]
         result["selection"] = selection_sweep(torch, cq)
         log("[bench] routed sweep")
         result["routed_sweep"] = routed_sweep(torch, cq)

@@ -10,7 +10,7 @@ Entry points (same names as the C ABI):
   cq_gemm_a8, cq_gemm_a8_fused, cq_build_carriers, cq_gemm_a8_carriers,
   cq_gemm_routed_model_dtype, cq_set_gemv_max_rows, cq_get_gemv_max_rows,
   cq_family_supported, cq_gemm_model_dtype_family, cq_gemm_a8_family,
-  cq_select_set, cq_select_query
+  cq_select_set, cq_select_query, cq_probe_read (measurement aid)
 The measured kernel-selection tuner that fills the selection table is in
 ``selection.py``.
 """
@@ -32,7 +32,7 @@ EXPORTS = ("cq_status_str", "cq_pack_groups", "cq_decode_ref", "cq_gemm_model_dt
            "cq_gemm_a8", "cq_gemm_a8_fused", "cq_build_carriers", "cq_gemm_a8_carriers",
            "cq_gemm_routed_model_dtype", "cq_set_gemv_max_rows", "cq_get_gemv_max_rows",
            "cq_family_supported", "cq_gemm_model_dtype_family", "cq_gemm_a8_family", "cq_select_set",
-           "cq_select_query")
+           "cq_select_query", "cq_probe_read")
 
 CQ_PATH_MODEL_DTYPE, CQ_PATH_A8 = 0, 1
 FAMILIES = {"auto": 0, "gemv_stream": 1, "gemv_lut": 2, "gemv_narrow": 3, "gemv_generic": 4, "gemm_mfma": 5,
@@ -106,6 +106,8 @@ def lib() -> ctypes.CDLL:
     L.cq_select_set.argtypes = [ctypes.POINTER(cq_select_entry), i64]
     L.cq_select_query.restype = ctypes.c_int
     L.cq_select_query.argtypes = [i32, ctypes.POINTER(cq_weight), ctypes.c_int, i64, ctypes.POINTER(i32)]
+    L.cq_probe_read.restype = ctypes.c_int
+    L.cq_probe_read.argtypes = [vp, i64, vp, vp]
     _lib = L
     return L
 
@@ -385,3 +387,10 @@ def cq_select_query(path: int, w, m: int, x_dtype: int = CQ_BF16) -> str:
     out = ctypes.c_int32(-1)
     _check(lib().cq_select_query(path, ctypes.byref(_desc(w)), x_dtype, m, ctypes.byref(out)), "cq_select_query")
     return FAMILY_NAMES[out.value]
+
+
+def cq_probe_read(buf, sink, stream=None):
+    """Read the whole device tensor ``buf`` once (HBM read ceiling probe);
+    ``sink`` is a one-element int32 device tensor."""
+    _check(lib().cq_probe_read(buf.data_ptr(), buf.numel() * buf.element_size(), sink.data_ptr(), _stream_ptr(stream)),
+           "cq_probe_read")

@@ -307,6 +307,13 @@ cq_status cq_select_set(const cq_select_entry *entries, int64_t count) {
     return CQ_OK;
 }
 
+cq_status cq_probe_read(const void *buf, int64_t bytes, uint32_t *sink, void *stream) {
+    if (!buf || !sink || bytes < 0) return CQ_ERR_ARG;
+    if (bytes % 16) return CQ_ERR_ARG;
+    if (!aligned16(buf) || (reinterpret_cast<uintptr_t>(sink) & 3u)) return CQ_ERR_ALIGN;
+    return hip_status(cq::launch_read_probe(buf, bytes, sink, static_cast<hipStream_t>(stream)));
+}
+
 cq_status cq_select_query(int32_t path, const cq_weight *w, cq_dtype x_dtype, int64_t m, int32_t *family) {
     const cq_status st = check_weight(w);
     if (st != CQ_OK) return st;

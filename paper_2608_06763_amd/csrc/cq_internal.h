@@ -100,4 +100,7 @@ bool select_entries_overlap(const cq_select_entry &a, const cq_select_entry &b);
 // replace the table (empty clears it)
 void select_install(std::vector<cq_select_entry> entries);
 
+// Pure streaming read (measurement aid).
+hipError_t launch_read_probe(const void *buf, int64_t bytes, uint32_t *sink, hipStream_t stream);
+
 }  // namespace cq

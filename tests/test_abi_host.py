@@ -376,3 +376,13 @@ def test_forced_family_errors_need_no_gpu():
     assert L.cq_select_query(0, ctypes.byref(d), 2, 1, ctypes.byref(out)) == 6
     assert L.cq_select_query(0, ctypes.byref(d), 0, 0, ctypes.byref(out)) == 1
     assert L.cq_family_supported(0, 1, None, 1) == 0
+
+
+def test_probe_read_argument_errors_need_no_gpu():
+    L = cq.lib()
+    assert L.cq_probe_read(None, 16, 4096, None) == 1
+    assert L.cq_probe_read(4096, 16, None, None) == 1
+    assert L.cq_probe_read(4096, 17, 4096, None) == 1
+    assert L.cq_probe_read(4096, -16, 4096, None) == 1
+    assert L.cq_probe_read(4104, 16, 4096, None) == 3
+    assert L.cq_probe_read(4096, 16, 4098, None) == 3

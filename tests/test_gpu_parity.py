@@ -746,3 +746,16 @@ def test_tuner_selects_valid_families(torch_dev):
                 assert cq.cq_select_query(path, w, m) == t["choice"][m]
     finally:
         S.clear()
+
+
+def test_probe_read_reads_without_writing(torch_dev):
+    # the HBM read probe of the benchmark: completes on odd sizes and leaves
+    # its sink untouched for real data
+    cq = _cq()
+    sink = torch_dev.zeros((4,), dtype=torch_dev.int32, device="cuda")
+    for n in (4, 1000, 1 << 20):
+        buf = torch_dev.ones((n,), dtype=torch_dev.float32, device="cuda")
+        say("probe_read", n)
+        cq.cq_probe_read(buf, sink)
+    torch_dev.cuda.synchronize()
+    assert int(sink.abs().sum()) == 0
