@@ -15,14 +15,18 @@
 // (RW rows of one column block) before it decodes the current one, and the
 // activations of an item are converted to FP32 once for all RW rows.
 //
-// Decode.  The UPG = G/32 lanes that share a group share its level table:
-// every lane writes some of the 2^B signed normalised levels (0 for the
-// reserved pattern) into the table columns of all lanes of its group with
-// 128-bit LDS stores, then reads one entry per weight from its own column at
-// byte (field << 8) + lane * 4 + wave base, which is free of bank conflicts.
-// For W4 the address is assembled by one byte permute per weight, and the
-// reads are issued 16 weights ahead of the products that consume them.  B >= 6
-// evaluates the cubic in registers instead of keeping a 64..256-entry table.
+// Decode.  Every lane reads one entry per weight of a table of the 2^B signed
+// normalised levels (0 for the reserved pattern) in its own LDS column, at
+// byte (field << 8) + lane * 4 + slot base, which is free of bank conflicts.
+// For B <= 4 every lane also writes its whole column: W4 at G = 128 evaluates
+// two magnitudes per lane and gathers the group's eight through DPP, other
+// widths evaluate all of them; W1/W2 tables are constant and written once.
+// (Writing one value into the columns of all lanes of a group puts those
+// lanes' stores of different fields on the same four banks: B = 5 still does
+// that, with 128-bit stores.)  For W4 the address is assembled by one byte
+// permute per weight, and the reads are issued 16 weights ahead of the
+// products that consume them.  B >= 6 evaluates the cubic in registers
+// instead of keeping a 64..256-entry table.
 #include "cq_device.h"
 #include "cq_internal.h"
 #include "stream_common.h"
@@ -62,6 +66,9 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
     constexpr int M = max_code(B);
     constexpr bool LUT = (B <= 5);
     constexpr int NT = LUT ? (1 << B) : 1;
+    // B <= 4: every lane owns a full column of the table (no replicated stores,
+    // whose lanes of one group all hit the same four banks)
+    constexpr bool OWN = B <= 4;
     // LDS (dynamic, starting at address 0): one NT x 256-byte table per wave,
     // then the cross-wave partial sums.  The W4 address build relies on bits
     // 8..15 of the table base being zero.
@@ -163,11 +170,49 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
             al_r[r] = a * (1.0f / float(M));
             be_r[r] = b * (1.0f / float(M * M));
             ga_r[r] = cc * (1.0f / float(M * M * M));
-            if constexpr (LUT) {
-                // Lane j of a group evaluates magnitudes j, j + UPG, ... (their t = i/M
-                // are per-lane constants) and stores +q at field i and -q at field
-                // NT - i into the table columns of all UPG lanes of the group; the lane
-                // holding magnitude 0 also clears the reserved field NT/2.
+            if constexpr (OWN) {
+                // every lane writes its own column: +q at field i and -q at field
+                // NT - i for i = 1 .. M (fields 0 and NT/2 hold 0, and W1/W2 tables
+                // are constant, all written once before the loop)
+                if constexpr (B >= 3) {
+                    float qa[M + 1];
+                    if constexpr (B == 4 && UPG == 4) {
+                        // the group is one DPP quad: lane j evaluates magnitudes j
+                        // and j + 4, and every lane gathers all eight
+                        float qv[2];
+#pragma unroll
+                        for (int t = 0; t < 2; ++t) {
+                            const float q = tq[t] * __builtin_fmaf(tq[t], __builtin_fmaf(tq[t], cc, b), a);
+                            qv[t] = mag[t] == M ? 1.f : q;
+                        }
+#pragma unroll
+                        for (int t = 0; t < 2; ++t) {
+                            const int u = int(__float_as_uint(qv[t]));
+                            qa[4 * t + 0] = __uint_as_float(uint32_t(__builtin_amdgcn_mov_dpp(u, 0x00, 0xf, 0xf, true)));
+                            qa[4 * t + 1] = __uint_as_float(uint32_t(__builtin_amdgcn_mov_dpp(u, 0x55, 0xf, 0xf, true)));
+                            qa[4 * t + 2] = __uint_as_float(uint32_t(__builtin_amdgcn_mov_dpp(u, 0xaa, 0xf, 0xf, true)));
+                            qa[4 * t + 3] = __uint_as_float(uint32_t(__builtin_amdgcn_mov_dpp(u, 0xff, 0xf, 0xf, true)));
+                        }
+                    } else {
+#pragma unroll
+                        for (int i = 1; i < M; ++i) {
+                            const float t = float(i) * (1.0f / float(M));
+                            qa[i] = t * __builtin_fmaf(t, __builtin_fmaf(t, cc, b), a);
+                        }
+                        qa[M] = 1.f;
+                    }
+                    const uint32_t own = col + uint32_t(r) * (NT * 256u);
+#pragma unroll
+                    for (int i = 1; i <= M; ++i) {
+                        lds_st(own + uint32_t(i) * 256u, qa[i]);
+                        lds_st(own + uint32_t(NT - i) * 256u, -qa[i]);
+                    }
+                }
+            } else if constexpr (LUT) {
+                // B = 5: lane j of a group evaluates magnitudes j, j + UPG, ... (their
+                // t = i/M are per-lane constants) and stores +q at field i and -q at
+                // field NT - i into the table columns of all UPG lanes of the group;
+                // the lane holding magnitude 0 also clears the reserved field NT/2.
                 const uint32_t gslot = gcol + uint32_t(r) * (NT * 256u);
 #pragma unroll
                 for (int t = 0; t < MPL; ++t) {
@@ -323,6 +368,26 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
     Item ia, ib;
     int tile = blockIdx.x, cb = wave;
     if (tile >= ntiles) return;
+    if constexpr (OWN) {
+        // the entries no item rewrites
+#pragma unroll
+        for (int r = 0; r < RW; ++r) {
+            const uint32_t own = col + uint32_t(r) * (NT * 256u);
+            if constexpr (B == 1) {
+                lds_st(own, -1.f);
+                lds_st(own + 256u, 1.f);
+            } else if constexpr (B == 2) {
+                lds_st(own, 0.f);
+                lds_st(own + 256u, 1.f);
+                lds_st(own + 512u, 0.f);
+                lds_st(own + 768u, -1.f);
+            } else {
+                lds_st(own, 0.f);
+                lds_st(own + uint32_t(NT / 2) * 256u, 0.f);
+            }
+        }
+        wave_lds_fence();
+    }
     fetch(ia, tile, cb, true);
     while (true) {
         int t1 = tile, c1 = cb;
