@@ -251,6 +251,11 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
             // reads of chunk c + 1 are issued before the products of chunk c, so
             // a wave keeps 16 to 32 LDS reads in flight.
             constexpr int BT = 16;
+            // the nibble mask lives in a vector register, so that mask and slot
+            // tag fold into one v_and_or_b32 (a literal and a scalar tag would
+            // exceed the one scalar operand a VOP3 instruction may read)
+            uint32_t nmask;
+            __asm__("v_mov_b32 %0, 0x0f0f0f0f" : "=v"(nmask));
             constexpr int CH = RW * 32 / BT;
             float lvb[2][BT];
             float pp[RW][2];
@@ -265,7 +270,7 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                     const int r = wi / 32, i = wi % 32;
                     const uint32_t wd = it.w[r][i / 8];
                     const uint32_t nib =
-                        ((i & 1) ? ((wd >> 4) & 0x0f0f0f0fu) : (wd & 0x0f0f0f0fu)) | (wtag + uint32_t(r) * 0x10101010u);
+                        ((i & 1) ? ((wd >> 4) & nmask) : (wd & nmask)) | (wtag + uint32_t(r) * 0x10101010u);
                     const uint32_t sel = 0x03020000u | (uint32_t(4 + (i % 8) / 2) << 8);
                     dst[e] = lds_ld(__builtin_amdgcn_perm(nib, col + uint32_t(r) * (NT * 256u), sel));
                 }
