@@ -178,7 +178,7 @@ def test_model_dtype_deterministic(torch_dev):
 # ---------------------------------------------------------------- Dynamic A8
 
 
-@pytest.mark.parametrize("m,k", [(1, 32), (7, 4096), (64, 768)])
+@pytest.mark.parametrize("m,k", [(1, 32), (7, 4096), (64, 768), (1, 4096), (1, 14336), (3, 18432), (2, 65568), (1, 139264), (600, 2080)])
 @pytest.mark.parametrize("dtype", ["bf16", "fp16"])
 def test_quantize_act_a8_bitexact(torch_dev, m, k, dtype):
     xb, xv = act(12 + m, m, k, dtype)
@@ -506,6 +506,7 @@ def test_gemm_a8_fused_carriers_near_rounding_boundaries(torch_dev, dtype):
     for i in range(0, len(top), 2000):
         rows.append((127.0, top[i:i + 2000]))
     hits = 0
+    batch = []
     for amax, pick in rows:
         row = np.zeros((1, k))
         vals = np.concatenate([pick, -pick])[:k - 1]
@@ -515,10 +516,24 @@ def test_gemm_a8_fused_carriers_near_rounding_boundaries(torch_dev, dtype):
         q = row / np.float64(d_ref[0])
         hits += int(np.sum(np.abs(np.abs(q - np.round(q)) - 0.5) < 2.0 ** -15))
         say("fused boundary", dtype, amax, len(vals))
-        _, x8, dx = _cq().cq_gemm_a8_fused(w, _x(torch_dev, _encode(row, dtype), dtype), y_dtype=torch_dev.float32)
+        xt = _x(torch_dev, _encode(row, dtype), dtype)
+        _, x8, dx = _cq().cq_gemm_a8_fused(w, xt, y_dtype=torch_dev.float32)
         assert np.array_equal(dx.cpu().numpy(), d_ref.astype(np.float32))
         assert np.array_equal(x8.cpu().numpy(), x8_ref), (dtype, amax)
+        # the standalone quantizer takes the same reciprocal path
+        x8q, dxq = _cq().cq_quantize_act_a8(xt)
+        assert np.array_equal(dxq.cpu().numpy(), d_ref.astype(np.float32))
+        assert np.array_equal(x8q.cpu().numpy(), x8_ref), (dtype, amax)
+        batch.append(row[0])
     assert hits >= 48
+    # many rows at once (the 256-thread configuration), rows repeated to 600
+    rows_np = np.stack(batch)
+    rows_np = np.concatenate([rows_np] * (600 // len(rows_np) + 1))[:600]
+    x8_ref, d_ref = A8.quantize_act(rows_np)
+    say("quantizer boundary batch", dtype, rows_np.shape)
+    x8q, dxq = _cq().cq_quantize_act_a8(_x(torch_dev, _encode(rows_np, dtype), dtype))
+    assert np.array_equal(dxq.cpu().numpy(), d_ref.astype(np.float32))
+    assert np.array_equal(x8q.cpu().numpy(), x8_ref)
 
 
 # ---------------------------------------------------------------- routed (mixture-of-experts) product
