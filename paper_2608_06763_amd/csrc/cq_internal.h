@@ -53,6 +53,11 @@ hipError_t launch_gemv_a16_routed(const cq_weight &w, int n_experts, const void 
                                   const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
                                   int y_dt, hipStream_t stream);
 bool routed_supported(const cq_weight &w, int64_t n_experts, int64_t tokens, int64_t routes);
+// Routed product with every route streaming its expert (few routes per expert).
+bool gemv_a16_stream_routed_supported(const cq_weight &w, int64_t n_experts, int64_t tokens, int64_t routes);
+hipError_t launch_gemv_a16_stream_routed(const cq_weight &w, int n_experts, const void *x, int x_dt, int64_t tokens,
+                                         const int32_t *token, const int32_t *expert, int64_t routes, void *y,
+                                         int y_dt, hipStream_t stream);
 int carrier_table_bytes(int bits);
 hipError_t launch_build_carriers(const cq_weight &w, int8_t *out, hipStream_t stream);
 hipError_t launch_gemv_a8_tab(const cq_weight &w, const int8_t *ctab, const int8_t *x8, const float *dx, int64_t m,

@@ -57,11 +57,17 @@ __device__ __forceinline__ void wave_lds_fence() {
 
 }  // namespace
 
-template <int B, int UPG, int RW, int XDT, int YDT>
+// ROUTED: a bank of n_experts matrices of n rows each (expert e at row e * n)
+// and `routes` (token, expert) pairs; route r computes x[token] W_expert^T
+// into row r of y, every route streaming its expert's weights (the decode
+// case of a few routes per expert).  Routes naming a token or expert out of
+// range are skipped and their output row is not written.
+template <int B, int UPG, int RW, int XDT, int YDT, bool ROUTED>
 __global__ void __launch_bounds__(256) gemv_a16_stream(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
-    int n, int k, const uint16_t *__restrict__ x, void *__restrict__ y) {
+    int n, int k, const uint16_t *__restrict__ x, void *__restrict__ y,
+    const int32_t *__restrict__ rtok, const int32_t *__restrict__ rexp, int routes, int tokens, int n_experts) {
     constexpr int G = UPG * 32;
     constexpr int M = max_code(B);
     constexpr bool LUT = (B <= 5);
@@ -79,15 +85,18 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
     const int nwaves = blockDim.x >> 6;  // the host keeps nwaves <= ncb
     float *red = tab + nwaves * RW * NT * 64;
     const int ntiles = (n + RW - 1) / RW;
+    // item space: the row tiles, or (route, row tile) pairs, route-major
+    const int nitems_t = ROUTED ? ntiles * routes : ntiles;
     const int units = k >> 5;
     const int ncb = (units + 63) >> 6;
     const int ng = k / G;
     const uint32_t row_bytes = uint32_t(k) * B / 8;
-    const auto rc = make_rsrc(codes, uint32_t(n) * row_bytes);
-    const auto rs = make_rsrc(scale, uint32_t(n) * ng * 4u);
-    const auto ra = make_rsrc(a16, uint32_t(n) * ng * 2u);
-    const auto rb = make_rsrc(b16, uint32_t(n) * ng * 2u);
-    const auto rx = make_rsrc(x, uint32_t(k) * 2u);
+    const uint32_t bank_rows = ROUTED ? uint32_t(n) * uint32_t(n_experts) : uint32_t(n);
+    const auto rc = make_rsrc(codes, bank_rows * row_bytes);
+    const auto rs = make_rsrc(scale, bank_rows * ng * 4u);
+    const auto ra = make_rsrc(a16, bank_rows * ng * 2u);
+    const auto rb = make_rsrc(b16, bank_rows * ng * 2u);
+    const auto rx = make_rsrc(x, uint32_t(ROUTED ? tokens : 1) * uint32_t(k) * 2u);
     const uint32_t tbase = uint32_t(uintptr_t((lds_f *)tab));
     // one table per (wave, row of the tile): slot index wave * RW + r
     const uint32_t col = tbase + uint32_t(wave * RW) * (NT * 256u) + uint32_t(lane) * 4u;
@@ -120,11 +129,34 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
         float s[RW];
         uint32_t a[RW], b[RW];
         uint32_t x[16];
+        bool ok;  // routed: the route names a valid token and expert
+    };
+    // route and row tile of an item (routed), else the row tile itself
+    auto split = [&](int ti, int &route, int &t) CQ_INLINE {
+        if constexpr (ROUTED) {
+            route = ti / ntiles;
+            t = ti - route * ntiles;
+        } else {
+            route = 0;
+            t = ti;
+        }
     };
     // An item past the last tile (ok false) still issues its loads, at an
     // out-of-range offset that reads zeros: every path through the loop then
     // has the same loads in flight, and the waits stay exact.
-    auto fetch = [&](Item &it, int t, int c, bool ok) CQ_INLINE {
+    auto fetch = [&](Item &it, int ti, int c, bool ok) CQ_INLINE {
+        int route, t;
+        split(ti, route, t);
+        uint32_t row_base = 0, x_base = 0;
+        if constexpr (ROUTED) {
+            const int rr = ok ? route : 0;
+            const int tok = __builtin_amdgcn_readfirstlane(rtok[rr]);
+            const int ex = __builtin_amdgcn_readfirstlane(rexp[rr]);
+            ok = ok && tok >= 0 && tok < tokens && ex >= 0 && ex < n_experts;
+            row_base = ok ? uint32_t(ex) * uint32_t(n) : 0u;
+            x_base = ok ? uint32_t(tok) * uint32_t(k) * 2u : 0u;
+        }
+        it.ok = ok;
         const int u = c * 64 + lane;
         const bool uok = ok && u < units;
         const uint32_t vc = uok ? uint32_t(u) * (4 * B) : kOobOffset;
@@ -133,21 +165,23 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
         const uint32_t xo = uok ? uint32_t(u) * 64u : kOobOffset;
 #pragma unroll
         for (int r = 0; r < RW; ++r) {
-            const uint32_t row = uint32_t(min(t * RW + r, n - 1));  // t may be past the last tile
+            const uint32_t row = row_base + uint32_t(min(t * RW + r, n - 1));  // t may be past the last tile
             const uint32_t gi = row * uint32_t(ng);
             load_words_s<B>(rc, vc, row * row_bytes, it.w[r]);
             it.s[r] = load_f32_s(rs, vm, gi * 4u);
             it.a[r] = load_u16_s(ra, vh, gi * 2u);
             it.b[r] = load_u16_s(rb, vh, gi * 2u);
         }
-        load_words<16>(rx, xo, it.x);
+        load_words_s<16>(rx, xo, x_base, it.x);
     };
 
     float acc[RW];
 #pragma unroll
     for (int i = 0; i < RW; ++i) acc[i] = 0.f;
 
-    auto process = [&](const Item &it, int tile, bool last_cb) CQ_INLINE {
+    auto process = [&](const Item &it, int ti, bool last_cb) CQ_INLINE {
+        int route, tile;
+        split(ti, route, tile);
         // ---- activations of this unit, FP32 in registers
         float xf[32];
 #pragma unroll
@@ -333,12 +367,25 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
         if (last_cb) {
             const int row0 = tile * RW;
             static_assert(RW == 2, "the output store writes row pairs");
+            // one lane stores the tile's row pair (routed: row route * n + row,
+            // two single stores, as that index can be odd; invalid routes store
+            // nothing)
+            auto store = [&](float v0, float v1) CQ_INLINE {
+                if constexpr (ROUTED) {
+                    if (!it.ok) return;
+                    const int64_t o = int64_t(route) * n + row0;
+                    store_out<YDT>(y, o, v0);
+                    if (row0 + 1 < n) store_out<YDT>(y, o + 1, v1);
+                } else {
+                    store_row_pair<YDT>(y, row0, v0, v1, row0 + 1 < n);
+                }
+            };
             if (nwaves == 1) {
                 const float v0 = wave_sum(acc[0]);
                 const float v1 = wave_sum(acc[1]);
                 acc[0] = 0.f;
                 acc[1] = 0.f;
-                if (lane == 0 && row0 < n) store_row_pair<YDT>(y, row0, v0, v1, row0 + 1 < n);
+                if (lane == 0 && row0 < n) store(v0, v1);
             } else {
 #pragma unroll
                 for (int r = 0; r < RW; ++r) {
@@ -353,7 +400,7 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                         v0 += red[wv * RW];
                         v1 += red[wv * RW + 1];
                     }
-                    store_row_pair<YDT>(y, row0, v0, v1, row0 + 1 < n);
+                    store(v0, v1);
                 }
                 __syncthreads();  // red is reused by the next tile
             }
@@ -372,7 +419,7 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
 
     Item ia, ib;
     int tile = blockIdx.x, cb = wave;
-    if (tile >= ntiles) return;
+    if (tile >= nitems_t) return;
     if constexpr (OWN) {
         // the entries no item rewrites
 #pragma unroll
@@ -398,14 +445,14 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
         int t1 = tile, c1 = cb;
         advance(t1, c1);
         const bool last0 = t1 != tile;
-        const bool have1 = t1 < ntiles;
+        const bool have1 = t1 < nitems_t;
         fetch(ib, t1, c1, have1);
         process(ia, tile, last0);
         if (!have1) break;
         int t2 = t1, c2 = c1;
         advance(t2, c2);
         const bool last1 = t2 != t1;
-        const bool have2 = t2 < ntiles;
+        const bool have2 = t2 < nitems_t;
         fetch(ia, t2, c2, have2);
         process(ib, t1, last1);
         if (!have2) break;
@@ -414,8 +461,15 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
     }
 }
 
-template <int B, int UPG, int RW, int XDT, int YDT>
-static hipError_t stream_waves(const cq_weight &w, const void *x, void *y, hipStream_t stream) {
+// route map of the routed mode (unused otherwise)
+struct StreamRoutes {
+    const int32_t *tok = nullptr, *exp = nullptr;
+    int routes = 0, tokens = 0, n_experts = 0;
+};
+
+template <int B, int UPG, int RW, int XDT, int YDT, bool ROUTED>
+static hipError_t stream_waves(const cq_weight &w, const void *x, void *y, const StreamRoutes &rt,
+                               hipStream_t stream) {
     const int64_t ncb = ((w.k >> 5) + 63) >> 6;
     constexpr int NT = B <= 5 ? (1 << B) : 1;
     constexpr int kMaxW = NT >= 32 ? 2 : 4;  // keep the tables within 32 KB and the W4 slot tag in 4 bits
@@ -425,47 +479,63 @@ static hipError_t stream_waves(const cq_weight &w, const void *x, void *y, hipSt
     int nw = ncb > 2 ? 2 : 1;
     if (nw > kMaxW) nw = kMaxW;
     const size_t lds = sizeof(float) * (size_t(nw) * RW * NT * 64 + size_t(nw) * RW);
-    const int64_t tiles = (w.n + RW - 1) / RW;
+    const int64_t tiles = (w.n + RW - 1) / RW * (ROUTED ? rt.routes : 1);
+    if (tiles < 1) return hipSuccess;
     // one workgroup per tile up to 64 per CU; the kernel strides over the rest
     int64_t blocks = int64_t(device_cu_count()) * 64;
     if (blocks > tiles) blocks = tiles;
-    hipLaunchKernelGGL((gemv_a16_stream<B, UPG, RW, XDT, YDT>), dim3(unsigned(blocks)), dim3(nw * 64), lds, stream,
-                       w.codes, w.scale, w.a, w.b, int(w.n), int(w.k), static_cast<const uint16_t *>(x), y);
+    hipLaunchKernelGGL((gemv_a16_stream<B, UPG, RW, XDT, YDT, ROUTED>), dim3(unsigned(blocks)), dim3(nw * 64), lds,
+                       stream, w.codes, w.scale, w.a, w.b, int(w.n), int(w.k), static_cast<const uint16_t *>(x), y,
+                       rt.tok, rt.exp, rt.routes, rt.tokens, rt.n_experts);
     return hipGetLastError();
 }
 
-template <int B, int UPG, int XDT, int YDT>
-static hipError_t stream_rows(const cq_weight &w, const void *x, void *y, hipStream_t stream) {
+template <int B, int UPG, int XDT, int YDT, bool ROUTED>
+static hipError_t stream_rows(const cq_weight &w, const void *x, void *y, const StreamRoutes &rt,
+                              hipStream_t stream) {
     // two rows per workgroup: the smallest tile keeps the most workgroups in
     // flight, which is what hides the load latency of a streaming GEMV
-    return stream_waves<B, UPG, 2, XDT, YDT>(w, x, y, stream);
+    return stream_waves<B, UPG, 2, XDT, YDT, ROUTED>(w, x, y, rt, stream);
 }
 
-template <int B, int XDT, int YDT>
-static hipError_t stream_group(const cq_weight &w, const void *x, void *y, hipStream_t stream) {
+template <int B, int XDT, int YDT, bool ROUTED>
+static hipError_t stream_group(const cq_weight &w, const void *x, void *y, const StreamRoutes &rt,
+                               hipStream_t stream) {
     switch (w.group) {
-        case 32: return stream_rows<B, 1, XDT, YDT>(w, x, y, stream);
-        case 64: return stream_rows<B, 2, XDT, YDT>(w, x, y, stream);
-        case 128: return stream_rows<B, 4, XDT, YDT>(w, x, y, stream);
-        case 256: return stream_rows<B, 8, XDT, YDT>(w, x, y, stream);
-        case 512: return stream_rows<B, 16, XDT, YDT>(w, x, y, stream);
+        case 32: return stream_rows<B, 1, XDT, YDT, ROUTED>(w, x, y, rt, stream);
+        case 64: return stream_rows<B, 2, XDT, YDT, ROUTED>(w, x, y, rt, stream);
+        case 128: return stream_rows<B, 4, XDT, YDT, ROUTED>(w, x, y, rt, stream);
+        case 256: return stream_rows<B, 8, XDT, YDT, ROUTED>(w, x, y, rt, stream);
+        case 512: return stream_rows<B, 16, XDT, YDT, ROUTED>(w, x, y, rt, stream);
     }
     return hipErrorNotSupported;
 }
 
-template <int XDT, int YDT>
-static hipError_t stream_bits(const cq_weight &w, const void *x, void *y, hipStream_t stream) {
+template <int XDT, int YDT, bool ROUTED>
+static hipError_t stream_bits(const cq_weight &w, const void *x, void *y, const StreamRoutes &rt,
+                              hipStream_t stream) {
     switch (w.bits) {
-        case 1: return stream_group<1, XDT, YDT>(w, x, y, stream);
-        case 2: return stream_group<2, XDT, YDT>(w, x, y, stream);
-        case 3: return stream_group<3, XDT, YDT>(w, x, y, stream);
-        case 4: return stream_group<4, XDT, YDT>(w, x, y, stream);
-        case 5: return stream_group<5, XDT, YDT>(w, x, y, stream);
-        case 6: return stream_group<6, XDT, YDT>(w, x, y, stream);
-        case 7: return stream_group<7, XDT, YDT>(w, x, y, stream);
-        case 8: return stream_group<8, XDT, YDT>(w, x, y, stream);
+        case 1: return stream_group<1, XDT, YDT, ROUTED>(w, x, y, rt, stream);
+        case 2: return stream_group<2, XDT, YDT, ROUTED>(w, x, y, rt, stream);
+        case 3: return stream_group<3, XDT, YDT, ROUTED>(w, x, y, rt, stream);
+        case 4: return stream_group<4, XDT, YDT, ROUTED>(w, x, y, rt, stream);
+        case 5: return stream_group<5, XDT, YDT, ROUTED>(w, x, y, rt, stream);
+        case 6: return stream_group<6, XDT, YDT, ROUTED>(w, x, y, rt, stream);
+        case 7: return stream_group<7, XDT, YDT, ROUTED>(w, x, y, rt, stream);
+        case 8: return stream_group<8, XDT, YDT, ROUTED>(w, x, y, rt, stream);
     }
     return hipErrorNotSupported;
+}
+
+template <bool ROUTED>
+static hipError_t stream_dtypes(const cq_weight &w, const void *x, int x_dt, void *y, int y_dt,
+                                const StreamRoutes &rt, hipStream_t stream) {
+    if (x_dt == 0) {
+        if (y_dt == 0) return stream_bits<0, 0, ROUTED>(w, x, y, rt, stream);
+        return stream_bits<0, 2, ROUTED>(w, x, y, rt, stream);
+    }
+    if (y_dt == 1) return stream_bits<1, 1, ROUTED>(w, x, y, rt, stream);
+    return stream_bits<1, 2, ROUTED>(w, x, y, rt, stream);
 }
 
 bool gemv_a16_stream_supported(const cq_weight &w, int64_t m) {
@@ -474,12 +544,25 @@ bool gemv_a16_stream_supported(const cq_weight &w, int64_t m) {
 
 hipError_t launch_gemv_a16_stream(const cq_weight &w, const void *x, int x_dt, void *y, int y_dt,
                                   hipStream_t stream) {
-    if (x_dt == 0) {
-        if (y_dt == 0) return stream_bits<0, 0>(w, x, y, stream);
-        return stream_bits<0, 2>(w, x, y, stream);
-    }
-    if (y_dt == 1) return stream_bits<1, 1>(w, x, y, stream);
-    return stream_bits<1, 2>(w, x, y, stream);
+    return stream_dtypes<false>(w, x, x_dt, y, y_dt, StreamRoutes{}, stream);
+}
+
+bool gemv_a16_stream_routed_supported(const cq_weight &w, int64_t n_experts, int64_t tokens, int64_t routes) {
+    const int64_t lim = int64_t(1) << 31;
+    return stream_fits(w.n * n_experts, w.k, w.bits, w.group) && tokens * w.k * 2 < lim && routes * w.n < lim &&
+           (w.n + 1) / 2 * routes < lim / 2;
+}
+
+hipError_t launch_gemv_a16_stream_routed(const cq_weight &w, int n_experts, const void *x, int x_dt, int64_t tokens,
+                                         const int32_t *token, const int32_t *expert, int64_t routes, void *y,
+                                         int y_dt, hipStream_t stream) {
+    StreamRoutes rt;
+    rt.tok = token;
+    rt.exp = expert;
+    rt.routes = int(routes);
+    rt.tokens = int(tokens);
+    rt.n_experts = n_experts;
+    return stream_dtypes<true>(w, x, x_dt, y, y_dt, rt, stream);
 }
 
 }  // namespace cq

@@ -76,6 +76,12 @@ bool routed_supported(const cq_weight &w, int64_t n_experts, int64_t tokens, int
 hipError_t launch_routed_model_dtype(const cq_weight &w, int n_experts, const void *x, int x_dt, int64_t tokens,
                                      const int32_t *token, const int32_t *expert, int64_t routes, int32_t *workspace,
                                      void *y, int y_dt, hipStream_t stream) {
+    // At most one route per expert on average (decode): every route streams
+    // its expert's weights once, with no grouping pass; the expert-grouped
+    // matrix-core path decodes each weight tile once for all routes of its
+    // expert and wins when experts receive several routes.
+    if (routes <= n_experts && gemv_a16_stream_routed_supported(w, n_experts, tokens, routes))
+        return launch_gemv_a16_stream_routed(w, n_experts, x, x_dt, tokens, token, expert, routes, y, y_dt, stream);
     int32_t *offsets = workspace;
     int32_t *order = workspace + n_experts + 1;
     const size_t lds = sizeof(int) * size_t(n_experts + 1);

@@ -541,11 +541,13 @@ def test_gemm_a8_fused_carriers_near_rounding_boundaries(torch_dev, dtype):
 
 @pytest.mark.parametrize("bits", [1, 2, 3, 4, 5])
 @pytest.mark.parametrize("group", [32, 128])
-@pytest.mark.parametrize("experts,tokens", [(1, 5), (3, 40), (8, 1), (8, 16)])
+@pytest.mark.parametrize("experts,tokens", [(1, 5), (3, 40), (8, 1), (8, 4), (8, 16)])
 def test_routed_model_dtype(torch_dev, bits, group, experts, tokens):
     # route-major outputs for a skewed top-2 route map (top-1 with one expert);
-    # 37 rows per expert (ragged strip), experts with more than 16 routes run
-    # several chunks; every route against the oracle
+    # 37 rows per expert (ragged strip, odd: route rows start at odd offsets),
+    # experts with more than 16 routes run several chunks; up to one route per
+    # expert (8 experts, 1 or 4 tokens) takes the streaming mode; every route
+    # against the oracle
     from oracle import routed as RT
     from workloads import route_map, synthetic_representation
     n, k = 37, 1024
@@ -568,12 +570,14 @@ def test_routed_model_dtype(torch_dev, bits, group, experts, tokens):
         assert torch_dev.equal(y, y2)
 
 
-def test_routed_invalid_routes_untouched(torch_dev):
+@pytest.mark.parametrize("experts", [4, 8])
+def test_routed_invalid_routes_untouched(torch_dev, experts):
     # routes naming a missing token or expert are dropped; their rows keep
-    # the caller's contents, the others match the oracle
+    # the caller's contents, the others match the oracle (7 routes: grouped
+    # mode with 4 experts, streaming mode with 8)
     from oracle import routed as RT
     from workloads import synthetic_representation
-    bits, group, experts, n, k, tokens = 4, 128, 4, 20, 512, 6
+    bits, group, n, k, tokens = 4, 128, 20, 512, 6
     codes, s, a, b = synthetic_representation(95, experts * n, k, bits, group)
     cq = _cq()
     bank = cq.CQWeight.from_codes(codes, s, a, b, bits, group)
@@ -587,7 +591,7 @@ def test_routed_invalid_routes_untouched(torch_dev):
                                   torch_dev.from_numpy(exp).cuda(), out=y)
     got = _np(y)
     valid = np.isfinite(y_ref[:, 0])
-    assert list(valid) == [True, True, False, False, False, False, True]
+    assert list(valid) == [True, True, False, False, experts > 4, False, True]
     assert np.all(got[~valid] == 7.0)
     assert R.eps_comp(got[valid], y_ref[valid], "fp32") <= 2e-4
 
