@@ -215,9 +215,12 @@ cq_status cq_gemm_a8_carriers(const cq_weight *w, const int8_t *carriers, const 
  * caller, y[r] = x[route_token[r]] W_e^T with W_e = expert route_expert[r]
  * of the bank, in the model-dtype arithmetic of cq_gemm_model_dtype (FP32
  * products and accumulation).  Outputs are route-major; routing weights and
- * expert choice stay with the caller.  Routes are grouped by expert on the
- * device (no host synchronisation), and every decoded weight tile serves all
- * routes of its expert.
+ * expert choice stay with the caller.  No host synchronisation: with at
+ * most one route per expert on average (routes <= n_experts, the decode
+ * case) every route streams its expert's weights through the single-row
+ * kernel; otherwise routes are grouped by expert on the device and every
+ * decoded weight tile serves all routes of its expert (Sec. 5.5's
+ * compaction and grouping).
  *   bank          n_experts experts of equal shape stacked along the rows:
  *                 bank->n is the row count of ONE expert, and codes, scale, a
  *                 and b hold n_experts * bank->n rows (expert e first at row
@@ -228,7 +231,8 @@ cq_status cq_gemm_a8_carriers(const cq_weight *w, const int8_t *carriers, const 
  *                 outside [0, n_experts) are dropped: their rows of y are not
  *                 written.
  *   workspace     device int32 [n_experts + 1 + routes], caller-owned scratch
- *                 (expert offsets and the grouped route order).
+ *                 (expert offsets and the grouped route order; not touched
+ *                 in the streaming case).
  *   y             device [routes, bank->n] in y_dtype: x_dtype or CQ_FP32.
  * Deterministic: a route's output does not depend on the other routes.
  */
