@@ -100,24 +100,28 @@ def graph_timed(torch, fn, count, reps=3):
     return start.elapsed_time(stop) / (reps * count)
 
 
-def cpu_baseline(layers_np, bits, group, budget_s=20.0):
+def cpu_baseline(layers_np, bits, group, budget_s=20.0, gpu_out=None):
     """Time the oracle (unpack, decode to fp64, fp64 product) on a bounded row
-    sample of the decode layers; scaled to effective GB/s."""
+    sample of the decode layers; scaled to effective GB/s.  With gpu_out (per
+    layer: the step's model-dtype output, carriers and d_x), the same sample
+    also checks the timed step against the oracle, outside the timing."""
     from oracle import format as F
     from oracle import ref as R
     from threadpoolctl import threadpool_info, threadpool_limits
     threads = os.cpu_count() or 1
     with threadpool_limits(threads):
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-        return _cpu_baseline_run(layers_np, bits, group, budget_s, blas_threads)
+        return _cpu_baseline_run(layers_np, bits, group, budget_s, blas_threads, gpu_out)
 
 
-def _cpu_baseline_run(layers_np, bits, group, budget_s, blas_threads):
+def _cpu_baseline_run(layers_np, bits, group, budget_s, blas_threads, gpu_out):
+    from oracle import a8 as A8
     from oracle import format as F
     from oracle import ref as R
     frac = 1.0 / 2
     done_bytes, spent, rows_done = 0.0, 0.0, 0
-    for (name, k, n, codes, s, a, b, x_vals) in layers_np:
+    parity = {"model_dtype_eps_comp_max": 0.0, "rows_checked": 0, "a8_x8_dx_bitexact": True}
+    for li, (name, k, n, codes, s, a, b, x_vals) in enumerate(layers_np):
         rows = max(1, int(n * frac))
         t0 = time.perf_counter()
         packed = F.pack(codes[:rows], bits)
@@ -127,12 +131,24 @@ def _cpu_baseline_run(layers_np, bits, group, budget_s, blas_threads):
         done_bytes += a16_bytes(1, rows, k, bits, group)
         rows_done += rows
         assert y.shape == (1, rows)
+        if gpu_out is not None:
+            y_gpu, x8_gpu, dx_gpu = gpu_out[li]
+            e = R.eps_comp(y_gpu[:, :rows], y, "bf16")
+            parity["model_dtype_eps_comp_max"] = max(parity["model_dtype_eps_comp_max"], float(e))
+            parity["rows_checked"] += rows
+            x8_ref, d_ref = A8.quantize_act(x_vals)
+            parity["a8_x8_dx_bitexact"] &= bool(np.array_equal(x8_gpu, x8_ref) and
+                                                np.array_equal(dx_gpu, d_ref.astype(np.float32)))
         if spent > budget_s:
             break
     return {"value": done_bytes / spent / 1e9, "unit": "GB/s", "cores": int(blas_threads), "kind": "oracle",
             "sample": f"oracle unpack+decode(fp64)+product on {rows_done} weight rows "
                       f"(first half of each decode layer, M=1), {spent:.1f} s; elementwise numpy on 1 thread, "
-                      f"product on {blas_threads} BLAS threads"}
+                      f"product on {blas_threads} BLAS threads",
+            "parity": None if gpu_out is None else
+            dict(parity, bar="eps_comp <= 2e-3 (bf16 output) on the sampled rows of the timed step's outputs; "
+                             "carriers and d_x bit for bit", ok=parity["model_dtype_eps_comp_max"] <= 2e-3 and
+                 parity["a8_x8_dx_bitexact"])}
 
 
 def routed_sweep(torch, cq, bits=4, group=128, token_counts=(1, 4, 16, 64)):
@@ -498,7 +514,9 @@ def main():
         result["routed_sweep"] = routed_sweep(torch, cq)
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
-        result["cpu_baseline"] = cpu_baseline(layers_np, bits, group)
+        gpu_out = [(y16s[li].float().cpu().numpy().astype(np.float64), x8s[li].cpu().numpy(), dxs[li].cpu().numpy())
+                   for li in range(nl)]
+        result["cpu_baseline"] = cpu_baseline(layers_np, bits, group, gpu_out=gpu_out)
     print(json.dumps(result), flush=True)
 
 
