@@ -1,7 +1,8 @@
 // Dynamic-A8 narrow-row GEMV (Sec. 5.4) for m <= 16 rows of INT8 carriers.
 //
 // Each weight maps to its INT8 carrier r(k) = sign(k) RNE(127 q(|k|/M)),
-// computed exactly (eq. carrier, Appendix A item 7); a packed 4 x int8 dot
+// computed exactly (eq. carrier, Appendix A item 7: an FP32 estimate, and the
+// exact evaluation when the estimate lies near a tie); a packed 4 x int8 dot
 // product accumulates exact INT32 partials over 32-code units, which are
 // K-tile partials of the group partial P_g (Sec. 5.4 allows smaller K-tile
 // partials); each is converted to FP32 and multiplied by s_g, and the row
@@ -12,6 +13,7 @@
 // (held by adjacent lanes) are summed exactly with lane shuffles first.
 #include "cq_device.h"
 #include "cq_internal.h"
+#include "a8_carriers.h"
 
 namespace cq {
 
@@ -49,11 +51,13 @@ __global__ void __launch_bounds__(256) gemv_a8_generic(
                 for (int i = 0; i < B; ++i) w[i] = wrow[u * B + i];
                 gidx = row * ng + u / upg;
                 s = scale[gidx];
-                double a = 1.0, b = 0.0;
+                float a = 1.f, b = 0.f;
                 if (B > 2 && !ctab) {
-                    a = double(f16_to_f32(a16[gidx]));
-                    b = double(f16_to_f32(b16[gidx]));
+                    a = f16_to_f32(a16[gidx]);
+                    b = f16_to_f32(b16[gidx]);
                 }
+                const float c3 = 1.f - a - b;
+                const float margin = carrier_margin(a, b, c3);
 #pragma unroll
                 for (int i = 0; i < 32; ++i) {
                     const int code = unit_code<B>(w, i);
@@ -64,7 +68,9 @@ __global__ void __launch_bounds__(256) gemv_a8_generic(
                         const int mag = code < 0 ? -code : code;
                         int c;
                         if constexpr (B == 2) c = mag ? 127 : 0;
-                        else c = ctab ? int(ctab[gidx * (M + 1) + mag]) : exact_carrier(mag, M, a, b);
+                        else if (ctab) c = int(ctab[gidx * (M + 1) + mag]);
+                        // FP32 estimate of 127 q, exact fallback near a tie
+                        else c = int(carrier_u8<M>(mag, float(mag) / float(M), a, b, c3, margin));
                         c = c > 127 ? 127 : (c < -127 ? -127 : c);
                         r = code < 0 ? -c : c;
                     }
