@@ -17,16 +17,16 @@
 //
 // Decode.  Every lane reads one entry per weight of a table of the 2^B signed
 // normalised levels (0 for the reserved pattern) in its own LDS column, at
-// byte (field << 8) + lane * 4 + slot base, which is free of bank conflicts.
-// For B <= 4 every lane also writes its whole column: W4 at G = 128 evaluates
-// two magnitudes per lane and gathers the group's eight through DPP, other
-// widths evaluate all of them; W1/W2 tables are constant and written once.
-// (Writing one value into the columns of all lanes of a group puts those
-// lanes' stores of different fields on the same four banks: B = 5 still does
-// that, with 128-bit stores.)  For W4 the address is assembled by one byte
-// permute per weight, and the reads are issued 16 weights ahead of the
-// products that consume them.  B >= 6 evaluates the cubic in registers
-// instead of keeping a 64..256-entry table.
+// byte (field << 8) + lane * 4 + slot base, which is free of bank conflicts,
+// and writes that whole column itself (writing one value into the columns of
+// all lanes of a group would put those lanes' stores of different fields on
+// the same four banks).  W4/W5 at G = 128 evaluate a quarter of the
+// magnitudes per lane and gather the group's others through DPP, other
+// widths and groups evaluate all of them; W1/W2 tables are constant and
+// written once.  For W4 the address is assembled by one byte permute per
+// weight, and the reads are issued 16 weights ahead of the products that
+// consume them.  B >= 6 evaluates the cubic in registers instead of keeping a
+// 64..256-entry table.
 #include "cq_device.h"
 #include "cq_internal.h"
 #include "stream_common.h"
@@ -38,13 +38,8 @@ namespace cq {
 namespace {
 
 typedef __attribute__((address_space(3))) float lds_f;
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) f32x4_t lds_f4;
 
 __device__ __forceinline__ float lds_ld(uint32_t a) { return *reinterpret_cast<const lds_f *>(uintptr_t(a)); }
-__device__ __forceinline__ void lds_st4(uint32_t a, float v) {
-    *reinterpret_cast<lds_f4 *>(uintptr_t(a)) = f32x4_t{v, v, v, v};
-}
 __device__ __forceinline__ void lds_st(uint32_t a, float v) { *reinterpret_cast<lds_f *>(uintptr_t(a)) = v; }
 
 __device__ __forceinline__ void wave_lds_fence() {
@@ -72,9 +67,9 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
     constexpr int M = max_code(B);
     constexpr bool LUT = (B <= 5);
     constexpr int NT = LUT ? (1 << B) : 1;
-    // B <= 4: every lane owns a full column of the table (no replicated stores,
-    // whose lanes of one group all hit the same four banks)
-    constexpr bool OWN = B <= 4;
+    // every lane owns a full column of the table (no replicated stores, whose
+    // lanes of one group all hit the same four banks)
+    constexpr bool OWN = LUT;
     // LDS (dynamic, starting at address 0): one NT x 256-byte table per wave,
     // then the cross-wave partial sums.  The W4 address build relies on bits
     // 8..15 of the table base being zero.
@@ -100,8 +95,6 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
     const uint32_t tbase = uint32_t(uintptr_t((lds_f *)tab));
     // one table per (wave, row of the tile): slot index wave * RW + r
     const uint32_t col = tbase + uint32_t(wave * RW) * (NT * 256u) + uint32_t(lane) * 4u;
-    // first column of this lane's group inside the wave (the group's UPG lanes are adjacent)
-    const uint32_t gcol = tbase + uint32_t(wave * RW) * (NT * 256u) + uint32_t(lane - lane % UPG) * 4u;
     const uint32_t wtag = uint32_t(wave * RW) * 0x10101010u;
 
     // magnitudes this lane evaluates for its group's table, and their t = i/M
@@ -210,17 +203,18 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                 // are constant, all written once before the loop)
                 if constexpr (B >= 3) {
                     float qa[M + 1];
-                    if constexpr (B == 4 && UPG == 4) {
-                        // the group is one DPP quad: lane j evaluates magnitudes j
-                        // and j + 4, and every lane gathers all eight
-                        float qv[2];
+                    if constexpr (B >= 4 && UPG == 4) {
+                        // the group is one DPP quad: lane j evaluates magnitudes j,
+                        // j + 4, ..., and every lane gathers all of them
+                        constexpr int NQ = (M + 1) / 4;
+                        float qv[NQ];
 #pragma unroll
-                        for (int t = 0; t < 2; ++t) {
+                        for (int t = 0; t < NQ; ++t) {
                             const float q = tq[t] * __builtin_fmaf(tq[t], __builtin_fmaf(tq[t], cc, b), a);
                             qv[t] = mag[t] == M ? 1.f : q;
                         }
 #pragma unroll
-                        for (int t = 0; t < 2; ++t) {
+                        for (int t = 0; t < NQ; ++t) {
                             const int u = int(__float_as_uint(qv[t]));
                             qa[4 * t + 0] = __uint_as_float(uint32_t(__builtin_amdgcn_mov_dpp(u, 0x00, 0xf, 0xf, true)));
                             qa[4 * t + 1] = __uint_as_float(uint32_t(__builtin_amdgcn_mov_dpp(u, 0x55, 0xf, 0xf, true)));
@@ -240,40 +234,6 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                     for (int i = 1; i <= M; ++i) {
                         lds_st(own + uint32_t(i) * 256u, qa[i]);
                         lds_st(own + uint32_t(NT - i) * 256u, -qa[i]);
-                    }
-                }
-            } else if constexpr (LUT) {
-                // B = 5: lane j of a group evaluates magnitudes j, j + UPG, ... (their
-                // t = i/M are per-lane constants) and stores +q at field i and -q at
-                // field NT - i into the table columns of all UPG lanes of the group;
-                // the lane holding magnitude 0 also clears the reserved field NT/2.
-                const uint32_t gslot = gcol + uint32_t(r) * (NT * 256u);
-#pragma unroll
-                for (int t = 0; t < MPL; ++t) {
-                    if (mag[t] <= M) {
-                        float q;
-                        if constexpr (B == 1) {
-                            q = 1.f;
-                        } else {
-                            q = tq[t] * __builtin_fmaf(tq[t], __builtin_fmaf(tq[t], cc, b), a);
-                            q = mag[t] == M ? 1.f : q;
-                        }
-                        const uint32_t up = gslot + uint32_t(B == 1 ? 1 : mag[t]) * 256u;
-                        const uint32_t um = gslot + uint32_t(mag[t] == 0 ? NT / 2 : (B == 1 ? 0 : NT - mag[t])) * 256u;
-                        const float qm = mag[t] == 0 ? 0.f : -q;
-                        if constexpr (UPG % 4 == 0) {
-#pragma unroll
-                            for (int c4 = 0; c4 < UPG; c4 += 4) {
-                                lds_st4(up + c4 * 4u, q);
-                                lds_st4(um + c4 * 4u, qm);
-                            }
-                        } else {
-#pragma unroll
-                            for (int c1 = 0; c1 < UPG; ++c1) {
-                                lds_st(up + c1 * 4u, q);
-                                lds_st(um + c1 * 4u, qm);
-                            }
-                        }
                     }
                 }
             }
