@@ -227,6 +227,35 @@ def rows_sweep(torch, cq, bits=4, group=128, k=8192, n=28672, ms=(1, 2, 8, 32, 1
     return {"shape": {"k": k, "n": n, "bits": bits, "group": group}, "rows": out, "a8_faster_from_m": cross}
 
 
+def width_group_sweep(torch, cq, k=8192, n=8192, widths=(1, 2, 3, 4, 6, 8), groups=(32, 64, 128, 256)):
+    """Single-row GEMV on K = N = 8192 for every width and group of the sweep
+    configuration, both paths, weights rotated over 512 MB; effective GB/s
+    against the B + 64/G bits-per-weight footprint."""
+    x = torch.randn(1, k, device="cuda").to(torch.bfloat16)
+    x8, dx = cq.cq_quantize_act_a8(x)
+    y = torch.empty((1, n), dtype=torch.bfloat16, device="cuda")
+    out = []
+    for bits in widths:
+        for g in groups:
+            w0 = make_weight(cq, 300 + bits, n, k, bits, g)
+            ws = [w0] + [w0.clone() for _ in range(max(1, math.ceil((512 << 20) / w0.nbytes)))]
+            rec = {"bits": bits, "group": g}
+            for path, fn in (("model_dtype", lambda i: cq.cq_gemm_model_dtype(ws[i % len(ws)], x, out=y)),
+                             ("a8", lambda i: cq.cq_gemm_a8(ws[i % len(ws)], x8, dx, out=y))):
+                for i in range(len(ws)):
+                    fn(i)
+                torch.cuda.synchronize()
+                t = timed(torch, fn, len(ws) * 4)
+                rec[path + "_us"] = round(t * 1e3, 2)
+                rec[path + "_gbs"] = round(a16_bytes(1, n, k, bits, g) / t / 1e6 if path == "model_dtype"
+                                           else a8_bytes(1, n, k, bits, g) / t / 1e6, 1)
+            out.append(rec)
+            del ws, w0
+    log("[sweep] widths: " + ", ".join(f"W{r['bits']}G{r['group']} {r['model_dtype_gbs']:.0f}/{r['a8_gbs']:.0f}"
+                                        for r in out))
+    return {"shape": {"k": k, "n": n, "m": 1}, "rows": out}
+
+
 def selection_sweep(torch, cq, bits=4, group=128, k=8192, n=28672, ms=(1, 2, 8, 32, 128, 512, 2048, 8192)):
     """Measured kernel selection on the crossover shape: every admissible family
     of both paths timed at each row count; the table is reported, not kept."""
@@ -510,6 +539,7 @@ def main():
             if ceil.get("int8_gemm_tops"):
                 r["a8_frac_of_measured_int8_gemm"] = r["a8_tops"] / ceil["int8_gemm_tops"]
         result["selection"] = selection_sweep(torch, cq)
+        result["width_group_sweep"] = width_group_sweep(torch, cq)
         log("[bench] routed sweep")
         result["routed_sweep"] = routed_sweep(torch, cq)
     if not args.no_cpu_baseline:
