@@ -199,8 +199,9 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
             ga_r[r] = cc * (1.0f / float(M * M * M));
             if constexpr (OWN) {
                 // every lane writes its own column: +q at field i and -q at field
-                // NT - i for i = 1 .. M (fields 0 and NT/2 hold 0, and W1/W2 tables
-                // are constant, all written once before the loop)
+                // NT - i for i = 1 .. M - 1 (fields 0 and NT/2 hold 0 and fields M
+                // and NT - M hold +1 and -1, and W1/W2 tables are constant, all
+                // written once before the loop)
                 if constexpr (B >= 3) {
                     float qa[M + 1];
                     if constexpr (B >= 4 && UPG == 4) {
@@ -210,8 +211,7 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                         float qv[NQ];
 #pragma unroll
                         for (int t = 0; t < NQ; ++t) {
-                            const float q = tq[t] * __builtin_fmaf(tq[t], __builtin_fmaf(tq[t], cc, b), a);
-                            qv[t] = mag[t] == M ? 1.f : q;
+                            qv[t] = tq[t] * __builtin_fmaf(tq[t], __builtin_fmaf(tq[t], cc, b), a);
                         }
 #pragma unroll
                         for (int t = 0; t < NQ; ++t) {
@@ -227,11 +227,10 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                             const float t = float(i) * (1.0f / float(M));
                             qa[i] = t * __builtin_fmaf(t, __builtin_fmaf(t, cc, b), a);
                         }
-                        qa[M] = 1.f;
                     }
                     const uint32_t own = col + uint32_t(r) * (NT * 256u);
 #pragma unroll
-                    for (int i = 1; i <= M; ++i) {
+                    for (int i = 1; i < M; ++i) {
                         lds_st(own + uint32_t(i) * 256u, qa[i]);
                         lds_st(own + uint32_t(NT - i) * 256u, -qa[i]);
                     }
@@ -396,6 +395,8 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
             } else {
                 lds_st(own, 0.f);
                 lds_st(own + uint32_t(NT / 2) * 256u, 0.f);
+                lds_st(own + uint32_t(M) * 256u, 1.f);
+                lds_st(own + uint32_t(NT - M) * 256u, -1.f);
             }
         }
         wave_lds_fence();
