@@ -328,9 +328,10 @@ typedef struct {
  * on the A8 path, bits outside 1..8, a group that is not a multiple of 32 in
  * 32..512, n or k < 1, m_lo < 1 or m_hi < m_lo, a bad x_dtype, reserved != 0)
  * or if two entries of the same path, shape and dtype overlap in m; count
- * above 65536 is CQ_ERR_ARG too.  The first matching entry wins; when its
- * family cannot take the call (cq_family_supported is 0) the built-in rules
- * decide.  The table does not apply to a cq_gemm_a8 call that asks for the
+ * above 65536 is CQ_ERR_ARG too.  With overlaps rejected, at most one entry
+ * matches a call (found by binary search over the shape, so large tables cost
+ * no more per call than small ones); when its family cannot take the call
+ * (cq_family_supported is 0) the built-in rules decide.  The table does not apply to a cq_gemm_a8 call that asks for the
  * partials dump, nor to cq_gemm_a8_fused, cq_gemm_a8_carriers or the routed
  * product.  Safe to call while other threads launch products; a call already
  * past its dispatch is not affected.

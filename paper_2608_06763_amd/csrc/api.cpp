@@ -298,11 +298,9 @@ cq_status cq_gemm_a8_family(const cq_weight *w, const int8_t *x8, const float *d
 cq_status cq_select_set(const cq_select_entry *entries, int64_t count) {
     if (count < 0 || count > 65536 || (count > 0 && !entries)) return CQ_ERR_ARG;
     std::vector<cq_select_entry> t(entries, entries + count);
-    for (int64_t i = 0; i < count; ++i) {
+    for (int64_t i = 0; i < count; ++i)
         if (!cq::select_entry_valid(t[i])) return CQ_ERR_ARG;
-        for (int64_t j = 0; j < i; ++j)
-            if (cq::select_entries_overlap(t[i], t[j])) return CQ_ERR_ARG;
-    }
+    if (!cq::select_sort_disjoint(t)) return CQ_ERR_ARG;
     cq::select_install(std::move(t));
     return CQ_OK;
 }

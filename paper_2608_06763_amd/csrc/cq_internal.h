@@ -101,7 +101,8 @@ hipError_t run_family_a16(int family, const cq_weight &w, const void *x, int x_d
 hipError_t run_family_a8(int family, const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
                          int y_dt, int32_t *partials, hipStream_t stream);
 bool select_entry_valid(const cq_select_entry &e);
-bool select_entries_overlap(const cq_select_entry &a, const cq_select_entry &b);
+// sort the entries into table order; false if two of them can match one call
+bool select_sort_disjoint(std::vector<cq_select_entry> &entries);
 // replace the table (empty clears it)
 void select_install(std::vector<cq_select_entry> entries);
 

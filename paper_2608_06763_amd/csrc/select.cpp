@@ -3,6 +3,7 @@
 // memory, so the choice for a call can be queried without a GPU.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <memory>
 #include <mutex>
@@ -91,7 +92,24 @@ hipError_t run_family_a8(int family, const cq_weight &w, const int8_t *x8, const
 
 namespace {
 
+// The installed table is sorted by (path, bits, group, n, k, m_lo), so a lookup
+// is a binary search for the shape followed by a scan of that shape's few
+// row ranges.
 using Table = std::vector<cq_select_entry>;
+
+bool shape_less(const cq_select_entry &a, const cq_select_entry &b) {
+    if (a.path != b.path) return a.path < b.path;
+    if (a.bits != b.bits) return a.bits < b.bits;
+    if (a.group != b.group) return a.group < b.group;
+    if (a.n != b.n) return a.n < b.n;
+    return a.k < b.k;
+}
+
+bool entry_less(const cq_select_entry &a, const cq_select_entry &b) {
+    if (shape_less(a, b)) return true;
+    if (shape_less(b, a)) return false;
+    return a.m_lo < b.m_lo;
+}
 
 std::mutex g_table_mutex;               // serialises writers
 std::shared_ptr<const Table> g_table;   // read with std::atomic_load
@@ -108,8 +126,15 @@ int table_family(int path, const cq_weight &w, int x_dt, int64_t m) {
     if (!g_table_nonempty.load(std::memory_order_acquire)) return CQ_FAMILY_AUTO;
     const std::shared_ptr<const Table> t = std::atomic_load(&g_table);
     if (!t) return CQ_FAMILY_AUTO;
-    for (const cq_select_entry &e : *t)
-        if (entry_matches(e, path, w, x_dt, m)) return e.family;
+    cq_select_entry probe{};
+    probe.path = path;
+    probe.bits = w.bits;
+    probe.group = w.group;
+    probe.n = w.n;
+    probe.k = w.k;
+    const auto range = std::equal_range(t->begin(), t->end(), probe, shape_less);
+    for (auto it = range.first; it != range.second; ++it)
+        if (entry_matches(*it, path, w, x_dt, m)) return it->family;
     return CQ_FAMILY_AUTO;
 }
 
@@ -125,10 +150,28 @@ bool select_entry_valid(const cq_select_entry &e) {
     return e.reserved == 0;
 }
 
-bool select_entries_overlap(const cq_select_entry &a, const cq_select_entry &b) {
-    const bool dtypes_meet = a.x_dtype < 0 || b.x_dtype < 0 || a.x_dtype == b.x_dtype;
-    return a.path == b.path && a.bits == b.bits && a.group == b.group && a.n == b.n && a.k == b.k && dtypes_meet &&
-           a.m_lo <= b.m_hi && b.m_lo <= a.m_hi;
+bool select_sort_disjoint(std::vector<cq_select_entry> &entries) {
+    std::sort(entries.begin(), entries.end(), entry_less);
+    // Within one shape, the entries that a model-dtype call with activations
+    // of dtype d can match (x_dtype d or any) must have disjoint row ranges;
+    // A8 entries all carry x_dtype -1, so one pass covers them.
+    for (size_t lo = 0; lo < entries.size();) {
+        size_t hi = lo + 1;
+        while (hi < entries.size() && !shape_less(entries[lo], entries[hi])) ++hi;
+        for (int d = 0; d <= 1; ++d) {
+            bool any = false;
+            int64_t reach = 0;
+            for (size_t i = lo; i < hi; ++i) {
+                const cq_select_entry &e = entries[i];
+                if (e.x_dtype >= 0 && e.x_dtype != d) continue;
+                if (any && e.m_lo <= reach) return false;
+                reach = any ? std::max(reach, e.m_hi) : e.m_hi;
+                any = true;
+            }
+        }
+        lo = hi;
+    }
+    return true;
 }
 
 void select_install(std::vector<cq_select_entry> entries) {

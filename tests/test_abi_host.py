@@ -6,6 +6,7 @@ every invalid input the format forbids; device entry points must reject bad
 arguments on the host before touching a device.
 """
 import ctypes
+import time
 import os
 import re
 
@@ -357,6 +358,43 @@ def test_table_rejects_overlaps_and_reserved(clean_table):
     assert L.cq_select_set(None, 1) == 1
     assert L.cq_select_set(arr, -1) == 1
     assert L.cq_select_set(arr, 65537) == 1
+
+
+def test_table_large_and_shuffled(clean_table):
+    # 4096 shapes x 4 row ranges given in shuffled order: installed in one
+    # sort, each call finds its own shape's entry
+    rng = np.random.default_rng(7)
+    fams = ["gemv_generic", "gemm_tiled", "gemm_mfma", "gemv_narrow"]
+    ranges = [(1, 4), (5, 16), (17, 256), (257, 1 << 40)]
+    entries = [_entry(n=64 * (i + 1), m_lo=lo, m_hi=hi, family=fams[(i + j) % 4])
+               for i in range(4096) for j, (lo, hi) in enumerate(ranges)]
+    order = rng.permutation(len(entries))
+    t0 = time.perf_counter()
+    cq.cq_select_set([entries[i] for i in order])
+    assert time.perf_counter() - t0 < 5.0
+    for i in (0, 1, 777, 4095):
+        d = _fake(4, 128, 64 * (i + 1), 4096)
+        for j, (lo, hi) in enumerate(ranges):
+            want = fams[(i + j) % 4]
+            got = cq.cq_select_query(cq.CQ_PATH_MODEL_DTYPE, d, lo)
+            if cq.cq_family_supported(cq.CQ_PATH_MODEL_DTYPE, want, d, lo):
+                assert got == want, (i, j)
+    # one overlapping pair anywhere in a large table is found
+    bad = [entries[i] for i in order] + [_entry(n=64 * 3000, m_lo=16, m_hi=16, family="gemm_tiled")]
+    with pytest.raises(cq.CQError):
+        cq.cq_select_set(bad)
+
+
+def test_table_dtype_classes_in_sorted_order(clean_table):
+    # bf16-only and fp16-only entries never meet; a wildcard meets both
+    cq.cq_select_set([_entry(x_dtype=cq.CQ_BF16, m_lo=1, m_hi=4), _entry(x_dtype=-1, m_lo=5, m_hi=8),
+                      _entry(x_dtype=cq.CQ_FP16, m_lo=1, m_hi=4)])
+    cq.cq_select_set([_entry(x_dtype=cq.CQ_BF16, m_lo=1, m_hi=4), _entry(x_dtype=cq.CQ_FP16, m_lo=3, m_hi=6)])
+    for pair in ([_entry(x_dtype=-1, m_lo=1, m_hi=4), _entry(x_dtype=cq.CQ_FP16, m_lo=4, m_hi=6)],
+                 [_entry(x_dtype=cq.CQ_BF16, m_lo=6, m_hi=9), _entry(x_dtype=cq.CQ_FP16, m_lo=1, m_hi=2),
+                  _entry(x_dtype=-1, m_lo=3, m_hi=6)]):
+        with pytest.raises(cq.CQError):
+            cq.cq_select_set(pair)
 
 
 def test_forced_family_errors_need_no_gpu():
