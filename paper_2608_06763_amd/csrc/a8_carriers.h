@@ -33,7 +33,11 @@ __device__ __forceinline__ uint32_t carrier_u8(int i, float t, float a, float b,
     const float f = 127.0f * (t * __builtin_fmaf(t, __builtin_fmaf(t, c, b), a));
     float r = __builtin_rintf(f);
     if (__builtin_expect(__builtin_fabsf(f - r) > 0.5f - margin, 0)) {
-        r = float(exact_carrier(i, M, double(a), double(b)));
+        // the exact path's double arithmetic stays inside this rarely taken
+        // branch (the compiler would otherwise hoist it for every carrier)
+        float ea = a, eb = b;
+        __asm__ volatile("" : "+v"(ea), "+v"(eb));
+        r = float(exact_carrier(i, M, double(ea), double(eb)));
     }
     r = r < 0.f ? 0.f : (r > 127.f ? 127.f : r);
     return uint32_t(int(r));
