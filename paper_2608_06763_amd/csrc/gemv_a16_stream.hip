@@ -153,8 +153,8 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
         const int u = c * 64 + lane;
         const bool uok = ok && u < units;
         const uint32_t vc = uok ? uint32_t(u) * (4 * B) : kOobOffset;
-        const uint32_t vm = uok ? uint32_t(u / UPG) * 4u : kOobOffset;
-        const uint32_t vh = uok ? uint32_t(u / UPG) * 2u : kOobOffset;
+        const uint32_t vm = uok ? uint32_t(u) / UPG * 4u : kOobOffset;
+        const uint32_t vh = uok ? uint32_t(u) / UPG * 2u : kOobOffset;
         const uint32_t xo = uok ? uint32_t(u) * 64u : kOobOffset;
 #pragma unroll
         for (int r = 0; r < RW; ++r) {

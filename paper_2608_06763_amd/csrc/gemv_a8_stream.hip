@@ -152,7 +152,7 @@ __global__ void __launch_bounds__(FX >= 0 ? 64 * kMaxFusedWaves : 256) gemv_a8_s
         for (int r = 0; r < RW; ++r) {
             const int row = t * RW + r;
             const bool ok = (u < units) && (row < n);
-            const uint32_t gi = uint32_t(row) * ng + uint32_t(u / UPG);
+            const uint32_t gi = uint32_t(row) * ng + uint32_t(u) / UPG;
             load_words<B>(rc, ok ? uint32_t(row) * row_bytes + uint32_t(u) * (4 * B) : kOobOffset, wn[r]);
             sn[r] = load_f32(rs, ok ? gi * 4u : kOobOffset);
             if constexpr (B == 4 || B == 3) {
