@@ -7,6 +7,13 @@ float64, A8 carriers from exact rationals) and the sampled outputs must meet
 the same bars as the small parity tests: eps_comp <= 2e-3 for bf16 outputs,
 1e-5 for FP32 outputs of the FP32-product paths, and bit-exact INT32 group
 partials where they are dumped.
+
+Weights.  The checked rows carry the configuration's own law, quantized by
+the oracle fit: exactly the sampled weight rows are drawn (row-seeded
+generators) and fitted, and spliced at their indices into a seeded packed
+stand-in that fills the rest of the full-size matrix.  Rows of y depend only
+on their own weight row, so the unchecked rows only set the shape, the
+launch configuration and the memory traffic.
 """
 import functools
 
@@ -16,8 +23,9 @@ import pytest
 from oracle import a8 as A8
 from oracle import ref as R
 from tests._cases import say
-from workloads import (LLAMA8B_LAYERS, PREFILL70B_SHAPES, bf16_bits_to_f32, crossover_act, gemv_4k, llama8b_act,
-                       prefill70b_act, sweep_act, synthetic_representation)
+from workloads import (LLAMA8B_LAYERS, PREFILL70B_SHAPES, bf16_bits_to_f32, crossover_act, crossover_weight, gemv_4k,
+                       llama8b_act, llama8b_weight, prefill70b_act, prefill70b_weight, sweep_act, sweep_weight,
+                       synthetic_representation)
 
 pytestmark = pytest.mark.gpu
 
@@ -42,15 +50,41 @@ def _dev_x(torch, bits):
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
 
 
-@functools.lru_cache(maxsize=2)
-def _synthetic(seed, n, k, bits, group):
-    """Seeded packed representation, uploaded once per module run."""
-    codes, s, a, b = synthetic_representation(seed, n, k, bits, group)
-    return codes, s, a, b, _cq().CQWeight.from_codes(codes, s, a, b, bits, group)
-
-
 def _sample(seed, count, total):
     return np.sort(np.random.default_rng(seed).choice(total, size=min(count, total), replace=False))
+
+
+# the configurations' weight laws, as functions of the sampled rows
+LAWS = {
+    "llama8b": lambda layer, k, n: (lambda rows: llama8b_weight(layer, k, n, rows)),
+    "sweep": lambda k, n: (lambda rows: sweep_weight(k, n, rows)),
+    "crossover": lambda k, n: (lambda rows: crossover_weight(k, n, rows)),
+    "prefill70b": lambda k, n, off: (lambda rows: prefill70b_weight(k, n, off, rows)),
+}
+
+
+@functools.lru_cache(maxsize=None)
+def _fitted_rows(law_key, rows_key, bits, group):
+    """Oracle fit of the sampled rows of a configuration's weights (cached)."""
+    from oracle import fit as FIT
+    law, args = law_key[0], law_key[1:]
+    w = LAWS[law](*args)(np.asarray(rows_key))
+    return FIT.fit(w, bits, group)
+
+
+def _spliced_np(seed, n, k, bits, group, law_key, rows):
+    """Seeded stand-in [N, K] with the oracle-fitted rows of the law at `rows`."""
+    codes, s, a, b = synthetic_representation(seed, n, k, bits, group)
+    fr = _fitted_rows(law_key, tuple(int(r) for r in rows), bits, group)
+    codes[rows], s[rows], a[rows], b[rows] = fr.codes, fr.scale, fr.a_bits, fr.b_bits
+    return codes, s, a, b
+
+
+@functools.lru_cache(maxsize=2)
+def _spliced(seed, n, k, bits, group, law_key, rows_key):
+    """The spliced matrix, packed by the library and uploaded once per module run."""
+    codes, s, a, b = _spliced_np(seed, n, k, bits, group, law_key, np.asarray(rows_key))
+    return codes, s, a, b, _cq().CQWeight.from_codes(codes, s, a, b, bits, group)
 
 
 def _ref_rows(xv, codes, s, a, b, bits, group, rows):
@@ -63,13 +97,24 @@ def _ref_a8_rows(x8, dx, codes, s, a, b, bits, group, rows):
     return y, p
 
 
+def _check_rounded_bound(got, y_ref, xs, codes, s, a, b, bits, group, rows):
+    """|y - y_ref| <= 2^-8 sum_j |x_j| |w_j| (one BF16 rounding per weight) plus
+    the FP32 accumulation, elementwise."""
+    from oracle import format as F
+    wabs = np.abs(F.decode(codes[rows], bits, group, s[rows], a[rows], b[rows]))
+    bound = 2.0 ** -8 * (np.abs(xs) @ wabs.T) * (1 + 2e-3) + 1e-6 * np.max(np.abs(y_ref))
+    assert np.all(np.abs(np.asarray(got, np.float64) - y_ref) <= bound)
+
+
 def _eps(got, ref, dtype):
     return R.eps_comp(np.asarray(got, np.float64), ref, dtype)
 
 
 def _check_both_paths(torch, w, xb, codes, s, a, b, bits, group, rows, tag, xrows=None):
     """Run both entry points at full size; compare sampled columns (and
-    sampled activation rows when xrows is given) with the oracle."""
+    sampled activation rows when xrows is given) with the oracle.  Where the
+    single-rounded matrix-core family can take the shape, it is held to the
+    same bar (its error is printed)."""
     cq = _cq()
     xs = bf16_bits_to_f32(xb if xrows is None else xb[xrows]).astype(np.float64)
     x = _dev_x(torch, xb)
@@ -78,6 +123,16 @@ def _check_both_paths(torch, w, xb, codes, s, a, b, bits, group, rows, tag, xrow
     y_ref = _ref_rows(xs, codes, s, a, b, bits, group, rows)
     got = y[:, rows] if xrows is None else y[xrows][:, rows]
     assert _eps(got, y_ref, "bf16") <= TOL
+    m = xb.shape[0]
+    if m > 16 and cq.cq_family_supported(cq.CQ_PATH_MODEL_DTYPE, "gemm_mfma_rounded", w, m):
+        # the single-rounded operand family: every weight rounded once to BF16
+        # (relative error <= 2^-8), products exact, FP32 accumulation; its
+        # FP32 output must lie within that rounding's own bound elementwise
+        say(tag, "model-dtype rounded operand")
+        yr = cq.cq_gemm_model_dtype_family(w, x, "gemm_mfma_rounded", y_dtype=torch.float32).cpu().numpy()
+        yr = yr[:, rows] if xrows is None else yr[xrows][:, rows]
+        say(tag, f"rounded operand eps_comp {_eps(yr, y_ref, 'fp32'):.3e}")
+        _check_rounded_bound(yr, y_ref, xs, codes, s, a, b, bits, group, rows)
     say(tag, "a8")
     x8, dx = cq.cq_quantize_act_a8(x)
     x8_ref, d_ref = A8.quantize_act(xs)
@@ -106,23 +161,26 @@ def test_fullsize_single_gemv_fitted(torch_dev):
 @pytest.mark.parametrize("m", [1, 4, 16])
 @pytest.mark.parametrize("layer", range(4))
 def test_fullsize_llama8b_decode_layers(torch_dev, layer, m):
-    # the benchmark's layers and weights (same seeds), 96 sampled output rows
+    # the benchmark's layer shapes and launches; 96 sampled output rows carry
+    # the layer's Laplace-with-outlier-channels weights, fitted by the oracle
     name, k, n = LLAMA8B_LAYERS[layer]
-    codes, s, a, b = synthetic_representation(2000 + layer, n, k, 4, 128)
-    w = _cq().CQWeight.from_codes(codes, s, a, b, 4, 128)
-    xb = llama8b_act(m, k, layer)
     rows = _sample(7 + layer, 96, n)
+    say(f"llama8b {name} fit of the sampled rows")
+    codes, s, a, b, w = _spliced(2000 + layer, n, k, 4, 128, ("llama8b", layer, k, n), tuple(rows.tolist()))
+    xb = llama8b_act(m, k, layer)
     _check_both_paths(torch_dev, w, xb, codes, s, a, b, 4, 128, rows, f"llama8b {name} m={m}")
 
 
 @pytest.mark.parametrize("m", [1, 2, 8, 32, 128, 512, 2048, 8192])
 def test_fullsize_crossover_shape(torch_dev, m):
     # K = 8192, N = 28672, W4 G128 at every row count of the crossover sweep;
-    # 48 sampled weight rows x (all or 24 sampled) activation rows
+    # 48 sampled weight rows (Student-t weights fitted by the oracle) x (all or
+    # 24 sampled) activation rows
     k, n = 8192, 28672
-    codes, s, a, b, w = _synthetic(4001, n, k, 4, 128)
-    xb = crossover_act(m, k)
     rows = _sample(11, 48, n)
+    say(f"crossover fit of the sampled rows")
+    codes, s, a, b, w = _spliced(4001, n, k, 4, 128, ("crossover", k, n), tuple(rows.tolist()))
+    xb = crossover_act(m, k)
     xrows = None if m <= 32 else _sample(12, 24, m)
     _check_both_paths(torch_dev, w, xb, codes, s, a, b, 4, 128, rows, f"crossover m={m}", xrows)
 
@@ -130,12 +188,14 @@ def test_fullsize_crossover_shape(torch_dev, m):
 @pytest.mark.parametrize("bits", [1, 2, 3, 4, 6, 8])
 @pytest.mark.parametrize("group", [32, 64, 128, 256])
 def test_fullsize_width_group_sweep(torch_dev, bits, group):
-    # M = 1, K = N = 8192 for every B x G of the sweep; 32 sampled rows
+    # M = 1, K = N = 8192 for every B x G of the sweep; 32 sampled rows of
+    # N(0, 0.015^2) weights fitted by the oracle at this B and G
     k = n = 8192
-    codes, s, a, b = synthetic_representation(5000 + 10 * bits + group // 32, n, k, bits, group)
-    w = _cq().CQWeight.from_codes(codes, s, a, b, bits, group)
-    xb = sweep_act(k)
     rows = _sample(13, 32, n)
+    say(f"sweep B={bits} G={group} fit of the sampled rows")
+    codes, s, a, b, w = _spliced(5000 + 10 * bits + group // 32, n, k, bits, group, ("sweep", k, n),
+                                 tuple(rows.tolist()))
+    xb = sweep_act(k)
     _check_both_paths(torch_dev, w, xb, codes, s, a, b, bits, group, rows, f"sweep B={bits} G={group}")
 
 
@@ -143,11 +203,14 @@ def test_fullsize_width_group_sweep(torch_dev, bits, group):
 @pytest.mark.parametrize("bits", [3, 4])
 @pytest.mark.parametrize("shape", range(3))
 def test_fullsize_prefill70b(torch_dev, shape, bits, m):
-    # 70B-class prefill GEMMs, W3 and W4 G128; 16 x 24 sampled outputs
+    # 70B-class prefill GEMMs, W3 and W4 G128; 16 x 24 sampled outputs, the
+    # 16 weight rows Laplace times their row multiplier, fitted by the oracle
     k, n = PREFILL70B_SHAPES[shape]
-    codes, s, a, b, w = _synthetic(6000 + 10 * shape + bits, n, k, bits, 128)
-    xb = prefill70b_act(m, k)
     rows = _sample(17, 16, n)
+    say(f"prefill70b {k}x{n} B={bits} fit of the sampled rows")
+    codes, s, a, b, w = _spliced(6000 + 10 * shape + bits, n, k, bits, 128, ("prefill70b", k, n, shape),
+                                 tuple(rows.tolist()))
+    xb = prefill70b_act(m, k)
     xrows = _sample(18, 24, m)
     _check_both_paths(torch_dev, w, xb, codes, s, a, b, bits, 128, rows, f"prefill70b {k}x{n} m={m} B={bits}",
                       xrows)
@@ -181,12 +244,12 @@ def test_fullsize_fused_a8_decode_layers(torch_dev, layer):
     # the benchmark's single-row fused A8 call on each decode layer: carriers
     # and d_x bit-exact, 96 sampled output rows against the A8 oracle
     name, k, n = LLAMA8B_LAYERS[layer]
-    codes, s, a, b = synthetic_representation(2000 + layer, n, k, 4, 128)
+    rows = _sample(31 + layer, 96, n)
+    say("fused a8", name, "fit of the sampled rows")
+    codes, s, a, b, w = _spliced(2000 + layer, n, k, 4, 128, ("llama8b", layer, k, n), tuple(rows.tolist()))
     cq = _cq()
-    w = cq.CQWeight.from_codes(codes, s, a, b, 4, 128)
     xb = llama8b_act(1, k, layer)
     xv = bf16_bits_to_f32(xb).astype(np.float64)
-    rows = _sample(31 + layer, 96, n)
     say("fused a8", name)
     y, x8, dx = cq.cq_gemm_a8_fused(w, _dev_x(torch_dev, xb), y_dtype=torch_dev.float32)
     x8_ref, d_ref = A8.quantize_act(xv)

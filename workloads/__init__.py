@@ -20,7 +20,10 @@ configurations:
     (8192, 10240)}; W ~ Laplace(0, 0.01) times a per-row factor log-uniform in
     [0.5, 2]; x ~ N(0,1).
 Seeds: for workload number c (1..5) tensor t uses 1000*c + t, except the first
-workload whose x uses seed 0 and W seed 1.
+workload whose x uses seed 0 and W seed 1.  The weights of the larger
+workloads are drawn row by row, each row from its own generator seeded by
+(tensor seed, row index), so that a sample of rows can be drawn (and fitted)
+without the whole matrix.
 """
 from __future__ import annotations
 
@@ -88,11 +91,32 @@ def gemv_4k():
     return x, w
 
 
-def llama8b_weight(layer: int, k: int, n: int) -> np.ndarray:
-    """Laplace(0, 0.014) weights [N, K], ceil(0.01 K) input channels x8."""
-    w = laplace(2000 + 2 * layer, (n, k), 0.014)
-    cols = rng(2001 + 2 * layer).choice(k, size=math.ceil(0.01 * k), replace=False)
-    w[:, cols] *= 8.0
+def row_rng(seed: int, row: int) -> np.random.Generator:
+    """Generator of one weight row: PCG64 seeded by the pair (tensor seed, row),
+    so that any subset of rows of a large matrix can be drawn on its own."""
+    return np.random.Generator(np.random.PCG64([seed, int(row)]))
+
+
+def _rows(rows, n: int) -> np.ndarray:
+    r = np.arange(n) if rows is None else np.asarray(rows, dtype=np.int64)
+    if r.size and (r.min() < 0 or r.max() >= n):
+        raise IndexError("row outside the matrix")
+    return r
+
+
+def llama8b_outlier_cols(layer: int, k: int) -> np.ndarray:
+    """The ceil(0.01 K) input channels of a decode layer scaled x8."""
+    return rng(2001 + 2 * layer).choice(k, size=math.ceil(0.01 * k), replace=False)
+
+
+def llama8b_weight(layer: int, k: int, n: int, rows=None) -> np.ndarray:
+    """Rows `rows` (default all) of the Laplace(0, 0.014) weights [N, K] of a
+    decode layer, with ceil(0.01 K) input channels x8."""
+    r = _rows(rows, n)
+    w = np.empty((r.size, k))
+    for i, row in enumerate(r):
+        w[i] = row_rng(2000 + 2 * layer, row).laplace(0.0, 0.014, k)
+    w[:, llama8b_outlier_cols(layer, k)] *= 8.0
     return to_f32(w)
 
 
@@ -103,16 +127,26 @@ def llama8b_act(m: int, k: int, seed_offset: int = 0) -> np.ndarray:
     return to_bf16_bits(x * u)
 
 
-def sweep_weight(k: int = 8192, n: int = 8192) -> np.ndarray:
-    return to_f32(normal(3001, (n, k), 0.015))
+def sweep_weight(k: int = 8192, n: int = 8192, rows=None) -> np.ndarray:
+    """Rows of the N(0, 0.015^2) weights of the bit-width / group sweep."""
+    r = _rows(rows, n)
+    w = np.empty((r.size, k))
+    for i, row in enumerate(r):
+        w[i] = row_rng(3001, row).standard_normal(k) * 0.015
+    return to_f32(w)
 
 
 def sweep_act(k: int = 8192) -> np.ndarray:
     return to_bf16_bits(normal(3002, (1, k)))
 
 
-def crossover_weight(k: int = 8192, n: int = 28672) -> np.ndarray:
-    return to_f32(student_t(4001, (n, k), 5.0, 0.02))
+def crossover_weight(k: int = 8192, n: int = 28672, rows=None) -> np.ndarray:
+    """Rows of the Student-t(5) weights scaled to std 0.02 (crossover shape)."""
+    r = _rows(rows, n)
+    w = np.empty((r.size, k))
+    for i, row in enumerate(r):
+        w[i] = row_rng(4001, row).standard_t(5.0, k) * (0.02 / math.sqrt(5.0 / 3.0))
+    return to_f32(w)
 
 
 def crossover_act(m: int, k: int = 8192) -> np.ndarray:
@@ -122,10 +156,19 @@ def crossover_act(m: int, k: int = 8192) -> np.ndarray:
     return to_bf16_bits(x)
 
 
-def prefill70b_weight(k: int, n: int, seed_offset: int = 0) -> np.ndarray:
-    w = laplace(5001 + seed_offset, (n, k), 0.01)
-    mult = np.exp(rng(5002 + seed_offset).uniform(math.log(0.5), math.log(2.0), (n, 1)))
-    return to_f32(w * mult)
+def prefill70b_row_multipliers(n: int, seed_offset: int = 0) -> np.ndarray:
+    """Per-output-row std multipliers, log-uniform in [0.5, 2]."""
+    return np.exp(rng(5002 + seed_offset).uniform(math.log(0.5), math.log(2.0), n))
+
+
+def prefill70b_weight(k: int, n: int, seed_offset: int = 0, rows=None) -> np.ndarray:
+    """Rows of the Laplace(0, 0.01) weights times their row multiplier."""
+    r = _rows(rows, n)
+    mult = prefill70b_row_multipliers(n, seed_offset)[r]
+    w = np.empty((r.size, k))
+    for i, row in enumerate(r):
+        w[i] = row_rng(5001 + seed_offset, row).laplace(0.0, 0.01, k) * mult[i]
+    return to_f32(w)
 
 
 def prefill70b_act(m: int, k: int) -> np.ndarray:
