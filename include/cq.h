@@ -275,6 +275,15 @@ int64_t cq_get_gemv_max_rows(int32_t path);
  *   GEMM_MFMA     tiled matrix-core GEMM (model dtype B <= 5; A8 W3/W4 with
  *                 G >= 64)
  *   GEMM_TILED    conservative 64 x 64 tiled GEMM (every B, G)
+ *   GEMM_MFMA_ROUNDED  model dtype only: the tiled matrix-core GEMM with the
+ *                 decoded weight s_g q rounded once to the activation dtype
+ *                 before the dot, the dense rounding point of Sec. 5.3 (BF16:
+ *                 one MFMA per product; GEMM_MFMA carries the BF16 operand as
+ *                 hi + lo).  Every weight then carries a relative error of up
+ *                 to 2^-8: measured 0.7e-3 to 2.1e-3 of max|y| on the
+ *                 benchmark layers (hi + lo: about 1e-6), above the 2e-3
+ *                 budget on some, so the built-in rules never pick it; a
+ *                 caller's selection table may.
  * Families that read 32-bit buffer offsets also need tensors below 2 GiB.
  */
 typedef enum { CQ_PATH_MODEL_DTYPE = 0, CQ_PATH_A8 = 1 } cq_path;
@@ -285,7 +294,8 @@ typedef enum {
     CQ_FAMILY_GEMV_NARROW = 3,
     CQ_FAMILY_GEMV_GENERIC = 4,
     CQ_FAMILY_GEMM_MFMA = 5,
-    CQ_FAMILY_GEMM_TILED = 6
+    CQ_FAMILY_GEMM_TILED = 6,
+    CQ_FAMILY_GEMM_MFMA_ROUNDED = 7
 } cq_family;
 
 /*
@@ -324,8 +334,8 @@ typedef struct {
 /*
  * Replace the process-wide table with a copy of entries[0 .. count) (count 0
  * clears it).  Host only.  CQ_ERR_ARG, with the previous table kept, if an
- * entry is malformed (unknown path or family, CQ_FAMILY_AUTO, the LUT family
- * on the A8 path, bits outside 1..8, a group that is not a multiple of 32 in
+ * entry is malformed (unknown path or family, CQ_FAMILY_AUTO, the LUT or
+ * ROUNDED family on the A8 path, bits outside 1..8, a group that is not a multiple of 32 in
  * 32..512, n or k < 1, m_lo < 1 or m_hi < m_lo, a bad x_dtype, reserved != 0)
  * or if two entries of the same path, shape and dtype overlap in m; count
  * above 65536 is CQ_ERR_ARG too.  With overlaps rejected, at most one entry

@@ -40,6 +40,10 @@ hipError_t launch_gemv_a8_narrow(const cq_weight &w, const int8_t *x8, const flo
 bool gemm_a16_mfma_supported(const cq_weight &w, int64_t m);
 hipError_t launch_gemm_a16_mfma(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                                 hipStream_t stream);
+// The same GEMM with the decoded weight rounded once to the activation dtype
+// (one MFMA per product for BF16; FP16 is the default kernel).
+hipError_t launch_gemm_a16_mfma_rounded(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                                        hipStream_t stream);
 
 // Dynamic-A8 activation quantizer.
 hipError_t launch_quant_a8(const void *x, int x_dt, int64_t m, int64_t k, int8_t *x8, float *dx,

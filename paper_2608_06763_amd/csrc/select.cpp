@@ -23,6 +23,7 @@ bool family_supported(int path, int family, const cq_weight &w, int64_t m) {
             case CQ_FAMILY_GEMV_GENERIC: return m <= kGemvMaxRows;
             case CQ_FAMILY_GEMM_MFMA: return gemm_a16_mfma_supported(w, m);
             case CQ_FAMILY_GEMM_TILED: return m <= int64_t(65535) * 64;
+            case CQ_FAMILY_GEMM_MFMA_ROUNDED: return gemm_a16_mfma_supported(w, m);
         }
         return false;
     }
@@ -72,6 +73,7 @@ hipError_t run_family_a16(int family, const cq_weight &w, const void *x, int x_d
         case CQ_FAMILY_GEMV_GENERIC: return launch_gemv_a16_generic(w, x, x_dt, m, y, y_dt, stream);
         case CQ_FAMILY_GEMM_MFMA: return launch_gemm_a16_mfma(w, x, x_dt, m, y, y_dt, stream);
         case CQ_FAMILY_GEMM_TILED: return launch_gemm_a16_tiled(w, x, x_dt, m, y, y_dt, stream);
+        case CQ_FAMILY_GEMM_MFMA_ROUNDED: return launch_gemm_a16_mfma_rounded(w, x, x_dt, m, y, y_dt, stream);
     }
     return hipErrorInvalidValue;
 }
@@ -140,8 +142,9 @@ int table_family(int path, const cq_weight &w, int x_dt, int64_t m) {
 
 bool select_entry_valid(const cq_select_entry &e) {
     if (e.path != CQ_PATH_MODEL_DTYPE && e.path != CQ_PATH_A8) return false;
-    if (e.family < CQ_FAMILY_GEMV_STREAM || e.family > CQ_FAMILY_GEMM_TILED) return false;
-    if (e.path == CQ_PATH_A8 && e.family == CQ_FAMILY_GEMV_LUT) return false;
+    if (e.family < CQ_FAMILY_GEMV_STREAM || e.family > CQ_FAMILY_GEMM_MFMA_ROUNDED) return false;
+    if (e.path == CQ_PATH_A8 && (e.family == CQ_FAMILY_GEMV_LUT || e.family == CQ_FAMILY_GEMM_MFMA_ROUNDED))
+        return false;
     if (e.bits < 1 || e.bits > 8) return false;
     if (e.group < 32 || e.group > 512 || e.group % 32) return false;
     if (e.n < 1 || e.k < 1) return false;

@@ -30,6 +30,9 @@ from . import (CQ_BF16, CQ_FP16, CQ_PATH_A8, CQ_PATH_MODEL_DTYPE, FAMILIES, CQWe
                cq_select_set)
 
 MODEL_DTYPE_FAMILIES = ("gemv_stream", "gemv_lut", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_tiled")
+# Families timed only when a caller asks for them: the single-rounded operand
+# family trades accuracy for speed (its error can exceed the 2e-3 budget).
+OPT_IN_FAMILIES = ("gemm_mfma_rounded",)
 A8_FAMILIES = ("gemv_stream", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_tiled")
 M_MAX = (1 << 40) - 1
 # relative agreement with the built-in choice (max |dy| / max |y|, FP32 output)
@@ -75,10 +78,12 @@ def regimes(ms, choice):
 
 
 def tune(w: CQWeight, path: int, ms, x_dtype=None, activations=None, target_ms: float = 2.0, max_calls: int = 50,
-         log=None) -> dict:
+         log=None, opt_in=()) -> dict:
     """Measure every admissible family of ``path`` on ``w`` at the row counts ``ms``.
 
     activations(m) -> bf16/fp16 [m, K] device tensor; by default N(0, 1) rows.
+    opt_in: families of OPT_IN_FAMILIES to time as well (still subject to the
+    agreement check).
     Returns {"signature", "device", "timings": {m: {family: us}}, "rejected",
     "choice": {m: family}, "entries": [...]} with entries ready for install().
     """
@@ -90,6 +95,7 @@ def tune(w: CQWeight, path: int, ms, x_dtype=None, activations=None, target_ms: 
         activations = lambda m: torch.randn((m, w.k), generator=gen, device="cuda", dtype=torch.float32).to(x_dtype)
     copies = [w] + [w.clone() for _ in range(max(0, min(15, math.ceil(ROTATE_BYTES / w.nbytes) - 1)))]
     names = MODEL_DTYPE_FAMILIES if path == CQ_PATH_MODEL_DTYPE else A8_FAMILIES
+    names = names + tuple(f for f in opt_in if f in OPT_IN_FAMILIES and path == CQ_PATH_MODEL_DTYPE)
     timings, rejected, choice = {}, {}, {}
     for m in ms:
         x = activations(m)

@@ -278,6 +278,8 @@ def test_family_predicates():
     assert not cq.cq_family_supported(md, "gemv_generic", d, 17)
     assert cq.cq_family_supported(md, "gemm_tiled", d, 1)
     assert cq.cq_family_supported(md, "gemm_mfma", d, 1)
+    assert cq.cq_family_supported(md, "gemm_mfma_rounded", d, 1)
+    assert not cq.cq_family_supported(a8, "gemm_mfma_rounded", d, 300)
     assert not cq.cq_family_supported(a8, "gemv_lut", d, 2)
     assert not cq.cq_family_supported(a8, "auto", d, 2)
     assert not cq.cq_family_supported(7, "gemm_tiled", d, 2)
@@ -331,7 +333,8 @@ def test_table_matches_activation_dtype(clean_table):
 
 
 @pytest.mark.parametrize("bad", [
-    dict(path=2), dict(family="auto"), dict(family=7), dict(path=1, family="gemv_lut"), dict(bits=0),
+    dict(path=2), dict(family="auto"), dict(family=8), dict(path=1, family="gemv_lut"),
+    dict(path=1, family="gemm_mfma_rounded"), dict(bits=0),
     dict(bits=9), dict(group=48), dict(group=1024), dict(n=0), dict(k=0), dict(m_lo=0), dict(m_lo=5, m_hi=4),
     dict(x_dtype=2), dict(path=1, x_dtype=0)])
 def test_table_rejects_malformed_entries(clean_table, bad):

@@ -650,7 +650,8 @@ def test_gemm_a8_carriers_equals_gemm_a8(torch_dev, bits, group, m):
 
 # ---------------------------------------------------------------- kernel families and the selection table
 
-MD_FAMILIES = ("gemv_stream", "gemv_lut", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_tiled")
+MD_FAMILIES = ("gemv_stream", "gemv_lut", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_tiled",
+               "gemm_mfma_rounded")
 A8_FAMILIES = ("gemv_stream", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_tiled")
 
 
@@ -659,7 +660,9 @@ A8_FAMILIES = ("gemv_stream", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_
 def test_every_family_matches_oracle(torch_dev, bits, group, m):
     # every admissible family of both paths computes the oracle's product; the
     # matrix-core model-dtype families carry the level as a BF16 hi + lo pair
-    # (16 significant bits), hence 2e-4 on their FP32 output
+    # (16 significant bits), hence 2e-4 on their FP32 output; the rounded
+    # family rounds every weight once to BF16 (relative error <= 2^-8) and is
+    # held to that rounding's own elementwise bound
     n, k = 131, 1024
     r = fitted(140 + bits, n, k, bits, group)
     xb, xv = act(141, m, k)
@@ -678,6 +681,12 @@ def test_every_family_matches_oracle(torch_dev, bits, group, m):
             continue
         say("family model dtype", f, bits, group, m)
         y = cq.cq_gemm_model_dtype_family(w, x, f, y_dtype=torch_dev.float32)
+        if f == "gemm_mfma_rounded":
+            wabs = np.abs(F.decode(r.codes, bits, group, r.scale, r.a_bits, r.b_bits))
+            bound = 2.0 ** -8 * (np.abs(xv) @ wabs.T) * (1 + 2e-3) + 1e-6 * np.max(np.abs(y16_ref))
+            assert np.all(np.abs(_np(y).astype(np.float64) - y16_ref) <= bound), f
+            ran += 1
+            continue
         assert R.eps_comp(_np(y), y16_ref, "fp32") <= 2e-4, f
         assert R.eps_comp(_np(cq.cq_gemm_model_dtype_family(w, x, f)), y16_ref, "bf16") <= TOL, f
         ran += 1
