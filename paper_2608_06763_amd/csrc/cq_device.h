@@ -123,9 +123,11 @@ __device__ __forceinline__ int exact_carrier(int i, int m, double a, double b) {
     if (e > half) { r += 1.0; e -= m3; }
     else if (e < -half) { r -= 1.0; e += m3; }
     if (e == half || e == -half) {
-        // exact tie between r and r +- 1: keep the even one
+        // exact tie between r and r +- 1: keep the even one (r is a small
+        // integer, so its parity is that of its int conversion; a double
+        // fmod would expand to a loop)
         const double other = (e == half) ? r + 1.0 : r - 1.0;
-        if (__builtin_fmod(r, 2.0) != 0.0) r = other;
+        if (int(r) & 1) r = other;
     }
     return int(r);
 }

@@ -36,10 +36,12 @@ bool gemv_a8_narrow_supported(const cq_weight &w, int64_t m);
 hipError_t launch_gemv_a8_narrow(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
                                  hipStream_t stream);
 
-// Model-dtype many-row GEMM for B <= 5 (tensors below 2 GiB).
+// Model-dtype many-row GEMM for B <= 5 (tensors below 2 GiB).  tile_rows is
+// the x-tile height (32, 64, 128 or 256), 0 for the built-in choice by m.
 bool gemm_a16_mfma_supported(const cq_weight &w, int64_t m);
+int a16_mfma_tile_rows(int64_t m);
 hipError_t launch_gemm_a16_mfma(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
-                                hipStream_t stream);
+                                int tile_rows, hipStream_t stream);
 // The same GEMM with the decoded weight rounded once to the activation dtype
 // (one MFMA per product for BF16; FP16 is the default kernel).
 hipError_t launch_gemm_a16_mfma_rounded(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
@@ -85,6 +87,18 @@ hipError_t launch_gemm_a8_mfma(const cq_weight &w, const int8_t *x8, const float
 
 // Largest row count each GEMV family accepts.
 constexpr int64_t kGemvMaxRows = 16;
+
+// x-tile height of a fixed-tile matrix-core family (CQ_FAMILY_GEMM_MFMA_M32
+// .. _M256), 0 for any other family.
+inline int family_tile_rows(int family) {
+    switch (family) {
+        case CQ_FAMILY_GEMM_MFMA_M32: return 32;
+        case CQ_FAMILY_GEMM_MFMA_M64: return 64;
+        case CQ_FAMILY_GEMM_MFMA_M128: return 128;
+        case CQ_FAMILY_GEMM_MFMA_M256: return 256;
+    }
+    return 0;
+}
 
 // Single families, for the measured kernel selection.
 hipError_t launch_gemm_a16_tiled(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,

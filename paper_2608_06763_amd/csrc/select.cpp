@@ -24,6 +24,10 @@ bool family_supported(int path, int family, const cq_weight &w, int64_t m) {
             case CQ_FAMILY_GEMM_MFMA: return gemm_a16_mfma_supported(w, m);
             case CQ_FAMILY_GEMM_TILED: return m <= int64_t(65535) * 64;
             case CQ_FAMILY_GEMM_MFMA_ROUNDED: return gemm_a16_mfma_supported(w, m);
+            case CQ_FAMILY_GEMM_MFMA_M32:
+            case CQ_FAMILY_GEMM_MFMA_M64:
+            case CQ_FAMILY_GEMM_MFMA_M128:
+            case CQ_FAMILY_GEMM_MFMA_M256: return gemm_a16_mfma_supported(w, m);
         }
         return false;
     }
@@ -71,9 +75,14 @@ hipError_t run_family_a16(int family, const cq_weight &w, const void *x, int x_d
         case CQ_FAMILY_GEMV_LUT: return launch_gemv_a16_lut(w, x, x_dt, m, y, y_dt, stream);
         case CQ_FAMILY_GEMV_NARROW: return launch_gemv_a16_narrow(w, x, x_dt, m, y, y_dt, stream);
         case CQ_FAMILY_GEMV_GENERIC: return launch_gemv_a16_generic(w, x, x_dt, m, y, y_dt, stream);
-        case CQ_FAMILY_GEMM_MFMA: return launch_gemm_a16_mfma(w, x, x_dt, m, y, y_dt, stream);
+        case CQ_FAMILY_GEMM_MFMA: return launch_gemm_a16_mfma(w, x, x_dt, m, y, y_dt, 0, stream);
         case CQ_FAMILY_GEMM_TILED: return launch_gemm_a16_tiled(w, x, x_dt, m, y, y_dt, stream);
         case CQ_FAMILY_GEMM_MFMA_ROUNDED: return launch_gemm_a16_mfma_rounded(w, x, x_dt, m, y, y_dt, stream);
+        case CQ_FAMILY_GEMM_MFMA_M32:
+        case CQ_FAMILY_GEMM_MFMA_M64:
+        case CQ_FAMILY_GEMM_MFMA_M128:
+        case CQ_FAMILY_GEMM_MFMA_M256:
+            return launch_gemm_a16_mfma(w, x, x_dt, m, y, y_dt, family_tile_rows(family), stream);
     }
     return hipErrorInvalidValue;
 }
@@ -142,8 +151,9 @@ int table_family(int path, const cq_weight &w, int x_dt, int64_t m) {
 
 bool select_entry_valid(const cq_select_entry &e) {
     if (e.path != CQ_PATH_MODEL_DTYPE && e.path != CQ_PATH_A8) return false;
-    if (e.family < CQ_FAMILY_GEMV_STREAM || e.family > CQ_FAMILY_GEMM_MFMA_ROUNDED) return false;
-    if (e.path == CQ_PATH_A8 && (e.family == CQ_FAMILY_GEMV_LUT || e.family == CQ_FAMILY_GEMM_MFMA_ROUNDED))
+    if (e.family < CQ_FAMILY_GEMV_STREAM || e.family > CQ_FAMILY_GEMM_MFMA_M256) return false;
+    if (e.path == CQ_PATH_A8 && (e.family == CQ_FAMILY_GEMV_LUT || e.family == CQ_FAMILY_GEMM_MFMA_ROUNDED ||
+                                 family_tile_rows(e.family) != 0))
         return false;
     if (e.bits < 1 || e.bits > 8) return false;
     if (e.group < 32 || e.group > 512 || e.group % 32) return false;

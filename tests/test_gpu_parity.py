@@ -650,8 +650,8 @@ def test_gemm_a8_carriers_equals_gemm_a8(torch_dev, bits, group, m):
 
 # ---------------------------------------------------------------- kernel families and the selection table
 
-MD_FAMILIES = ("gemv_stream", "gemv_lut", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_tiled",
-               "gemm_mfma_rounded")
+MD_FAMILIES = ("gemv_stream", "gemv_lut", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_mfma_m32",
+               "gemm_mfma_m64", "gemm_mfma_m128", "gemm_mfma_m256", "gemm_tiled", "gemm_mfma_rounded")
 A8_FAMILIES = ("gemv_stream", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_tiled")
 
 
@@ -698,6 +698,29 @@ def test_every_family_matches_oracle(torch_dev, bits, group, m):
         assert R.eps_comp(_np(y), y8_ref, "fp32") <= 1e-5, f
         ran += 1
     assert ran >= 2
+
+
+# ---------------------------------------------------------------- x-tile heights of the matrix-core GEMM
+
+@pytest.mark.parametrize("m", [5, 17, 40, 64, 100, 129, 300])
+def test_gemm_tile_heights_bit_equal(torch_dev, m):
+    # every x-tile height runs the same FP32 accumulation chain per output:
+    # the fixed-height families are bit-equal to each other and to the oracle
+    # within the dense-path bar
+    cq = _cq()
+    n, k, bits, group = 300, 1024, 4, 128
+    r = fitted(340, n, k, bits, group)
+    w = _weight(r, bits, group)
+    xb, xv = act(341 + m, m, k)
+    x = _x(torch_dev, xb, "bf16")
+    y_ref = ref_model_dtype(xv, r, bits, group)
+    outs = []
+    for f in ("gemm_mfma_m32", "gemm_mfma_m64", "gemm_mfma_m128", "gemm_mfma_m256", "gemm_mfma"):
+        say("tile height", f, m)
+        outs.append(cq.cq_gemm_model_dtype_family(w, x, f, y_dtype=torch_dev.float32))
+    for o in outs[1:]:
+        assert torch_dev.equal(o, outs[0])
+    assert R.eps_comp(_np(outs[0]), y_ref, "fp32") <= 2e-4
 
 
 def test_selection_table_drives_dispatch(torch_dev):
