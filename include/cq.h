@@ -287,7 +287,8 @@ int64_t cq_get_gemv_max_rows(int32_t path);
  *   GEMM_MFMA_M32, _M64, _M128, _M256  GEMM_MFMA with a fixed x-tile height
  *                 (rows of x per workgroup tile; the tile-height dimension of
  *                 the selection in Sec. 5.6).  GEMM_MFMA picks the smallest of
- *                 32, 64, 128 that holds m, else 256.  Model dtype B <= 5.
+ *                 32, 64, 128 that holds m, else 256 (an A8 partials dump
+ *                 always runs the 256-row tile).  Same widths as GEMM_MFMA.
  * Families that read 32-bit buffer offsets also need tensors below 2 GiB.
  */
 typedef enum { CQ_PATH_MODEL_DTYPE = 0, CQ_PATH_A8 = 1 } cq_path;
@@ -342,8 +343,8 @@ typedef struct {
 /*
  * Replace the process-wide table with a copy of entries[0 .. count) (count 0
  * clears it).  Host only.  CQ_ERR_ARG, with the previous table kept, if an
- * entry is malformed (unknown path or family, CQ_FAMILY_AUTO, the LUT,
- * ROUNDED or fixed-tile-height families on the A8 path, bits outside 1..8, a group that is not a multiple of 32 in
+ * entry is malformed (unknown path or family, CQ_FAMILY_AUTO, the LUT or
+ * ROUNDED family on the A8 path, bits outside 1..8, a group that is not a multiple of 32 in
  * 32..512, n or k < 1, m_lo < 1 or m_hi < m_lo, a bad x_dtype, reserved != 0)
  * or if two entries of the same path, shape and dtype overlap in m; count
  * above 65536 is CQ_ERR_ARG too.  With overlaps rejected, at most one entry

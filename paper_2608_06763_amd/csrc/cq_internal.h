@@ -81,9 +81,13 @@ hipError_t launch_gemv_a8_stream(const cq_weight &w, const int8_t *x8, const flo
                                  hipStream_t stream);
 
 // Dynamic-A8 many-row GEMM for W3 and W4, G >= 64 (tensors below 2 GiB).
+// tile_rows: x-tile height 32, 64, 128 (gemm_a8_tile.hip) or 256, 0 for the
+// built-in choice by m; a partials dump always takes the 256-row kernel.
 bool gemm_a8_mfma_supported(const cq_weight &w, int64_t m);
 hipError_t launch_gemm_a8_mfma(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
-                               int32_t *partials, hipStream_t stream);
+                               int32_t *partials, int tile_rows, hipStream_t stream);
+hipError_t launch_gemm_a8_tile(const cq_weight &w, const int8_t *ctab, const int8_t *x8, const float *dx, int64_t m,
+                               void *y, int y_dt, int tile_rows, hipStream_t stream);
 
 // Largest row count each GEMV family accepts.
 constexpr int64_t kGemvMaxRows = 16;

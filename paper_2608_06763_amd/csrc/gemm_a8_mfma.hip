@@ -494,13 +494,22 @@ static hipError_t a8_mfma_dispatch(const cq_weight &w, const int8_t *ctab, const
     return a8_mfma_group<4, 2, TB>(w, x8, dx, m, y, partials, ctab, stream);
 }
 
+// x-tile height for m rows when the caller does not name one: the smallest
+// of 32, 64, 128 that holds m (gemm_a8_tile.hip), else 256 (this file)
+static int a8_mfma_tile_rows(int64_t m) { return m <= 32 ? 32 : m <= 64 ? 64 : m <= 128 ? 128 : 256; }
+
 hipError_t launch_gemm_a8_mfma(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
-                               int32_t *partials, hipStream_t stream) {
+                               int32_t *partials, int tile_rows, hipStream_t stream) {
+    // the partials dump is written by the 256-row kernel's four-wave variant
+    const int tr = partials ? 256 : (tile_rows ? tile_rows : a8_mfma_tile_rows(m));
+    if (tr != 256) return launch_gemm_a8_tile(w, nullptr, x8, dx, m, y, y_dt, tr, stream);
     return a8_mfma_dispatch<false>(w, nullptr, x8, dx, m, y, y_dt, partials, stream);
 }
 
 hipError_t launch_gemm_a8_mfma_tab(const cq_weight &w, const int8_t *ctab, const int8_t *x8, const float *dx,
                                    int64_t m, void *y, int y_dt, hipStream_t stream) {
+    const int tr = a8_mfma_tile_rows(m);
+    if (tr != 256) return launch_gemm_a8_tile(w, ctab, x8, dx, m, y, y_dt, tr, stream);
     return a8_mfma_dispatch<true>(w, ctab, x8, dx, m, y, y_dt, nullptr, stream);
 }
 

@@ -38,6 +38,10 @@ bool family_supported(int path, int family, const cq_weight &w, int64_t m) {
             case CQ_FAMILY_GEMV_GENERIC: return m <= kGemvMaxRows;
             case CQ_FAMILY_GEMM_MFMA: return gemm_a8_mfma_supported(w, m);
             case CQ_FAMILY_GEMM_TILED: return m <= int64_t(65535) * 64;
+            case CQ_FAMILY_GEMM_MFMA_M32:
+            case CQ_FAMILY_GEMM_MFMA_M64:
+            case CQ_FAMILY_GEMM_MFMA_M128:
+            case CQ_FAMILY_GEMM_MFMA_M256: return gemm_a8_mfma_supported(w, m);
         }
         return false;
     }
@@ -93,8 +97,13 @@ hipError_t run_family_a8(int family, const cq_weight &w, const int8_t *x8, const
         case CQ_FAMILY_GEMV_STREAM: return launch_gemv_a8_stream(w, x8, dx, y, y_dt, stream);
         case CQ_FAMILY_GEMV_NARROW: return launch_gemv_a8_narrow(w, x8, dx, m, y, y_dt, stream);
         case CQ_FAMILY_GEMV_GENERIC: return launch_gemv_a8_generic(w, x8, dx, m, y, y_dt, partials, stream);
-        case CQ_FAMILY_GEMM_MFMA: return launch_gemm_a8_mfma(w, x8, dx, m, y, y_dt, partials, stream);
+        case CQ_FAMILY_GEMM_MFMA: return launch_gemm_a8_mfma(w, x8, dx, m, y, y_dt, partials, 0, stream);
         case CQ_FAMILY_GEMM_TILED: return launch_gemm_a8_tiled(w, x8, dx, m, y, y_dt, partials, stream);
+        case CQ_FAMILY_GEMM_MFMA_M32:
+        case CQ_FAMILY_GEMM_MFMA_M64:
+        case CQ_FAMILY_GEMM_MFMA_M128:
+        case CQ_FAMILY_GEMM_MFMA_M256:
+            return launch_gemm_a8_mfma(w, x8, dx, m, y, y_dt, partials, family_tile_rows(family), stream);
     }
     return hipErrorInvalidValue;
 }
@@ -152,8 +161,7 @@ int table_family(int path, const cq_weight &w, int x_dt, int64_t m) {
 bool select_entry_valid(const cq_select_entry &e) {
     if (e.path != CQ_PATH_MODEL_DTYPE && e.path != CQ_PATH_A8) return false;
     if (e.family < CQ_FAMILY_GEMV_STREAM || e.family > CQ_FAMILY_GEMM_MFMA_M256) return false;
-    if (e.path == CQ_PATH_A8 && (e.family == CQ_FAMILY_GEMV_LUT || e.family == CQ_FAMILY_GEMM_MFMA_ROUNDED ||
-                                 family_tile_rows(e.family) != 0))
+    if (e.path == CQ_PATH_A8 && (e.family == CQ_FAMILY_GEMV_LUT || e.family == CQ_FAMILY_GEMM_MFMA_ROUNDED))
         return false;
     if (e.bits < 1 || e.bits > 8) return false;
     if (e.group < 32 || e.group > 512 || e.group % 32) return false;

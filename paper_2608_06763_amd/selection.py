@@ -34,7 +34,8 @@ MODEL_DTYPE_FAMILIES = ("gemv_stream", "gemv_lut", "gemv_narrow", "gemv_generic"
 # Families timed only when a caller asks for them: the single-rounded operand
 # family trades accuracy for speed (its error can exceed the 2e-3 budget).
 OPT_IN_FAMILIES = ("gemm_mfma_rounded",)
-A8_FAMILIES = ("gemv_stream", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_tiled")
+A8_FAMILIES = ("gemv_stream", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_mfma_m32", "gemm_mfma_m64",
+               "gemm_mfma_m128", "gemm_mfma_m256", "gemm_tiled")
 M_MAX = (1 << 40) - 1
 # relative agreement with the built-in choice (max |dy| / max |y|, FP32 output)
 AGREE = 2e-3

@@ -333,7 +333,7 @@ def test_table_matches_activation_dtype(clean_table):
 
 
 @pytest.mark.parametrize("bad", [
-    dict(path=2), dict(family="auto"), dict(family=12), dict(path=1, family="gemv_lut"), dict(path=1, family="gemm_mfma_m64"),
+    dict(path=2), dict(family="auto"), dict(family=12), dict(path=1, family="gemv_lut"),
     dict(path=1, family="gemm_mfma_rounded"), dict(bits=0),
     dict(bits=9), dict(group=48), dict(group=1024), dict(n=0), dict(k=0), dict(m_lo=0), dict(m_lo=5, m_hi=4),
     dict(x_dtype=2), dict(path=1, x_dtype=0)])

