@@ -22,7 +22,8 @@
  *   - All pointers marked "device" are HIP device pointers; the caller owns
  *     every buffer and keeps it alive until the stream has finished the call.
  *     The library allocates no memory in any call declared here and keeps no
- *     state besides a per-device property cache.
+ *     state besides a per-device property cache and the scratch array of
+ *     cq_gemm_routed_model_dtype_noalloc.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *     Device calls are asynchronous and stream ordered; they validate their
  *     arguments on the host in O(1) and return a status synchronously.  A
@@ -240,6 +241,27 @@ cq_status cq_gemm_routed_model_dtype(const cq_weight *bank, int32_t n_experts, c
                                      cq_dtype x_dtype, int64_t tokens, const int32_t *route_token,
                                      const int32_t *route_expert, int64_t routes, int32_t *workspace,
                                      void *y, cq_dtype y_dtype, void *stream);
+
+/*
+ * cq_gemm_routed_model_dtype_noalloc -- the routed product without a caller
+ * workspace, for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation).
+ *
+ * Arguments, result and routing rules as cq_gemm_routed_model_dtype, minus
+ * `workspace`: the expert grouping uses a scratch array that the library
+ * holds on each device for the life of the process (4 MiB per device, found
+ * on the first call on a device).  Limit: n_experts + 1 + routes <= 2^20
+ * (CQ_ERR_SHAPE otherwise, before anything is launched).  The call allocates
+ * nothing.  All calls on one device share its scratch: calls that can overlap
+ * on that device (other streams, other host threads) race on it and must be
+ * ordered by the caller; calls on one stream are ordered.  Nothing in the
+ * scratch needs to start at zero (every entry read is first written by the
+ * same call).
+ */
+cq_status cq_gemm_routed_model_dtype_noalloc(const cq_weight *bank, int32_t n_experts, const void *x,
+                                             cq_dtype x_dtype, int64_t tokens, const int32_t *route_token,
+                                             const int32_t *route_expert, int64_t routes, void *y,
+                                             cq_dtype y_dtype, void *stream);
 
 /*
  * Row-regime kernel selection (Sec. 5.5-5.6).  Each path picks the GEMV

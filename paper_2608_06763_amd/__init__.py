@@ -8,7 +8,7 @@ GPU; calling a device entry point does, and a missing library raises.
 Entry points (same names as the C ABI):
   cq_pack_groups, cq_decode_ref, cq_gemm_model_dtype, cq_quantize_act_a8,
   cq_gemm_a8, cq_gemm_a8_fused, cq_build_carriers, cq_gemm_a8_carriers,
-  cq_gemm_routed_model_dtype, cq_set_gemv_max_rows, cq_get_gemv_max_rows,
+  cq_gemm_routed_model_dtype, cq_gemm_routed_model_dtype_noalloc, cq_set_gemv_max_rows, cq_get_gemv_max_rows,
   cq_family_supported, cq_gemm_model_dtype_family, cq_gemm_a8_family,
   cq_select_set, cq_select_query, cq_probe_read (measurement aid)
 The measured kernel-selection tuner that fills the selection table is in
@@ -32,7 +32,7 @@ EXPORTS = ("cq_status_str", "cq_pack_groups", "cq_decode_ref", "cq_gemm_model_dt
            "cq_gemm_a8", "cq_gemm_a8_fused", "cq_build_carriers", "cq_gemm_a8_carriers",
            "cq_gemm_routed_model_dtype", "cq_set_gemv_max_rows", "cq_get_gemv_max_rows",
            "cq_family_supported", "cq_gemm_model_dtype_family", "cq_gemm_a8_family", "cq_select_set",
-           "cq_select_query", "cq_probe_read")
+           "cq_select_query", "cq_probe_read", "cq_gemm_routed_model_dtype_noalloc")
 
 CQ_PATH_MODEL_DTYPE, CQ_PATH_A8 = 0, 1
 FAMILIES = {"auto": 0, "gemv_stream": 1, "gemv_lut": 2, "gemv_narrow": 3, "gemv_generic": 4, "gemm_mfma": 5,
@@ -92,6 +92,9 @@ def lib() -> ctypes.CDLL:
     L.cq_gemm_routed_model_dtype.restype = ctypes.c_int
     L.cq_gemm_routed_model_dtype.argtypes = [ctypes.POINTER(cq_weight), i32, vp, ctypes.c_int, i64, vp, vp, i64, vp, vp,
                                              ctypes.c_int, vp]
+    L.cq_gemm_routed_model_dtype_noalloc.restype = ctypes.c_int
+    L.cq_gemm_routed_model_dtype_noalloc.argtypes = [ctypes.POINTER(cq_weight), i32, vp, ctypes.c_int, i64, vp, vp, i64,
+                                                     vp, ctypes.c_int, vp]
     L.cq_set_gemv_max_rows.restype = ctypes.c_int
     L.cq_set_gemv_max_rows.argtypes = [i32, i64]
     L.cq_get_gemv_max_rows.restype = i64
@@ -319,6 +322,28 @@ def cq_gemm_routed_model_dtype(bank: CQWeight, n_experts: int, x, route_token, r
                                           route_token.data_ptr(), route_expert.data_ptr(), routes, workspace.data_ptr(),
                                           out.data_ptr(), _dt(out.dtype), _stream_ptr(stream))
     _check(st, "cq_gemm_routed_model_dtype")
+    return out
+
+
+def cq_gemm_routed_model_dtype_noalloc(bank: CQWeight, n_experts: int, x, route_token, route_expert, y_dtype=None,
+                                       out=None, stream=None):
+    """The routed product without a workspace: the library's per-device scratch
+    holds the expert grouping (n_experts + 1 + routes <= 2^20)."""
+    torch = _torch()
+    assert x.dim() == 2 and x.shape[1] == bank.k and x.is_contiguous()
+    assert bank.n % n_experts == 0
+    n = bank.n // n_experts
+    routes = route_token.numel()
+    assert route_expert.numel() == routes and route_token.dtype == torch.int32 and route_expert.dtype == torch.int32
+    y_dtype = y_dtype or x.dtype
+    if out is None:
+        out = torch.empty((routes, n), dtype=y_dtype, device=x.device)
+    desc = cq_weight(bank.bits, bank.group, n, bank.k, bank.codes.data_ptr(), bank.scale.data_ptr(), bank.a.data_ptr(),
+                     bank.b.data_ptr())
+    st = lib().cq_gemm_routed_model_dtype_noalloc(ctypes.byref(desc), n_experts, x.data_ptr(), _dt(x.dtype),
+                                                  x.shape[0], route_token.data_ptr(), route_expert.data_ptr(), routes,
+                                                  out.data_ptr(), _dt(out.dtype), _stream_ptr(stream))
+    _check(st, "cq_gemm_routed_model_dtype_noalloc")
     return out
 
 

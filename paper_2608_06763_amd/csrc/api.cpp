@@ -224,6 +224,28 @@ cq_status cq_gemm_routed_model_dtype(const cq_weight *bank, int32_t n_experts, c
                                                     static_cast<hipStream_t>(stream)));
 }
 
+cq_status cq_gemm_routed_model_dtype_noalloc(const cq_weight *bank, int32_t n_experts, const void *x, cq_dtype x_dtype,
+                                             int64_t tokens, const int32_t *route_token, const int32_t *route_expert,
+                                             int64_t routes, void *y, cq_dtype y_dtype, void *stream) {
+    const cq_status st = check_weight(bank);
+    if (st != CQ_OK) return st;
+    if (n_experts < 1 || tokens < 1 || routes < 0) return CQ_ERR_ARG;
+    if (!x || !route_token || !route_expert || !y) return CQ_ERR_ARG;
+    if (x_dtype != CQ_BF16 && x_dtype != CQ_FP16) return CQ_ERR_DTYPE;
+    if (y_dtype != x_dtype && y_dtype != CQ_FP32) return CQ_ERR_DTYPE;
+    if (!aligned16(x) || !aligned16(y)) return CQ_ERR_ALIGN;
+    if ((reinterpret_cast<uintptr_t>(route_token) | reinterpret_cast<uintptr_t>(route_expert)) % 4) return CQ_ERR_ALIGN;
+    if (bank->n > (int64_t(1) << 40) / bank->k / n_experts) return CQ_ERR_SHAPE;
+    if (tokens > (int64_t(1) << 40) / bank->k || routes > (int64_t(1) << 40) / bank->n) return CQ_ERR_SHAPE;
+    // the grouping needs n_experts + 1 + routes ints of the library's scratch
+    if (int64_t(n_experts) + 1 + routes > cq::kNoAllocRoutedInts) return CQ_ERR_SHAPE;
+    if (!cq::routed_supported(*bank, n_experts, tokens, routes)) return CQ_ERR_UNSUPPORTED;
+    if (routes == 0) return CQ_OK;
+    return hip_status(cq::launch_routed_model_dtype_noalloc(*bank, n_experts, x, int(x_dtype), tokens, route_token,
+                                                            route_expert, routes, y, int(y_dtype),
+                                                            static_cast<hipStream_t>(stream)));
+}
+
 cq_status cq_build_carriers(const cq_weight *w, int8_t *carriers, void *stream) {
     const cq_status st = check_weight(w);
     if (st != CQ_OK) return st;

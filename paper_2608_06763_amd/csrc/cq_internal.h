@@ -75,6 +75,13 @@ hipError_t launch_gemm_a8_mfma_tab(const cq_weight &w, const int8_t *ctab, const
 hipError_t launch_routed_model_dtype(const cq_weight &w, int n_experts, const void *x, int x_dt, int64_t tokens,
                                      const int32_t *token, const int32_t *expert, int64_t routes, int32_t *workspace,
                                      void *y, int y_dt, hipStream_t stream);
+// The same with the library's per-device scratch array as the workspace
+// (n_experts + 1 + routes <= kNoAllocRoutedInts; checked by the caller).
+constexpr int64_t kNoAllocRoutedInts = int64_t(1) << 20;
+hipError_t routed_scratch(int32_t **ptr);
+hipError_t launch_routed_model_dtype_noalloc(const cq_weight &w, int n_experts, const void *x, int x_dt,
+                                             int64_t tokens, const int32_t *token, const int32_t *expert,
+                                             int64_t routes, void *y, int y_dt, hipStream_t stream);
 hipError_t launch_gemv_a8_fused(const cq_weight &w, const void *x, int x_dt, int8_t *x8_out, float *dx_out, void *y,
                                 int y_dt, hipStream_t stream);
 hipError_t launch_gemv_a8_stream(const cq_weight &w, const int8_t *x8, const float *dx, void *y, int y_dt,

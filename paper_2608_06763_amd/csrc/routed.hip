@@ -17,9 +17,17 @@
 #include "cq_device.h"
 #include "cq_internal.h"
 
+#include <mutex>
+
 namespace cq {
 
 constexpr int kRouteThreads = 1024;
+
+// Device scratch of the no-allocation routed call: the expert offsets and the
+// grouped route order (n_experts + 1 + routes ints), one array per device,
+// held until the process ends.  Host code never names it directly: its device
+// address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) int32_t scratch[kNoAllocRoutedInts];
 
 // offsets: [E + 1]; order: [R].  counters in dynamic LDS: E + 1 ints, the last
 // one counts dropped routes.
@@ -90,6 +98,43 @@ hipError_t launch_routed_model_dtype(const cq_weight &w, int n_experts, const vo
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_gemv_a16_routed(w, n_experts, x, x_dt, tokens, token, order, offsets, y, y_dt, stream);
+}
+
+namespace {
+
+constexpr int kMaxScratchDevices = 64;
+struct scratch_slot {
+    std::once_flag once;
+    int32_t *ptr = nullptr;
+    hipError_t err = hipSuccess;
+};
+scratch_slot g_scratch[kMaxScratchDevices];
+
+}  // namespace
+
+hipError_t routed_scratch(int32_t **ptr) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+    scratch_slot &s = g_scratch[dev];
+    // first call on this device, with it current: the array's address there
+    std::call_once(s.once, [&s] {
+        void *p = nullptr;
+        s.err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (s.err == hipSuccess) s.ptr = static_cast<int32_t *>(p);
+    });
+    *ptr = s.ptr;
+    return s.err;
+}
+
+hipError_t launch_routed_model_dtype_noalloc(const cq_weight &w, int n_experts, const void *x, int x_dt,
+                                             int64_t tokens, const int32_t *token, const int32_t *expert,
+                                             int64_t routes, void *y, int y_dt, hipStream_t stream) {
+    int32_t *ws = nullptr;
+    const hipError_t e = routed_scratch(&ws);
+    if (e != hipSuccess) return e;
+    return launch_routed_model_dtype(w, n_experts, x, x_dt, tokens, token, expert, routes, ws, y, y_dt, stream);
 }
 
 }  // namespace cq
