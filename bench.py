@@ -11,9 +11,13 @@ times the 256 MB Infinity Cache): every step reads its weights from HBM.
 
 The reported value is effective HBM GB/s: algorithmic bytes (packed payload
 plus metadata read once, activations, outputs) per second of wall time.
-A rows sweep on the K=8192, N=28672 shape adds GEMM TFLOPS/TOPS against row
-count for both paths.  The CPU oracle is timed on a bounded sample of the same
-decode workload as a reported baseline.
+Sweeps add: the decode layers at M = 1, 4, 16; a rows sweep on the K=8192,
+N=28672 shape (GEMM TFLOPS/TOPS against row count for both paths, and the
+crossover); the 70B-class prefill GEMMs (W3/W4, M = 2048 and 8192); the
+bit-width/group sweep; kernel selection; the routed product; a flushed
+single-launch latency.  The CPU oracle is timed on a bounded sample of the
+same decode workload as a reported baseline, in the same leg as an oracle fit
+of the single-GEMV weights whose GPU timing is compared with the stand-in's.
 
 Prints one JSON line on stdout; progress goes to stderr.
 """
@@ -53,9 +57,9 @@ def a8_bytes(m, n, k, bits, group):
     return weight_bytes(n, k, bits, group) + m * k + 4 * m + 2 * m * n
 
 
-def make_weight(cq, seed, n, k, bits, group):
+def make_weight(cq, seed, n, k, bits, group, block_rows=None):
     from workloads import synthetic_representation
-    codes, s, a, b = synthetic_representation(seed, n, k, bits, group)
+    codes, s, a, b = synthetic_representation(seed, n, k, bits, group, block_rows=block_rows)
     return cq.CQWeight.from_codes(codes, s, a, b, bits, group)
 
 
@@ -123,8 +127,8 @@ def _cpu_baseline_run(layers_np, bits, group, budget_s, blas_threads, gpu_out):
     parity = {"model_dtype_eps_comp_max": 0.0, "rows_checked": 0, "a8_x8_dx_bitexact": True}
     for li, (name, k, n, codes, s, a, b, x_vals) in enumerate(layers_np):
         rows = max(1, int(n * frac))
+        packed = F.pack(codes[:rows], bits)  # the packed input the oracle starts from (not timed)
         t0 = time.perf_counter()
-        packed = F.pack(codes[:rows], bits)
         kk = F.unpack(packed, bits, k)
         y = R.gemm_model_dtype(x_vals, kk, bits, group, s[:rows], a[:rows], b[:rows])
         spent += time.perf_counter() - t0
@@ -142,6 +146,7 @@ def _cpu_baseline_run(layers_np, bits, group, budget_s, blas_threads, gpu_out):
         if spent > budget_s:
             break
     return {"value": done_bytes / spent / 1e9, "unit": "GB/s", "cores": int(blas_threads), "kind": "oracle",
+            "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
             "sample": f"oracle unpack+decode(fp64)+product on {rows_done} weight rows "
                       f"(first half of each decode layer, M=1), {spent:.1f} s; elementwise numpy on 1 thread, "
                       f"product on {blas_threads} BLAS threads",
@@ -164,8 +169,11 @@ def routed_sweep(torch, cq, bits=4, group=128, token_counts=(1, 4, 16, 64)):
         banks = [cq.CQWeight(rep(w1.codes), rep(w1.scale), rep(w1.a), rep(w1.b), bits, group, n * MOE_EXPERTS, k)]
         banks.append(banks[0].clone())  # two banks alternate (together above the 256 MB Infinity Cache)
         del w1
-        for t in token_counts:
-            tok, exp = route_map(7100 + t, t, MOE_EXPERTS, MOE_TOPK)
+        cases = [(t, route_map(7100 + t, t, MOE_EXPERTS, MOE_TOPK)) for t in token_counts]
+        # a skewed map: 8 tokens all routed to one expert (8 routes <= 8 experts,
+        # so the streaming mode runs and streams that expert once per route)
+        cases.append((8, (np.arange(8, dtype=np.int32), np.zeros(8, dtype=np.int32))))
+        for t, (tok, exp) in cases:
             tt = torch.from_numpy(tok).cuda()
             te = torch.from_numpy(exp).cuda()
             x = torch.randn(t, k, device="cuda").to(torch.bfloat16)
@@ -175,7 +183,8 @@ def routed_sweep(torch, cq, bits=4, group=128, token_counts=(1, 4, 16, 64)):
             us = graph_timed(torch, run, 8) * 1e3
             active = len(set(exp.tolist()))
             eff = active * weight_bytes(n, k, bits, group) + 2 * t * k + 2 * len(tok) * n
-            rec = {"layer": name, "k": k, "n": n, "experts": MOE_EXPERTS, "topk": MOE_TOPK, "tokens": t,
+            rec = {"layer": name, "k": k, "n": n, "experts": MOE_EXPERTS,
+                   "topk": MOE_TOPK if len(set(exp.tolist())) > 1 else "skewed: every route to one expert", "tokens": t,
                    "routes": len(tok), "active_experts": active, "us": round(us, 2),
                    "effective_gbs": round(eff / us / 1e3, 1), "hbm_frac": round(eff / us / 1e3 / HBM_PEAK_GBS, 4)}
             out.append(rec)
@@ -204,12 +213,21 @@ def rows_sweep(torch, cq, bits=4, group=128, k=8192, n=28672, ms=(1, 2, 8, 32, 1
         a8t = lambda i: cq.cq_gemm_a8_carriers(copies[i % len(copies)], tabs[i % len(copies)], x8, dx, out=y)
         a16(0); quant(0); a8g(0); a8t(0)
         torch.cuda.synchronize()
+        t16r = None
+        if cq.cq_family_supported(cq.CQ_PATH_MODEL_DTYPE, "gemm_mfma_rounded", w0, m) and m > 16:
+            # the single-rounded operand (diagnostic family, outside the error budget on this layer)
+            a16r = lambda i: cq.cq_gemm_model_dtype_family(copies[i % len(copies)], x, "gemm_mfma_rounded", out=y)
+            a16r(0)
+            t16r = timed(torch, a16r, it)
         t16 = timed(torch, a16, it)
         tq = timed(torch, quant, it)
         t8 = timed(torch, a8g, it)
         t8t = timed(torch, a8t, it)
         flops = 2.0 * m * n * k
-        rec = {"m": m, "a16_ms": t16, "a8_gemm_ms": t8, "a8_quant_ms": tq, "a8_op_ms": t8 + tq,
+        rec = {"m": m, "a16_family": cq.cq_select_query(cq.CQ_PATH_MODEL_DTYPE, w0, m),
+               "a8_family": cq.cq_select_query(cq.CQ_PATH_A8, w0, m),
+               "a16_ms": t16, "a8_gemm_ms": t8, "a8_quant_ms": tq, "a8_op_ms": t8 + tq,
+               "a16_rounded_operand_ms": t16r,
                "a8_gemm_tables_ms": t8t, "a8_tables_tops": flops / t8t / 1e9,
                "a16_tflops": flops / t16 / 1e9, "a8_tops": flops / t8 / 1e9,
                "a16_gbs": a16_bytes(m, n, k, bits, group) / t16 / 1e6,
@@ -278,6 +296,196 @@ def selection_sweep(torch, cq, bits=4, group=128, k=8192, n=28672, ms=(1, 2, 8, 
             "rejected": {str(m): v for m, v in t["rejected"].items()},
         }
     return {"shape": {"k": k, "n": n, "bits": bits, "group": group}, "device": S.device_signature(), **out}
+
+
+def prefill_sweep(torch, cq, ceil, widths=(3, 4), group=128, ms=(2048, 8192)):
+    """70B-class prefill GEMMs (K, N) in {(8192, 28672), (28672, 8192),
+    (8192, 10240)}, W3 and W4 G128, M in {2048, 8192}, both paths: the
+    model-dtype matrix-core GEMM (TFLOP/s, against the BF16 peak and the
+    measured hipBLASLt GEMM) and the Dynamic-A8 operator (quantizer + int8
+    GEMM, TOP/s against the int8 peak; the GEMM alone too).  Two weight copies
+    alternate; at these row counts the products are matrix-core bound."""
+    from workloads import PREFILL70B_SHAPES, prefill70b_act
+    out = []
+    for si, (k, n) in enumerate(PREFILL70B_SHAPES):
+        for bits in widths:
+            w0 = make_weight(cq, 6000 + 10 * si + bits, n, k, bits, group, block_rows=1024)
+            ws = [w0, w0.clone()]
+            for m in ms:
+                x = torch.from_numpy(prefill70b_act(m, k).view(np.int16)).cuda().view(torch.bfloat16)
+                y = torch.empty((m, n), dtype=torch.bfloat16, device="cuda")
+                x8 = torch.empty((m, k), dtype=torch.int8, device="cuda")
+                dx = torch.empty((m,), dtype=torch.float32, device="cuda")
+                it = 4 if m <= 2048 else 2
+                a16 = lambda i: cq.cq_gemm_model_dtype(ws[i % 2], x, out=y)
+                quant = lambda i: cq.cq_quantize_act_a8(x, x8, dx)
+                a8g = lambda i: cq.cq_gemm_a8(ws[i % 2], x8, dx, out=y)
+                a16(0); quant(0); a8g(0)
+                torch.cuda.synchronize()
+                t16, tq, t8 = timed(torch, a16, it), timed(torch, quant, it), timed(torch, a8g, it)
+                flops = 2.0 * m * n * k
+                rec = {"k": k, "n": n, "bits": bits, "group": group, "m": m,
+                       "a16_ms": round(t16, 4), "a16_tflops": round(flops / t16 / 1e9, 1),
+                       "a16_frac_bf16_peak": round(flops / t16 / 1e9 / BF16_PEAK_TFLOPS, 4),
+                       "a16_frac_of_measured_bf16_gemm": round(flops / t16 / 1e9 / ceil["bf16_gemm_tflops"], 4),
+                       "a8_gemm_ms": round(t8, 4), "a8_quant_ms": round(tq, 4),
+                       "a8_gemm_tops": round(flops / t8 / 1e9, 1), "a8_op_tops": round(flops / (t8 + tq) / 1e9, 1),
+                       "a8_frac_int8_peak": round(flops / t8 / 1e9 / INT8_PEAK_TOPS, 4)}
+                if ceil.get("int8_gemm_tops"):
+                    rec["a8_frac_of_measured_int8_gemm"] = round(flops / t8 / 1e9 / ceil["int8_gemm_tops"], 4)
+                out.append(rec)
+                log(f"[prefill] {k}x{n} W{bits} m={m}: a16 {t16:.3f} ms {rec['a16_tflops']} TF, "
+                    f"a8 {t8:.3f}+{tq:.3f} ms {rec['a8_gemm_tops']} TOPS")
+                del x, y, x8, dx
+            del ws, w0
+            torch.cuda.empty_cache()
+    return {"workload": "70B-class prefill GEMMs, W3/W4 G128, bf16 activations N(0,1)", "rows": out}
+
+
+def decode_rows_sweep(torch, cq, ms=(1, 4, 16), bits=4, group=128):
+    """Llama-3-8B-shaped decode layers at M in {1, 4, 16}: the model-dtype
+    product and the Dynamic-A8 operator (quantizer + product), built-in
+    dispatch, weights rotated over more than 1 GiB; effective GB/s and the
+    fraction of the 8 TB/s HBM peak."""
+    from workloads import LLAMA8B_LAYERS, llama8b_act
+    out = []
+    for li, (name, k, n) in enumerate(LLAMA8B_LAYERS):
+        w0 = make_weight(cq, 2000 + li, n, k, bits, group, block_rows=1024)
+        ws = [w0] + [w0.clone() for _ in range(max(1, math.ceil((1 << 30) / w0.nbytes)))]
+        for m in ms:
+            x = torch.from_numpy(llama8b_act(m, k, li).view(np.int16)).cuda().view(torch.bfloat16)
+            y = torch.empty((m, n), dtype=torch.bfloat16, device="cuda")
+            x8 = torch.empty((m, k), dtype=torch.int8, device="cuda")
+            dx = torch.empty((m,), dtype=torch.float32, device="cuda")
+            a16 = lambda i: cq.cq_gemm_model_dtype(ws[i % len(ws)], x, out=y)
+            a8 = lambda i: (cq.cq_quantize_act_a8(x, x8, dx), cq.cq_gemm_a8(ws[i % len(ws)], x8, dx, out=y))
+            for i in range(len(ws)):
+                a16(i); a8(i)
+            torch.cuda.synchronize()
+            t16 = timed(torch, a16, 4 * len(ws))
+            t8 = timed(torch, a8, 4 * len(ws))
+            b16, b8 = a16_bytes(m, n, k, bits, group), a8_bytes(m, n, k, bits, group)
+            rec = {"layer": name, "k": k, "n": n, "m": m,
+                   "model_dtype_family": cq.cq_select_query(cq.CQ_PATH_MODEL_DTYPE, w0, m),
+                   "a8_family": cq.cq_select_query(cq.CQ_PATH_A8, w0, m),
+                   "model_dtype_us": round(t16 * 1e3, 2), "model_dtype_gbs": round(b16 / t16 / 1e6, 1),
+                   "model_dtype_hbm_frac": round(b16 / t16 / 1e6 / HBM_PEAK_GBS, 4),
+                   "a8_op_us": round(t8 * 1e3, 2), "a8_op_gbs": round(b8 / t8 / 1e6, 1),
+                   "a8_op_hbm_frac": round(b8 / t8 / 1e6 / HBM_PEAK_GBS, 4)}
+            out.append(rec)
+            log(f"[decode] {name} m={m}: model dtype {rec['model_dtype_us']} us ({rec['model_dtype_gbs']} GB/s), "
+                f"a8 {rec['a8_op_us']} us ({rec['a8_op_gbs']} GB/s)")
+            del x, y, x8, dx
+        del ws, w0
+        torch.cuda.empty_cache()
+    return {"workload": "Llama-3-8B-shaped decode layers, W4 G128, bf16 activations", "rows": out}
+
+
+def flushed_latency(torch, cq, trials=20, bits=4, group=128, k=4096, n=4096):
+    """Single-launch latency of the single-GEMV configuration (M = 1, K = N =
+    4096, W4 G128) after the caches are flushed by a 1 GiB streaming read:
+    HIP events around one launch, median over the trials."""
+    from workloads import gemv_4k
+    w = make_weight(cq, 1, n, k, bits, group)
+    xb, _ = gemv_4k()
+    x = torch.from_numpy(xb.view(np.int16)).cuda().view(torch.bfloat16)
+    y = torch.empty((1, n), dtype=torch.bfloat16, device="cuda")
+    flush = torch.ones((1 << 28,), dtype=torch.float32, device="cuda")
+    sink = torch.zeros((4,), dtype=torch.int32, device="cuda")
+    x8, dx = cq.cq_quantize_act_a8(x)
+    out = {}
+    for name, fn in (("model_dtype", lambda: cq.cq_gemm_model_dtype(w, x, out=y)),
+                     ("a8_gemv", lambda: cq.cq_gemm_a8(w, x8, dx, out=y))):
+        fn()
+        ts = []
+        for _ in range(trials):
+            cq.cq_probe_read(flush, sink)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e3)
+        out[name + "_us"] = round(float(np.median(ts)), 2)
+    out["note"] = ("one launch between HIP events after a 1 GiB read evicts the weights from L2 and the "
+                   "Infinity Cache; includes the launch latency")
+    del flush
+    return out
+
+
+# The paper's own kernel measurements (preliminary, NVIDIA H200, G512; Sec. 6,
+# the H200 kernel crossover): prior art on other hardware, not a target.
+PAPER_CONTEXT = {
+    "hardware": "NVIDIA H200 (the paper's preliminary kernel measurements), Cubic G512",
+    "status": "context only: other hardware, other group size; not a target",
+    "t_a16_over_t_a8": {
+        "shapes": "(N, K) = (3584, 3072) and (6144, 3584); >1 means Dynamic-A8 is faster",
+        "W2": {"1": "0.40-0.59", "16": "1.00-1.60", "64": "1.74-2.03", "256": "2.21-2.23"},
+        "W5": {"1": "0.78-0.87", "16": "1.62-2.60", "64": "2.94-3.16", "256": "3.35-3.93"},
+        "W8": {"1": "0.35-0.42", "16": "1.62-2.40", "64": "2.37-4.19", "256": "4.31-4.46"}},
+    "latency_ms_a16_a8": {
+        "shape": "(N, K) = (3584, 3072)",
+        "W2": {"1": [0.0184, 0.0461], "16": [0.0945, 0.0945], "64": [0.1653, 0.0950], "256": [0.5484, 0.2484]},
+        "W5": {"1": [0.0364, 0.0467], "16": [0.2658, 0.1642], "64": [0.4872, 0.1656], "256": [1.9521, 0.4965]},
+        "W8": {"1": [0.0171, 0.0489], "16": [0.2181, 0.1344], "64": [0.3950, 0.1670], "256": [1.5317, 0.3557]}},
+}
+
+
+def cpu_model():
+    """CPU model name of this host (from /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def fitted_timing(torch, cq, fitted_rep, bits=4, group=128, k=4096, n=4096):
+    """Model-dtype and A8 GEMV on the single-GEMV configuration with the
+    oracle-fitted weights against the seeded stand-in of the same shape
+    (rotated copies, weights from HBM): the kernels' time must not depend on
+    the code values."""
+    from workloads import gemv_4k
+    xb, _ = gemv_4k()
+    x = torch.from_numpy(xb.view(np.int16)).cuda().view(torch.bfloat16)
+    x8, dx = cq.cq_quantize_act_a8(x)
+    y = torch.empty((1, n), dtype=torch.bfloat16, device="cuda")
+    codes, s, a, b = fitted_rep
+    wf = cq.CQWeight.from_codes(codes, s, a, b, bits, group)
+    wsb = make_weight(cq, 1, n, k, bits, group)
+    out = {}
+    for name, w0 in (("fitted", wf), ("standin", wsb)):
+        ws = [w0] + [w0.clone() for _ in range(math.ceil((1 << 30) / w0.nbytes))]
+        for path, fn in (("model_dtype", lambda i: cq.cq_gemm_model_dtype(ws[i % len(ws)], x, out=y)),
+                         ("a8", lambda i: cq.cq_gemm_a8(ws[i % len(ws)], x8, dx, out=y))):
+            for i in range(len(ws)):
+                fn(i)
+            torch.cuda.synchronize()
+            out[f"{path}_{name}_us"] = round(timed(torch, fn, 4 * len(ws)) * 1e3, 2)
+        del ws
+    for path in ("model_dtype", "a8"):
+        out[f"{path}_fitted_over_standin"] = round(out[f"{path}_fitted_us"] / out[f"{path}_standin_us"], 3)
+    return out
+
+
+def profile_gemm(torch, cq, m, bits=4, group=128, k=8192, n=28672, calls=3):
+    """A few launches of both matrix-core GEMMs at m rows on the crossover
+    shape (for hardware-counter runs of the kernels alone)."""
+    from workloads import crossover_act
+    w = make_weight(cq, 4001, n, k, bits, group, block_rows=1024)
+    x = torch.from_numpy(crossover_act(m, k).view(np.int16)).cuda().view(torch.bfloat16)
+    x8, dx = cq.cq_quantize_act_a8(x)
+    y = torch.empty((m, n), dtype=torch.bfloat16, device="cuda")
+    for _ in range(calls):
+        cq.cq_gemm_model_dtype(w, x, out=y)
+        cq.cq_gemm_a8(w, x8, dx, out=y)
+    torch.cuda.synchronize()
+    return {"profiled": {"m": m, "k": k, "n": n, "bits": bits, "group": group, "calls": calls,
+                         "model_dtype_family": cq.cq_select_query(cq.CQ_PATH_MODEL_DTYPE, w, m),
+                         "a8_family": cq.cq_select_query(cq.CQ_PATH_A8, w, m)}}
 
 
 def measured_ceilings(torch):
@@ -363,6 +571,8 @@ def main():
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 256 MiB device copy (reference for HBM counters)")
+    ap.add_argument("--profile-gemm", type=int, default=0, metavar="M",
+                    help="only run a few launches of both matrix-core GEMMs at M rows (for counter runs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
@@ -373,6 +583,10 @@ def main():
     assert torch.cuda.is_available(), "needs a GPU"
     import paper_2608_06763_amd as cq
     from workloads import LLAMA8B_LAYERS, bf16_bits_to_f32, llama8b_act
+
+    if args.profile_gemm:
+        print(json.dumps(profile_gemm(torch, cq, args.profile_gemm)), flush=True)
+        return
 
     bits, group, m = 4, 128, 1
     log("[bench] building weights")
@@ -531,7 +745,14 @@ def main():
                      "frac_of_measured_hbm_read": round(achieved / ceil["hbm_read_gbs"], 4)},
         "measured_ceilings": ceil,
     }
+    result["paper_context"] = PAPER_CONTEXT
     if not args.no_sweep:
+        log("[bench] flushed single-launch latency")
+        result["single_launch_flushed"] = flushed_latency(torch, cq)
+        log("[bench] decode layers at M = 1, 4, 16")
+        result["decode_rows_sweep"] = decode_rows_sweep(torch, cq)
+        log("[bench] 70B-class prefill GEMMs")
+        result["prefill_sweep"] = prefill_sweep(torch, cq, ceil)
         log("[bench] rows sweep")
         result["rows_sweep"] = rows_sweep(torch, cq)
         for r in result["rows_sweep"]["rows"]:
@@ -547,6 +768,19 @@ def main():
         gpu_out = [(y16s[li].float().cpu().numpy().astype(np.float64), x8s[li].cpu().numpy(), dxs[li].cpu().numpy())
                    for li in range(nl)]
         result["cpu_baseline"] = cpu_baseline(layers_np, bits, group, gpu_out=gpu_out)
+        # the same leg fits the single-GEMV configuration's weights with the
+        # oracle (offline work, timed on its own) and times both GEMVs on them
+        # against the seeded stand-in the benchmark uses elsewhere
+        from oracle import fit as FIT
+        from workloads import gemv_4k
+        _, w_fit = gemv_4k()
+        t0 = time.perf_counter()
+        fr = FIT.fit(w_fit, bits, group)
+        fit_s = time.perf_counter() - t0
+        log(f"[bench] oracle fit of the 4096x4096 weights: {fit_s:.1f} s")
+        result["cpu_baseline"]["fitted_weights"] = {
+            "fit_s": round(fit_s, 2), "what": "oracle fit of the single-GEMV weights (4096 x 4096, W4 G128)",
+            **fitted_timing(torch, cq, (fr.codes, fr.scale, fr.a_bits, fr.b_bits))}
     print(json.dumps(result), flush=True)
 
 

@@ -206,11 +206,18 @@ PRINTED_SHAPES = ((1.0, 0.0), (0.7932, -0.3847), (0.5203, -0.2936), (0.8517, -0.
                   (0.6216, -0.1495), (0.7510, -0.5253), (0.4603, -0.3881))
 
 
-def synthetic_representation(seed: int, n: int, k: int, bits: int, group: int, scale_center: float = 0.05):
+def synthetic_representation(seed: int, n: int, k: int, bits: int, group: int, scale_center: float = 0.05,
+                             block_rows: int | None = None):
     """Random stand-in for a quantized matrix: codes drawn from a rounded
     Laplace law clipped to [-M, M], lognormal FP32 scales and shapes taken from
     PRINTED_SHAPES.  Kernel timing does not depend on the values, only on the
-    layout, so this serves timing runs that must not call the oracle."""
+    layout, so this serves timing runs that must not call the oracle.  With
+    block_rows, only that many rows are drawn and repeated down the matrix
+    (a faster stand-in for large timing matrices)."""
+    if block_rows is not None and block_rows < n:
+        parts = synthetic_representation(seed, block_rows, k, bits, group, scale_center)
+        reps = -(-n // block_rows)
+        return tuple(np.ascontiguousarray(np.tile(p, (reps, 1))[:n]) for p in parts)
     g = rng(seed)
     m = 1 if bits == 1 else (1 << (bits - 1)) - 1
     if bits == 1:
