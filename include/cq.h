@@ -386,16 +386,6 @@ cq_status cq_select_set(const cq_select_entry *entries, int64_t count);
  */
 cq_status cq_select_query(int32_t path, const cq_weight *w, cq_dtype x_dtype, int64_t m, int32_t *family);
 
-/*
- * Measurement aid, not part of the method: read `bytes` of device memory at
- * `buf` once, as a plain streaming kernel, so that a benchmark can state the
- * HBM read ceiling its weight-streaming kernels are compared with.  buf is
- * 16-byte aligned and bytes a multiple of 16 (else CQ_ERR_ALIGN / CQ_ERR_ARG);
- * sink is a caller-owned device word the kernel writes only in a case that
- * does not arise for real data (it keeps the loads from being removed).
- */
-cq_status cq_probe_read(const void *buf, int64_t bytes, uint32_t *sink, void *stream);
-
 #ifdef __cplusplus
 }
 #endif

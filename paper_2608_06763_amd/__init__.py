@@ -10,7 +10,7 @@ Entry points (same names as the C ABI):
   cq_gemm_a8, cq_gemm_a8_fused, cq_build_carriers, cq_gemm_a8_carriers,
   cq_gemm_routed_model_dtype, cq_gemm_routed_model_dtype_noalloc, cq_set_gemv_max_rows, cq_get_gemv_max_rows,
   cq_family_supported, cq_gemm_model_dtype_family, cq_gemm_a8_family,
-  cq_select_set, cq_select_query, cq_probe_read (measurement aid)
+  cq_select_set, cq_select_query, cq_probe_read (measurement aid, include/cq_measure.h)
 The measured kernel-selection tuner that fills the selection table is in
 ``selection.py``.
 """

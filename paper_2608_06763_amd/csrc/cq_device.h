@@ -11,6 +11,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace cq {
 
 constexpr int kWave = 64;
@@ -132,17 +134,19 @@ __device__ __forceinline__ int exact_carrier(int i, int m, double a, double b) {
     return int(r);
 }
 
-// Compute units of the current device (cached per device id).
+// Compute units of the current device, cached per device id.  Host threads
+// may race to fill an entry; they store the same value through an atomic, so
+// the cache is free of data races.
 inline int device_cu_count() {
-    static int cus[64] = {0};
+    static std::atomic<int> cus[64];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (cus[dev] == 0) {
-        int v = 0;
+    int v = cus[dev].load(std::memory_order_relaxed);
+    if (v == 0) {
         if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
-        cus[dev] = v;
+        cus[dev].store(v, std::memory_order_relaxed);
     }
-    return cus[dev];
+    return v;
 }
 
 }  // namespace cq

@@ -7,6 +7,7 @@
 #include <vector>
 
 #include "../../include/cq.h"
+#include "../../include/cq_measure.h"
 
 namespace cq {
 

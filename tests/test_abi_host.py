@@ -1,6 +1,6 @@
 """Host-side checks of the C ABI (no GPU needed).
 
-The library must load and export every function ``include/cq.h`` declares;
+The library must load and export every function ``include/*.h`` declares;
 ``cq_pack_groups`` must equal the oracle's packer byte for byte and reject
 every invalid input the format forbids; device entry points must reject bad
 arguments on the host before touching a device.
@@ -18,13 +18,16 @@ from oracle import fit as FIT
 from oracle import format as F
 from workloads import small_weight
 
-HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "cq.h")
+INCLUDE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+HEADERS = sorted(os.path.join(INCLUDE, f) for f in os.listdir(INCLUDE) if f.endswith(".h"))
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(cq_[a-z0-9_]+)\s*\(", text)))
+    names = set()
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(cq_[a-z0-9_]+)\s*\(", text))
+    return sorted(names)
 
 
 def test_library_exports_every_declared_symbol():
