@@ -311,6 +311,11 @@ int64_t cq_get_gemv_max_rows(int32_t path);
  *                 the selection in Sec. 5.6).  GEMM_MFMA picks the smallest of
  *                 32, 64, 128 that holds m, else 256 (an A8 partials dump
  *                 always runs the 256-row tile).  Same widths as GEMM_MFMA.
+ *   GEMM_SLAB     model dtype only, 1 <= m <= 32, B <= 5: matrix-core GEMM for
+ *                 few rows in which every lane decodes its codes straight into
+ *                 its own MFMA operand (no decoded tile in LDS, no barrier in
+ *                 the K loop) and the waves of a workgroup split K; numerics
+ *                 as GEMM_MFMA (hi + lo BF16 operand, FP32 accumulation).
  * Families that read 32-bit buffer offsets also need tensors below 2 GiB.
  */
 typedef enum { CQ_PATH_MODEL_DTYPE = 0, CQ_PATH_A8 = 1 } cq_path;
@@ -326,7 +331,8 @@ typedef enum {
     CQ_FAMILY_GEMM_MFMA_M32 = 8,
     CQ_FAMILY_GEMM_MFMA_M64 = 9,
     CQ_FAMILY_GEMM_MFMA_M128 = 10,
-    CQ_FAMILY_GEMM_MFMA_M256 = 11
+    CQ_FAMILY_GEMM_MFMA_M256 = 11,
+    CQ_FAMILY_GEMM_SLAB = 12
 } cq_family;
 
 /*
@@ -365,8 +371,8 @@ typedef struct {
 /*
  * Replace the process-wide table with a copy of entries[0 .. count) (count 0
  * clears it).  Host only.  CQ_ERR_ARG, with the previous table kept, if an
- * entry is malformed (unknown path or family, CQ_FAMILY_AUTO, the LUT or
- * ROUNDED family on the A8 path, bits outside 1..8, a group that is not a multiple of 32 in
+ * entry is malformed (unknown path or family, CQ_FAMILY_AUTO, the LUT,
+ * ROUNDED or SLAB family on the A8 path, bits outside 1..8, a group that is not a multiple of 32 in
  * 32..512, n or k < 1, m_lo < 1 or m_hi < m_lo, a bad x_dtype, reserved != 0)
  * or if two entries of the same path, shape and dtype overlap in m; count
  * above 65536 is CQ_ERR_ARG too.  With overlaps rejected, at most one entry

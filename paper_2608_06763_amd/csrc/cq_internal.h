@@ -48,6 +48,14 @@ hipError_t launch_gemm_a16_mfma(const cq_weight &w, const void *x, int x_dt, int
 hipError_t launch_gemm_a16_mfma_rounded(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                                         hipStream_t stream);
 
+// Model-dtype GEMM for few rows (1 <= m <= kSlabMaxRows, B <= 5) that decodes
+// each weight into the matrix-core operand of the decoding lane, with split-K
+// over the waves of a workgroup.
+constexpr int64_t kSlabMaxRows = 32;
+bool gemm_a16_slab_supported(const cq_weight &w, int64_t m);
+hipError_t launch_gemm_a16_slab(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                                hipStream_t stream);
+
 // Dynamic-A8 activation quantizer.
 hipError_t launch_quant_a8(const void *x, int x_dt, int64_t m, int64_t k, int8_t *x8, float *dx,
                            hipStream_t stream);

@@ -1,0 +1,410 @@
+// Model-dtype GEMM for few rows of x (Sec. 5.3 dense tactic, in the regime of
+// Sec. 5.5 between the single-row GEMV and the tiled GEMM) for B <= 5 on gfx950
+// matrix cores, with every weight decoded straight into the matrix-core
+// operand of the lane that decoded it: no decoded tile goes through LDS and
+// the K loop has no barrier.
+//
+// Numerics: every weight is reconstructed in FP32 as s_g sign(k) q(|k|/M)
+// (eq. cubic in the Horner form of eq. gpu-horner, q(1) = 1) and carried as
+// the unevaluated sum hi + lo of two numbers in the activation dtype (hi =
+// RNE(v), lo = RNE(v - hi)); both halves go through the matrix core into one
+// FP32 accumulator (v_mfma_f32_16x16x32_{bf16,f16}), as in the tiled GEMM's
+// BF16 default.
+//
+// Mapping.  A wave owns BJ blocks of 16 weight rows and 16 BI rows of x.  In
+// the 16x16x32 MFMA, lane l supplies column l % 16 of B and row l % 16 of A,
+// each with the K slots 8 (l / 16) .. +7.  K is visited in sweeps of four
+// groups: during sweep j the lanes 16 q .. 16 q + 15 feed the slots 8 q .. +7
+// of each MFMA from group 4 j + q of their rows, 8 consecutive codes per
+// MFMA, so a sweep takes G / 8 MFMAs and each lane stays inside one group of
+// one weight row for the whole sweep.  A sum does not depend on the order of
+// its terms, and the activations are read in the same order.  Each lane thus
+// builds one table of the 2^B signed levels (hi | lo << 16) per group, in
+// its own LDS column (byte field * 256 + lane * 4 of its wave's slot: every
+// lane reads its own bank), and a code costs one address permute, one LDS
+// read and one of the two byte permutes that form the hi and lo operands.
+//
+// Split-K.  The S waves of a workgroup share its weight rows and take the
+// sweeps w, w + S, w + 2S, ...; their accumulators meet in LDS once at the
+// end.  Each wave requests the codes, activations and group metadata of a
+// chunk (four MFMAs) R chunks before it decodes it; every load is issued
+// unconditionally and in program order, so each wait is for the oldest slot.
+#pragma once
+
+#include "cq_device.h"
+#include "cq_internal.h"
+#include "stream_common.h"
+
+#include <type_traits>
+
+namespace cq {
+
+namespace a16_slab {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) uint32_t lds_u32;
+typedef __attribute__((address_space(3))) f32x4_t lds_f32x4;
+
+__device__ __forceinline__ uint32_t lds_ld(uint32_t a) { return *reinterpret_cast<const lds_u32 *>(uintptr_t(a)); }
+__device__ __forceinline__ void lds_st(uint32_t a, uint32_t v) { *reinterpret_cast<lds_u32 *>(uintptr_t(a)) = v; }
+
+template <int XDT>
+__device__ __forceinline__ f32x4_t mma(const u32x4 &a, const u32x4 &b, f32x4_t c) {
+    if constexpr (XDT == 0)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                       c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b),
+                                                      c, 0, 0, 0);
+}
+
+template <int P0, int PN, typename F>
+__device__ __forceinline__ void unroll_for(F &&f) {
+    if constexpr (P0 < PN) {
+        f(std::integral_constant<int, P0>{});
+        unroll_for<P0 + 1, PN>(f);
+    }
+}
+
+// vector-memory reads stay in program order (the wait before a ring slot is
+// used counts the loads issued after it)
+__device__ __forceinline__ void vmem_order() { __builtin_amdgcn_sched_barrier(0x78f); }
+
+__device__ __forceinline__ void wave_lds_fence() {
+    // one wavefront's LDS operations complete in issue order; only the
+    // compiler must not move them across this point
+    __asm__ __volatile__("" ::: "memory");
+    __builtin_amdgcn_wave_barrier();
+}
+
+// table entry of the FP32 weight v: (hi | lo << 16) in the activation dtype,
+// hi = RNE(v), lo = RNE(v - hi)
+template <int XDT>
+__device__ __forceinline__ uint32_t operand_entry(float v) {
+    if constexpr (XDT == 0) {
+        const __bf16 hi = __bf16(v);
+        const __bf16 lo = __bf16(v - float(hi));
+        return uint32_t(__builtin_bit_cast(uint16_t, hi)) | (uint32_t(__builtin_bit_cast(uint16_t, lo)) << 16);
+    } else {
+        const _Float16 hi = _Float16(v);
+        const _Float16 lo = _Float16(v - float(hi));
+        return uint32_t(__builtin_bit_cast(uint16_t, hi)) | (uint32_t(__builtin_bit_cast(uint16_t, lo)) << 16);
+    }
+}
+
+}  // namespace a16_slab
+
+template <int B, int UPG, int XDT, int YDT, int BI, int BJ, int R>
+__global__ void __launch_bounds__(1024) gemm_a16_slab(
+    const uint8_t *__restrict__ codes, const float *__restrict__ scale,
+    const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
+    int n, int k, const uint16_t *__restrict__ x, int m, void *__restrict__ y, int tiles_n) {
+    using namespace a16_slab;
+    constexpr int M = max_code(B);
+    constexpr int NE = 1 << B;                // table fields
+    constexpr int G = 32 * UPG;
+    constexpr bool SPLIT = true;
+    constexpr uint32_t kTab = NE * 256u;      // bytes of one lane-column table set
+    constexpr uint32_t kNeg = 0x80008000u;
+    constexpr int PER = R > UPG ? R : UPG;    // chunks per unrolled period
+    static_assert(PER % R == 0 && PER % UPG == 0, "ring depth and chunks per group nest");
+    extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+    const int nw = blockDim.x >> 6;
+    const int nl = lane & 15, q = lane >> 4;
+    const int tm = blockIdx.x / tiles_n, tn = blockIdx.x - tm * tiles_n;
+    const int m0 = tm * 16 * BI, n0 = tn * 16 * BJ;
+
+    const int ng = k / G;
+    const int nsw = (ng + 3) >> 2;            // sweeps of four groups
+    const int mysw = wave < nsw ? (nsw - 1 - wave) / nw + 1 : 0;
+    const int nch = mysw * UPG;               // chunks of this wave
+    const uint32_t row_bytes = uint32_t(k) * B / 8u;
+    const auto rc = make_rsrc(codes, uint32_t(n) * row_bytes);
+    const auto rs = make_rsrc(scale, uint32_t(n) * ng * 4u);
+    const auto ra = make_rsrc(a16, uint32_t(n) * ng * 2u);
+    const auto rb = make_rsrc(b16, uint32_t(n) * ng * 2u);
+    const auto rx = make_rsrc(x, uint32_t(m) * uint32_t(k) * 2u);
+
+    // this lane's table columns (one per weight-row block)
+    const uint32_t tbase = uint32_t(uintptr_t((lds_u32 *)lds));
+    const uint32_t col0 = tbase + uint32_t(wave * BJ) * kTab + uint32_t(lane) * 4u;
+
+    // ring of R chunk slots
+    uint32_t cw[R][BJ][B];
+    uint32_t xw[R][BI][16];
+    float sv[R][BJ];
+    uint32_t av[R][BJ], bv[R][BJ];
+
+    // chunk c of this wave: sweep wave + nw (c / UPG), unit c % UPG of the group
+    auto load_slot = [&](int c, auto slot_c, auto meta_c) {
+        constexpr int SL = decltype(slot_c)::value;
+        constexpr bool META = decltype(meta_c)::value;
+        const int sw = wave + nw * (c / UPG);
+        const int u = c % UPG;
+        const int g = 4 * sw + q;
+        const bool gok = g < ng;
+#pragma unroll
+        for (int j = 0; j < BJ; ++j) {
+            const int row = n0 + 16 * j + nl;
+            const bool ok = gok && row < n;
+            const uint32_t gi = uint32_t(row) * uint32_t(ng) + uint32_t(g);
+            load_words<B>(rc, ok ? uint32_t(row) * row_bytes + (uint32_t(g) * UPG + uint32_t(u)) * (4u * B) : kOobOffset,
+                          cw[SL][j]);
+            if constexpr (META) {
+                sv[SL][j] = load_f32(rs, ok ? gi * 4u : kOobOffset);
+                av[SL][j] = load_u16(ra, ok ? gi * 2u : kOobOffset);
+                bv[SL][j] = load_u16(rb, ok ? gi * 2u : kOobOffset);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < BI; ++i) {
+            const int row = m0 + 16 * i + nl;
+            const bool ok = gok && row < m;
+            load_words<16>(rx, ok ? (uint32_t(row) * uint32_t(k) + uint32_t(g) * G + uint32_t(u) * 32u) * 2u : kOobOffset,
+                           xw[SL][i]);
+        }
+    };
+
+    // fields that no group rewrites: the zero code and the reserved pattern
+    if constexpr (B >= 2) {
+#pragma unroll
+        for (int j = 0; j < BJ; ++j) {
+            lds_st(col0 + j * kTab, 0u);
+            lds_st(col0 + j * kTab + uint32_t(NE / 2) * 256u, 0u);
+        }
+    }
+
+    // the lane's tables for the group whose metadata sit in slot SL
+    auto build_tables = [&](auto slot_c) {
+        constexpr int SL = decltype(slot_c)::value;
+        wave_lds_fence();  // the previous group's reads are issued
+#pragma unroll
+        for (int j = 0; j < BJ; ++j) {
+            const uint32_t cj = col0 + j * kTab;
+            const float s = sv[SL][j];
+            const uint32_t es = operand_entry<XDT>(s);  // q(1) = 1
+            if constexpr (B == 1) {
+                lds_st(cj, es ^ kNeg);
+                lds_st(cj + 256u, es);
+            } else {
+                lds_st(cj + uint32_t(M) * 256u, es);
+                lds_st(cj + uint32_t(NE - M) * 256u, es ^ kNeg);
+                if constexpr (B >= 3) {
+                    const float a = f16_to_f32(uint16_t(av[SL][j]));
+                    const float b = f16_to_f32(uint16_t(bv[SL][j]));
+                    const float cc = 1.f - a - b;
+#pragma unroll
+                    for (int i = 1; i < M; ++i) {
+                        const float t = float(i) / float(M);
+                        const float qv = t * __builtin_fmaf(t, __builtin_fmaf(t, cc, b), a);
+                        const uint32_t e = operand_entry<XDT>(s * qv);
+                        lds_st(cj + uint32_t(i) * 256u, e);
+                        lds_st(cj + uint32_t(NE - i) * 256u, e ^ kNeg);
+                    }
+                }
+            }
+        }
+        wave_lds_fence();
+    };
+
+    f32x4_t acc[BI][BJ];
+#pragma unroll
+    for (int i = 0; i < BI; ++i)
+#pragma unroll
+        for (int j = 0; j < BJ; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    // the nibble mask sits in a vector register so that mask and slot tag
+    // fold into one v_and_or_b32
+    uint32_t nmask;
+    __asm__("v_mov_b32 %0, 0x0f0f0f0f" : "=v"(nmask));
+
+    // decode and multiply the chunk in slot SL
+    auto compute = [&](auto slot_c) {
+        constexpr int SL = decltype(slot_c)::value;
+#pragma unroll
+        for (int j = 0; j < BJ; ++j) {
+            const uint32_t cj = col0 + j * kTab;
+            uint32_t ent[32];
+            if constexpr (B == 4) {
+                // byte 1 of the address is (slot << 4) | field; bytes 0, 2, 3 come
+                // from the column (the tables end below 64 KB)
+                const uint32_t tag = uint32_t(wave * BJ + j) * 0x10101010u;
+#pragma unroll
+                for (int st = 0; st < 4; ++st) {
+                    const uint32_t wd = cw[SL][j][st];
+                    const uint32_t lo4 = (wd & nmask) | tag;
+                    const uint32_t hi4 = ((wd >> 4) & nmask) | tag;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const uint32_t sel = 0x03020000u | (uint32_t(4 + e / 2) << 8);
+                        ent[8 * st + e] = lds_ld(__builtin_amdgcn_perm((e & 1) ? hi4 : lo4, cj, sel));
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 32; ++e) {
+                    const int bit = e * B;
+                    const int wd = bit >> 5, sh = bit & 31;
+                    uint32_t v;
+                    if (sh + B <= 32) v = cw[SL][j][wd] >> sh;
+                    else v = __builtin_amdgcn_alignbit(cw[SL][j][wd + 1], cw[SL][j][wd], sh);
+                    ent[e] = lds_ld(((v & uint32_t(NE - 1)) << 8) + cj);
+                }
+            }
+#pragma unroll
+            for (int st = 0; st < 4; ++st) {
+                u32x4 bh, bl;
+#pragma unroll
+                for (int p = 0; p < 4; ++p) {
+                    bh[p] = __builtin_amdgcn_perm(ent[8 * st + 2 * p + 1], ent[8 * st + 2 * p], 0x05040100u);
+                    if constexpr (SPLIT)
+                        bl[p] = __builtin_amdgcn_perm(ent[8 * st + 2 * p + 1], ent[8 * st + 2 * p], 0x07060302u);
+                }
+#pragma unroll
+                for (int i = 0; i < BI; ++i) {
+                    const u32x4 af = u32x4{xw[SL][i][4 * st], xw[SL][i][4 * st + 1], xw[SL][i][4 * st + 2],
+                                           xw[SL][i][4 * st + 3]};
+                    acc[i][j] = mma<XDT>(af, bh, acc[i][j]);
+                    if constexpr (SPLIT) acc[i][j] = mma<XDT>(af, bl, acc[i][j]);
+                }
+            }
+        }
+    };
+
+    if (nch > 0) {
+        // prologue: chunks 0 .. R - 1 requested into their slots
+        unroll_for<0, R>([&](auto p_c) {
+            constexpr int P = decltype(p_c)::value;
+            load_slot(min(P, nch - 1), p_c, std::integral_constant<bool, P % UPG == 0>{});
+            vmem_order();
+        });
+        for (int c0 = 0; c0 < nch; c0 += PER) {
+            unroll_for<0, PER>([&](auto p_c) {
+                constexpr int P = decltype(p_c)::value;
+                constexpr int SL = P % R;
+                const int c = c0 + P;
+                if (c < nch) {
+                    if constexpr (P % UPG == 0) build_tables(std::integral_constant<int, SL>{});
+                    compute(std::integral_constant<int, SL>{});
+                }
+                // the slot just used receives chunk c + R
+                load_slot(min(c + R, nch - 1), std::integral_constant<int, SL>{},
+                          std::integral_constant<bool, (P + R) % UPG == 0>{});
+                vmem_order();
+            });
+        }
+    }
+
+    // ---- cross-wave sum and store
+    auto store_block = [&](int i, int j, const f32x4_t &v) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int row = m0 + 16 * i + 4 * q + e;
+            const int col = n0 + 16 * j + nl;
+            if (row < m && col < n) store_out<YDT>(y, int64_t(row) * n + col, v[e]);
+        }
+    };
+    if (nw == 1) {
+#pragma unroll
+        for (int i = 0; i < BI; ++i)
+#pragma unroll
+            for (int j = 0; j < BJ; ++j) store_block(i, j, acc[i][j]);
+        return;
+    }
+    __syncthreads();  // every wave is done with its tables
+    lds_f32x4 *red = reinterpret_cast<lds_f32x4 *>(uintptr_t(tbase));
+#pragma unroll
+    for (int i = 0; i < BI; ++i)
+#pragma unroll
+        for (int j = 0; j < BJ; ++j) red[((wave * BI + i) * BJ + j) * 64 + lane] = acc[i][j];
+    __syncthreads();
+    for (int blk = wave; blk < BI * BJ; blk += nw) {
+        f32x4_t v = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int w = 0; w < nw; ++w) v += red[(w * BI * BJ + blk) * 64 + lane];
+        store_block(blk / BJ, blk % BJ, v);
+    }
+}
+
+namespace a16_slab {
+
+template <int B, int UPG, int XDT, int YDT, int BI, int BJ>
+hipError_t slab_launch(const cq_weight &w, const void *x, int64_t m, void *y, hipStream_t stream) {
+    constexpr int R = 2;  // chunks in flight per wave
+    constexpr int NE = 1 << B;
+    const int64_t tiles_m = (m + 16 * BI - 1) / (16 * BI);
+    const int64_t tiles_n = (w.n + 16 * BJ - 1) / (16 * BJ);
+    const int64_t tiles = tiles_m * tiles_n;
+    if (tiles > 0x7fffffff) return hipErrorInvalidValue;
+    const int64_t ng = w.k / w.group;
+    const int64_t nsw = (ng + 3) / 4;
+    // waves per workgroup: enough for about four waves per SIMD over the
+    // chip, no more than there are sweeps, and table slots within 64 KB
+    int64_t s = int64_t(device_cu_count()) * 16 / tiles;
+    const int64_t smax = 65536 / (int64_t(BJ) * NE * 256);
+    if (s > smax) s = smax;
+    if (s > 16) s = 16;
+    if (s > nsw) s = nsw;
+    if (s < 1) s = 1;
+    const size_t tab = size_t(s) * BJ * NE * 256;
+    const size_t red = size_t(s) * BI * BJ * 1024;
+    const size_t lds = tab > red ? tab : red;
+    hipLaunchKernelGGL((gemm_a16_slab<B, UPG, XDT, YDT, BI, BJ, R>), dim3(unsigned(tiles)), dim3(unsigned(64 * s)),
+                       lds, stream, w.codes, w.scale, w.a, w.b, int(w.n), int(w.k), static_cast<const uint16_t *>(x),
+                       int(m), y, int(tiles_n));
+    return hipGetLastError();
+}
+
+template <int B, int XDT, int YDT, int BI, int BJ>
+hipError_t slab_group(const cq_weight &w, const void *x, int64_t m, void *y, hipStream_t stream) {
+    switch (w.group) {
+        case 32: return slab_launch<B, 1, XDT, YDT, BI, BJ>(w, x, m, y, stream);
+        case 64: return slab_launch<B, 2, XDT, YDT, BI, BJ>(w, x, m, y, stream);
+        case 128: return slab_launch<B, 4, XDT, YDT, BI, BJ>(w, x, m, y, stream);
+        case 256: return slab_launch<B, 8, XDT, YDT, BI, BJ>(w, x, m, y, stream);
+        case 512: return slab_launch<B, 16, XDT, YDT, BI, BJ>(w, x, m, y, stream);
+    }
+    return hipErrorNotSupported;
+}
+
+template <int XDT, int YDT, int BI, int BJ>
+hipError_t slab_bits(const cq_weight &w, const void *x, int64_t m, void *y, hipStream_t stream) {
+    switch (w.bits) {
+        case 1: return slab_group<1, XDT, YDT, BI, BJ>(w, x, m, y, stream);
+        case 2: return slab_group<2, XDT, YDT, BI, BJ>(w, x, m, y, stream);
+        case 3: return slab_group<3, XDT, YDT, BI, BJ>(w, x, m, y, stream);
+        case 4: return slab_group<4, XDT, YDT, BI, BJ>(w, x, m, y, stream);
+        case 5: return slab_group<5, XDT, YDT, BI, BJ>(w, x, m, y, stream);
+    }
+    return hipErrorNotSupported;
+}
+
+// every width, group and dtype pair of one (x-row blocks, weight-row blocks) shape
+template <int BI, int BJ>
+hipError_t slab_dtypes(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                       hipStream_t stream) {
+    if (x_dt == 0) {
+        if (y_dt == 0) return slab_bits<0, 0, BI, BJ>(w, x, m, y, stream);
+        return slab_bits<0, 2, BI, BJ>(w, x, m, y, stream);
+    }
+    if (y_dt == 1) return slab_bits<1, 1, BI, BJ>(w, x, m, y, stream);
+    return slab_bits<1, 2, BI, BJ>(w, x, m, y, stream);
+}
+
+}  // namespace a16_slab
+
+// one file per shape: 16 rows of x with 16 or 32 weight rows per wave, and
+// 32 rows of x with 16
+hipError_t launch_a16_slab_1x1(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                               hipStream_t stream);
+hipError_t launch_a16_slab_1x2(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                               hipStream_t stream);
+hipError_t launch_a16_slab_2x1(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                               hipStream_t stream);
+
+}  // namespace cq

@@ -1,0 +1,11 @@
+// Few-row model-dtype GEMM, 32 rows of x and 16 weight rows per wave.
+#include "gemm_a16_slab.h"
+
+namespace cq {
+
+hipError_t launch_a16_slab_2x1(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                               hipStream_t stream) {
+    return a16_slab::slab_dtypes<2, 1>(w, x, x_dt, m, y, y_dt, stream);
+}
+
+}  // namespace cq

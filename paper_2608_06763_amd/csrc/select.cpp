@@ -28,6 +28,7 @@ bool family_supported(int path, int family, const cq_weight &w, int64_t m) {
             case CQ_FAMILY_GEMM_MFMA_M64:
             case CQ_FAMILY_GEMM_MFMA_M128:
             case CQ_FAMILY_GEMM_MFMA_M256: return gemm_a16_mfma_supported(w, m);
+            case CQ_FAMILY_GEMM_SLAB: return gemm_a16_slab_supported(w, m);
         }
         return false;
     }
@@ -53,13 +54,18 @@ int default_family(int path, const cq_weight &w, int64_t m, int64_t gemv_max_row
     if (path == CQ_PATH_MODEL_DTYPE) {
         if (gemv) {
             if (gemv_a16_stream_supported(w, m)) return CQ_FAMILY_GEMV_STREAM;
-            // 2..4 rows: the table-decode family streams each weight once per
-            // row set with FP32 products and measured faster there; more rows
-            // go to the matrix-core narrow-row family
+            // 2..16 rows: the lane-decoded matrix-core GEMM measured faster
+            // than the table-decode and narrow-row families on every decode
+            // and crossover shape; B >= 6 keeps the GEMV families
+            if (gemm_a16_slab_supported(w, m)) return CQ_FAMILY_GEMM_SLAB;
             if (gemv_a16_lut_supported(w, m)) return CQ_FAMILY_GEMV_LUT;
             if (gemv_a16_narrow_supported(w, m)) return CQ_FAMILY_GEMV_NARROW;
             return CQ_FAMILY_GEMV_GENERIC;
         }
+        // 17..32 rows: the lane-decoded GEMM splits K over the waves of a
+        // workgroup, which the tiled GEMM lacks; it wins by 2-3x on layers
+        // of up to 14336 weight rows and ties on 28672 rows
+        if (m > kGemvMaxRows && w.n < 16384 && gemm_a16_slab_supported(w, m)) return CQ_FAMILY_GEMM_SLAB;
         return gemm_a16_mfma_supported(w, m) ? CQ_FAMILY_GEMM_MFMA : CQ_FAMILY_GEMM_TILED;
     }
     // Dynamic A8: a partials dump is written by the generic GEMV, the W4
@@ -87,6 +93,7 @@ hipError_t run_family_a16(int family, const cq_weight &w, const void *x, int x_d
         case CQ_FAMILY_GEMM_MFMA_M128:
         case CQ_FAMILY_GEMM_MFMA_M256:
             return launch_gemm_a16_mfma(w, x, x_dt, m, y, y_dt, family_tile_rows(family), stream);
+        case CQ_FAMILY_GEMM_SLAB: return launch_gemm_a16_slab(w, x, x_dt, m, y, y_dt, stream);
     }
     return hipErrorInvalidValue;
 }
@@ -160,8 +167,9 @@ int table_family(int path, const cq_weight &w, int x_dt, int64_t m) {
 
 bool select_entry_valid(const cq_select_entry &e) {
     if (e.path != CQ_PATH_MODEL_DTYPE && e.path != CQ_PATH_A8) return false;
-    if (e.family < CQ_FAMILY_GEMV_STREAM || e.family > CQ_FAMILY_GEMM_MFMA_M256) return false;
-    if (e.path == CQ_PATH_A8 && (e.family == CQ_FAMILY_GEMV_LUT || e.family == CQ_FAMILY_GEMM_MFMA_ROUNDED))
+    if (e.family < CQ_FAMILY_GEMV_STREAM || e.family > CQ_FAMILY_GEMM_SLAB) return false;
+    if (e.path == CQ_PATH_A8 && (e.family == CQ_FAMILY_GEMV_LUT || e.family == CQ_FAMILY_GEMM_MFMA_ROUNDED ||
+                                 e.family == CQ_FAMILY_GEMM_SLAB))
         return false;
     if (e.bits < 1 || e.bits > 8) return false;
     if (e.group < 32 || e.group > 512 || e.group % 32) return false;

@@ -244,15 +244,16 @@ def clean_table():
 
 @pytest.mark.parametrize("bits,group,m,md,a8", [
     (4, 128, 1, "gemv_stream", "gemv_stream"),
-    (4, 128, 3, "gemv_lut", "gemv_narrow"),
-    (4, 256, 3, "gemv_narrow", "gemv_narrow"),
-    (4, 128, 8, "gemv_narrow", "gemv_narrow"),
-    (4, 32, 8, "gemv_narrow", "gemv_generic"),
+    (4, 128, 3, "gemm_slab", "gemv_narrow"),
+    (4, 256, 3, "gemm_slab", "gemv_narrow"),
+    (4, 128, 8, "gemm_slab", "gemv_narrow"),
+    (4, 32, 8, "gemm_slab", "gemv_generic"),
     (3, 128, 1, "gemv_stream", "gemv_stream"),
-    (3, 128, 8, "gemv_narrow", "gemv_generic"),
+    (3, 128, 8, "gemm_slab", "gemv_generic"),
     (6, 128, 1, "gemv_stream", "gemv_generic"),
     (6, 128, 8, "gemv_generic", "gemv_generic"),
-    (4, 128, 17, "gemm_mfma", "gemm_mfma"),
+    (4, 128, 17, "gemm_slab", "gemm_mfma"),
+    (4, 128, 33, "gemm_mfma", "gemm_mfma"),
     (3, 64, 300, "gemm_mfma", "gemm_mfma"),
     (3, 32, 300, "gemm_mfma", "gemm_tiled"),
     (6, 128, 300, "gemm_tiled", "gemm_tiled"),
@@ -269,6 +270,7 @@ def test_builtin_rules_follow_gemv_threshold(clean_table):
     d = _fake(4, 128, 4096, 4096)
     cq.cq_set_gemv_max_rows(0, 0)
     assert cq.cq_select_query(cq.CQ_PATH_MODEL_DTYPE, d, 1) == "gemm_mfma"
+    assert cq.cq_select_query(cq.CQ_PATH_MODEL_DTYPE, _fake(4, 128, 28672, 4096), 24) == "gemm_mfma"
     assert cq.cq_select_query(cq.CQ_PATH_A8, d, 1) == "gemv_stream"
 
 
@@ -283,6 +285,9 @@ def test_family_predicates():
     assert cq.cq_family_supported(md, "gemm_mfma", d, 1)
     assert cq.cq_family_supported(md, "gemm_mfma_rounded", d, 1)
     assert not cq.cq_family_supported(a8, "gemm_mfma_rounded", d, 300)
+    assert cq.cq_family_supported(md, "gemm_slab", d, 1) and cq.cq_family_supported(md, "gemm_slab", d, 32)
+    assert not cq.cq_family_supported(md, "gemm_slab", d, 33)
+    assert not cq.cq_family_supported(a8, "gemm_slab", d, 8)
     assert not cq.cq_family_supported(a8, "gemv_lut", d, 2)
     assert not cq.cq_family_supported(a8, "auto", d, 2)
     assert not cq.cq_family_supported(7, "gemm_tiled", d, 2)
@@ -325,7 +330,7 @@ def test_table_overrides_and_falls_back(clean_table):
     assert cq.cq_select_query(md, d, 1) == "gemv_stream"
     assert cq.cq_select_query(md, d, 2) == "gemv_narrow"
     cq.cq_select_set([])
-    assert cq.cq_select_query(md, d, 4) == "gemv_lut"
+    assert cq.cq_select_query(md, d, 4) == "gemm_slab"
 
 
 def test_table_matches_activation_dtype(clean_table):
@@ -336,8 +341,8 @@ def test_table_matches_activation_dtype(clean_table):
 
 
 @pytest.mark.parametrize("bad", [
-    dict(path=2), dict(family="auto"), dict(family=12), dict(path=1, family="gemv_lut"),
-    dict(path=1, family="gemm_mfma_rounded"), dict(bits=0),
+    dict(path=2), dict(family="auto"), dict(family=13), dict(path=1, family="gemv_lut"),
+    dict(path=1, family="gemm_mfma_rounded"), dict(path=1, family="gemm_slab"), dict(bits=0),
     dict(bits=9), dict(group=48), dict(group=1024), dict(n=0), dict(k=0), dict(m_lo=0), dict(m_lo=5, m_hi=4),
     dict(x_dtype=2), dict(path=1, x_dtype=0)])
 def test_table_rejects_malformed_entries(clean_table, bad):

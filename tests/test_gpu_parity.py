@@ -650,7 +650,7 @@ def test_gemm_a8_carriers_equals_gemm_a8(torch_dev, bits, group, m):
 
 # ---------------------------------------------------------------- kernel families and the selection table
 
-MD_FAMILIES = ("gemv_stream", "gemv_lut", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_mfma_m32",
+MD_FAMILIES = ("gemv_stream", "gemv_lut", "gemv_narrow", "gemv_generic", "gemm_slab", "gemm_mfma", "gemm_mfma_m32",
                "gemm_mfma_m64", "gemm_mfma_m128", "gemm_mfma_m256", "gemm_tiled", "gemm_mfma_rounded")
 A8_FAMILIES = ("gemv_stream", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_mfma_m32", "gemm_mfma_m64",
                "gemm_mfma_m128", "gemm_mfma_m256", "gemm_tiled")
@@ -722,6 +722,58 @@ def test_gemm_tile_heights_bit_equal(torch_dev, m):
     for o in outs[1:]:
         assert torch_dev.equal(o, outs[0])
     assert R.eps_comp(_np(outs[0]), y_ref, "fp32") <= 2e-4
+
+
+# ---------------------------------------------------------------- few-row GEMM with lane-decoded operands
+
+
+@pytest.mark.parametrize("bits", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("group,k", [(32, 640), (64, 640), (128, 640), (256, 1280), (512, 2560)])
+@pytest.mark.parametrize("m", [1, 7, 17, 32])
+def test_gemm_slab(torch_dev, bits, group, k, m):
+    # five groups per row (a last sweep with one group of four), 83 weight rows
+    # (a ragged 16-row block), one and two x-row blocks; FP32 and BF16 outputs
+    n = 83
+    r = fitted(360 + bits, n, k, bits, group)
+    w = _weight(r, bits, group)
+    xb, xv = act(361 + m, m, k)
+    y_ref = ref_model_dtype(xv, r, bits, group)
+    cq = _cq()
+    x = _x(torch_dev, xb, "bf16")
+    say("gemm_slab", bits, group, k, m)
+    y = cq.cq_gemm_model_dtype_family(w, x, "gemm_slab", y_dtype=torch_dev.float32)
+    assert R.eps_comp(_np(y), y_ref, "fp32") <= 2e-4
+    y16 = cq.cq_gemm_model_dtype_family(w, x, "gemm_slab")
+    assert R.eps_comp(_np(y16), y_ref, "bf16") <= TOL
+
+
+@pytest.mark.parametrize("n,k,m", [(40, 8192, 5), (300, 4096, 32), (16, 1024, 1), (1024, 4096, 16)])
+def test_gemm_slab_split_k_and_fp16(torch_dev, n, k, m):
+    # few weight rows over long K: up to 16 waves per workgroup split K and
+    # meet in LDS.  FP16 activations take one FP16 operand, the weight rounded
+    # once to FP16 (relative error <= 2^-11, absolute 2^-25 below the normal
+    # range), held to that rounding's elementwise bound and to the FP16 output bar
+    bits, group = 4, 128
+    r = fitted(370, n, k, bits, group)
+    w = _weight(r, bits, group)
+    cq = _cq()
+    for dtype in ("bf16", "fp16"):
+        xb, xv = act(371 + m, m, k, dtype)
+        y_ref = ref_model_dtype(xv, r, bits, group)
+        say("gemm_slab split-k", n, k, m, dtype)
+        y = cq.cq_gemm_model_dtype_family(w, _x(torch_dev, xb, dtype), "gemm_slab", y_dtype=torch_dev.float32)
+        if dtype == "bf16":
+            assert R.eps_comp(_np(y), y_ref, "fp32") <= 2e-4
+        else:
+            wabs = np.abs(F.decode(r.codes, bits, group, r.scale, r.a_bits, r.b_bits))
+            xabs = np.abs(xv)
+            bound = (2.0 ** -11 * (xabs @ wabs.T) * (1 + 2e-3) + 2.0 ** -25 * xabs.sum(axis=1, keepdims=True)
+                     + 1e-6 * np.max(np.abs(y_ref)))
+            assert np.all(np.abs(_np(y).astype(np.float64) - y_ref) <= bound)
+            y16 = cq.cq_gemm_model_dtype_family(w, _x(torch_dev, xb, dtype), "gemm_slab")
+            assert R.eps_comp(_np(y16), y_ref, "fp16") <= TOL
+        y2 = cq.cq_gemm_model_dtype_family(w, _x(torch_dev, xb, dtype), "gemm_slab", y_dtype=torch_dev.float32)
+        assert torch_dev.equal(y, y2)
 
 
 @pytest.mark.parametrize("bits,group", [(4, 128), (3, 64), (4, 512), (3, 256)])
