@@ -315,7 +315,14 @@ int64_t cq_get_gemv_max_rows(int32_t path);
  *                 few rows in which every lane decodes its codes straight into
  *                 its own MFMA operand (no decoded tile in LDS, no barrier in
  *                 the K loop) and the waves of a workgroup split K; numerics
- *                 as GEMM_MFMA (hi + lo BF16 operand, FP32 accumulation).
+ *                 as GEMM_MFMA (hi + lo operand in the activation dtype, FP32
+ *                 accumulation).
+ *   GEMM_SLAB_STAGED  model dtype only, 1 <= m <= 16, G <= 128, G B <= 512,
+ *                 K / G a multiple of 4: GEMM_SLAB whose waves each take a
+ *                 contiguous K range and bring codes and group metadata in
+ *                 through LDS with whole-cache-line loads; same numerics.
+ *                 The built-in rules pick it when the K split gives the waves
+ *                 two or more sweeps of four groups each.
  * Families that read 32-bit buffer offsets also need tensors below 2 GiB.
  */
 typedef enum { CQ_PATH_MODEL_DTYPE = 0, CQ_PATH_A8 = 1 } cq_path;
@@ -332,7 +339,8 @@ typedef enum {
     CQ_FAMILY_GEMM_MFMA_M64 = 9,
     CQ_FAMILY_GEMM_MFMA_M128 = 10,
     CQ_FAMILY_GEMM_MFMA_M256 = 11,
-    CQ_FAMILY_GEMM_SLAB = 12
+    CQ_FAMILY_GEMM_SLAB = 12,
+    CQ_FAMILY_GEMM_SLAB_STAGED = 13
 } cq_family;
 
 /*
@@ -372,7 +380,7 @@ typedef struct {
  * Replace the process-wide table with a copy of entries[0 .. count) (count 0
  * clears it).  Host only.  CQ_ERR_ARG, with the previous table kept, if an
  * entry is malformed (unknown path or family, CQ_FAMILY_AUTO, the LUT,
- * ROUNDED or SLAB family on the A8 path, bits outside 1..8, a group that is not a multiple of 32 in
+ * ROUNDED or either SLAB family on the A8 path, bits outside 1..8, a group that is not a multiple of 32 in
  * 32..512, n or k < 1, m_lo < 1 or m_hi < m_lo, a bad x_dtype, reserved != 0)
  * or if two entries of the same path, shape and dtype overlap in m; count
  * above 65536 is CQ_ERR_ARG too.  With overlaps rejected, at most one entry

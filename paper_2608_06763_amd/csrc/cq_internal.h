@@ -55,6 +55,13 @@ constexpr int64_t kSlabMaxRows = 32;
 bool gemm_a16_slab_supported(const cq_weight &w, int64_t m);
 hipError_t launch_gemm_a16_slab(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                                 hipStream_t stream);
+// The staged variant (codes and metadata through LDS, contiguous K per wave)
+// and the built-in preference for it: the waves of the K split get two or
+// more sweeps each (host only, sized for 256 compute units).
+bool gemm_a16_slab_staged_supported(const cq_weight &w, int64_t m);
+bool gemm_a16_slab_staged_preferred(const cq_weight &w, int64_t m);
+hipError_t launch_gemm_a16_slab_staged(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                                       hipStream_t stream);
 
 // Dynamic-A8 activation quantizer.
 hipError_t launch_quant_a8(const void *x, int x_dt, int64_t m, int64_t k, int8_t *x8, float *dx,

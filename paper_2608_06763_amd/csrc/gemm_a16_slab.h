@@ -331,6 +331,279 @@ __global__ void __launch_bounds__(1024) gemm_a16_slab(
     }
 }
 
+// Staged variant for up to 16 rows of x and 16 weight rows per wave.  The
+// mapping of lanes to MFMA slots, the K order and the tables are those above;
+// what changes is how codes and group metadata reach a lane.  A lane's own
+// slice of the weights (16 B of one group of one row per chunk) lies apart
+// from its neighbours', so loading it directly touches many cache lines per
+// wave load.  Here each wave takes a contiguous range of sweeps and, per
+// sweep, loads the 16 rows' code bytes of the sweep's four groups as runs of
+// whole cache lines (a row's bytes of one sweep are contiguous), writes them
+// to its own LDS staging area and reads each lane's slice back from there;
+// the group metadata of four sweeps (16 groups per row) are loaded the same
+// way once per four sweeps.  Only the wave itself touches its staging area,
+// so program order orders the writes and reads.  Requires a multiple of four
+// groups per row and at most 512 code bytes per row and sweep.
+template <int B, int UPG, int XDT, int YDT>
+__global__ void __launch_bounds__(1024) gemm_a16_slab_st(
+    const uint8_t *__restrict__ codes, const float *__restrict__ scale,
+    const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
+    int n, int k, const uint16_t *__restrict__ x, int m, void *__restrict__ y, int tiles_n) {
+    using namespace a16_slab;
+    typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
+    typedef __attribute__((address_space(3))) float lds_f32;
+    constexpr int M = max_code(B);
+    constexpr int NE = 1 << B;
+    constexpr int G = 32 * UPG;
+    constexpr int GB = G * B / 8;             // code bytes of one group of a row
+    constexpr int SEG = 4 * GB;               // ... of one sweep
+    constexpr int P = SEG / 16;               // 16-byte pieces of a row per sweep
+    constexpr int T = (16 * P + 63) / 64;     // wave loads per sweep
+    constexpr uint32_t CS = SEG + 16;         // staged row stride (bytes)
+    constexpr int NB = 4;                     // sweeps per metadata batch
+    constexpr uint32_t kTab = NE * 256u;
+    constexpr uint32_t kMeta = 16u * NB * 16u;  // one metadata array of a batch (bytes)
+    constexpr uint32_t kStage = 16u * CS + 2u * kMeta;
+    constexpr uint32_t kNeg = 0x80008000u;
+    static_assert(SEG % 16 == 0 && SEG <= 512, "staged sweep size");
+    extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+    const int nw = blockDim.x >> 6;
+    const int nl = lane & 15, q = lane >> 4;
+    const int tm = blockIdx.x / tiles_n, tn = blockIdx.x - tm * tiles_n;
+    const int m0 = tm * 16, n0 = tn * 16;
+
+    const int ng = k / G;                     // a multiple of 4
+    const int nsw = ng >> 2;
+    const int per = (nsw + nw - 1) / nw;      // contiguous sweeps per wave
+    const int sa = min(wave * per, nsw);
+    const int sb = min(sa + per, nsw);
+    const int nmy = sb - sa;
+    const int nch = nmy * UPG;
+    const uint32_t row_bytes = uint32_t(k) * B / 8u;
+    const auto rc = make_rsrc(codes, uint32_t(n) * row_bytes);
+    const auto rs = make_rsrc(scale, uint32_t(n) * ng * 4u);
+    const auto ra = make_rsrc(a16, uint32_t(n) * ng * 2u);
+    const auto rb = make_rsrc(b16, uint32_t(n) * ng * 2u);
+    const auto rx = make_rsrc(x, uint32_t(m) * uint32_t(k) * 2u);
+
+    // LDS: the tables of all waves (below 64 KB, for the W4 address build),
+    // then one staging area per wave
+    const uint32_t tbase = uint32_t(uintptr_t((lds_u32 *)lds));
+    const uint32_t col = tbase + uint32_t(wave) * kTab + uint32_t(lane) * 4u;
+    const uint32_t stg = tbase + uint32_t(nw) * kTab + uint32_t(wave) * kStage;
+    const uint32_t mst = stg + 16u * CS;      // batch scales [row][sweep][group]
+    const uint32_t mab = mst + kMeta;         // batch a | b << 16, same layout
+
+    uint32_t cr[T][4];                        // codes of one sweep as loaded
+    uint32_t ms4[4], ma2[2], mb2[2];          // metadata of one batch as loaded
+    uint32_t xw[2][16];                       // activations of two chunks
+
+    // codes of sweep sw (out-of-range sweeps and rows read zeros)
+    auto load_codes = [&](int sw) {
+        const bool ok = sw < sb;
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+            const int f = 64 * t + lane;
+            const int r = f / P, p = f - r * P;
+            const bool okr = ok && r < 16 && n0 + r < n;
+            load_words<4>(rc, okr ? uint32_t(n0 + r) * row_bytes + uint32_t(sw) * SEG + uint32_t(p) * 16u : kOobOffset,
+                          cr[t]);
+        }
+    };
+    auto store_codes = [&]() {
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+            const int f = 64 * t + lane;
+            const int r = f / P, p = f - r * P;
+            if ((16 * P) % 64 == 0 || r < 16)
+                *reinterpret_cast<lds_u32x4 *>(uintptr_t(stg + uint32_t(r) * CS + uint32_t(p) * 16u)) =
+                    u32x4{cr[t][0], cr[t][1], cr[t][2], cr[t][3]};
+        }
+    };
+    // batch bi (sweeps sa + 4 bi .. + 3): lane L holds the four groups of
+    // sweep sa + 4 bi + L % 4 of row L / 4
+    auto load_meta = [&](int bi) {
+        const int r = lane >> 2;
+        const int sw = sa + NB * bi + (lane & 3);
+        const bool ok = sw < sb && n0 + r < n;
+        const uint32_t gi = uint32_t(n0 + r) * uint32_t(ng) + 4u * uint32_t(sw);
+        load_words<4>(rs, ok ? gi * 4u : kOobOffset, ms4);
+        load_words<2>(ra, ok ? gi * 2u : kOobOffset, ma2);
+        load_words<2>(rb, ok ? gi * 2u : kOobOffset, mb2);
+    };
+    auto store_meta = [&]() {
+        const uint32_t o = uint32_t(lane) * 16u;  // [row][sweep of batch][group]
+        *reinterpret_cast<lds_u32x4 *>(uintptr_t(mst + o)) = u32x4{ms4[0], ms4[1], ms4[2], ms4[3]};
+        *reinterpret_cast<lds_u32x4 *>(uintptr_t(mab + o)) =
+            u32x4{__builtin_amdgcn_perm(mb2[0], ma2[0], 0x05040100u), __builtin_amdgcn_perm(mb2[0], ma2[0], 0x07060302u),
+                  __builtin_amdgcn_perm(mb2[1], ma2[1], 0x05040100u), __builtin_amdgcn_perm(mb2[1], ma2[1], 0x07060302u)};
+    };
+    // activations of chunk c (sweep sa + c / UPG, unit c % UPG of the lane's group)
+    auto load_x = [&](int c, auto slot_c) {
+        constexpr int SL = decltype(slot_c)::value;
+        const int sw = sa + c / UPG, u = c % UPG;
+        const int row = m0 + nl;
+        const bool ok = row < m && sw < sb;
+        load_words<16>(rx, ok ? (uint32_t(row) * uint32_t(k) + uint32_t(4 * sw + q) * G + uint32_t(u) * 32u) * 2u
+                              : kOobOffset,
+                       xw[SL]);
+    };
+
+    // the lane's table for its group of sweep i of the wave (batch slot i % NB)
+    auto build_table = [&](int j) {
+        wave_lds_fence();  // staged metadata written, previous group's reads issued
+        const uint32_t o = (uint32_t(nl) * NB + uint32_t(j)) * 16u + uint32_t(q) * 4u;
+        const float s = *reinterpret_cast<const lds_f32 *>(uintptr_t(mst + o));
+        const uint32_t ab = lds_ld(mab + o);
+        const uint32_t es = operand_entry<XDT>(s);
+        if constexpr (B == 1) {
+            lds_st(col, es ^ kNeg);
+            lds_st(col + 256u, es);
+        } else {
+            lds_st(col + uint32_t(M) * 256u, es);
+            lds_st(col + uint32_t(NE - M) * 256u, es ^ kNeg);
+            if constexpr (B >= 3) {
+                const float a = f16_to_f32(uint16_t(ab & 0xffffu));
+                const float b = f16_to_f32(uint16_t(ab >> 16));
+                const float cc = 1.f - a - b;
+#pragma unroll
+                for (int i = 1; i < M; ++i) {
+                    const float t = float(i) / float(M);
+                    const float qv = t * __builtin_fmaf(t, __builtin_fmaf(t, cc, b), a);
+                    const uint32_t e = operand_entry<XDT>(s * qv);
+                    lds_st(col + uint32_t(i) * 256u, e);
+                    lds_st(col + uint32_t(NE - i) * 256u, e ^ kNeg);
+                }
+            }
+        }
+        wave_lds_fence();
+    };
+
+    uint32_t nmask;
+    __asm__("v_mov_b32 %0, 0x0f0f0f0f" : "=v"(nmask));
+    const uint32_t tag = uint32_t(wave) * 0x10101010u;
+    f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    // decode unit u of the staged sweep and multiply with activation slot SL
+    auto compute = [&](int u, auto slot_c) {
+        constexpr int SL = decltype(slot_c)::value;
+        const uint32_t ca = stg + uint32_t(nl) * CS + uint32_t(q) * GB + uint32_t(u) * (4u * B);
+        uint32_t cw[B];
+        if constexpr (B == 4) {
+            const u32x4 v = *reinterpret_cast<const lds_u32x4 *>(uintptr_t(ca));
+            cw[0] = v[0]; cw[1] = v[1]; cw[2] = v[2]; cw[3] = v[3];
+        } else {
+#pragma unroll
+            for (int e = 0; e < B; ++e) cw[e] = lds_ld(ca + 4u * e);
+        }
+        uint32_t ent[32];
+        if constexpr (B == 4) {
+#pragma unroll
+            for (int st = 0; st < 4; ++st) {
+                const uint32_t lo4 = (cw[st] & nmask) | tag;
+                const uint32_t hi4 = ((cw[st] >> 4) & nmask) | tag;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const uint32_t sel = 0x03020000u | (uint32_t(4 + e / 2) << 8);
+                    ent[8 * st + e] = lds_ld(__builtin_amdgcn_perm((e & 1) ? hi4 : lo4, col, sel));
+                }
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < 32; ++e) {
+                const int bit = e * B;
+                const int wd = bit >> 5, sh = bit & 31;
+                uint32_t v;
+                if (sh + B <= 32) v = cw[wd] >> sh;
+                else v = __builtin_amdgcn_alignbit(cw[wd + 1], cw[wd], sh);
+                ent[e] = lds_ld(((v & uint32_t(NE - 1)) << 8) + col);
+            }
+        }
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+            u32x4 bh, bl;
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                bh[p] = __builtin_amdgcn_perm(ent[8 * st + 2 * p + 1], ent[8 * st + 2 * p], 0x05040100u);
+                bl[p] = __builtin_amdgcn_perm(ent[8 * st + 2 * p + 1], ent[8 * st + 2 * p], 0x07060302u);
+            }
+            const u32x4 af = u32x4{xw[SL][4 * st], xw[SL][4 * st + 1], xw[SL][4 * st + 2], xw[SL][4 * st + 3]};
+            acc = mma<XDT>(af, bh, acc);
+            acc = mma<XDT>(af, bl, acc);
+        }
+    };
+
+    if (nmy > 0) {
+        if constexpr (B >= 2) {
+            lds_st(col, 0u);
+            lds_st(col + uint32_t(NE / 2) * 256u, 0u);
+        }
+        // prologue: metadata of batch 0, codes of the first sweep, activations of chunks 0 and 1
+        load_meta(0);
+        vmem_order();
+        load_codes(sa);
+        vmem_order();
+        load_x(0, std::integral_constant<int, 0>{});
+        load_x(min(1, nch - 1), std::integral_constant<int, 1>{});
+        vmem_order();
+        // one period: a metadata batch of NB sweeps of UPG chunks each
+        for (int i0 = 0; i0 < nmy; i0 += NB) {
+            unroll_for<0, NB>([&](auto j_c) {
+                constexpr int J = decltype(j_c)::value;
+                const int i = i0 + J;
+                const bool active = i < nmy;
+                if constexpr (J == 0) {
+                    store_meta();
+                    load_meta(i0 / NB + 1);
+                    vmem_order();
+                }
+                if (active) {
+                    store_codes();
+                    build_table(J);
+                }
+                unroll_for<0, UPG>([&](auto u_c) {
+                    constexpr int U = decltype(u_c)::value;
+                    constexpr int SL = (J * UPG + U) % 2;
+                    const int c = i * UPG + U;
+                    if (active) compute(U, std::integral_constant<int, SL>{});
+                    load_x(min(c + 2, nch - 1), std::integral_constant<int, SL>{});
+                    vmem_order();
+                    if constexpr (U == 0) {
+                        load_codes(sa + i + 1);
+                        vmem_order();
+                    }
+                });
+            });
+        }
+    }
+
+    // ---- cross-wave sum and store
+    auto store_block = [&](const f32x4_t &v) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int row = m0 + 4 * q + e;
+            const int cl = n0 + nl;
+            if (row < m && cl < n) store_out<YDT>(y, int64_t(row) * n + cl, v[e]);
+        }
+    };
+    if (nw == 1) {
+        store_block(acc);
+        return;
+    }
+    __syncthreads();
+    lds_f32x4 *red = reinterpret_cast<lds_f32x4 *>(uintptr_t(tbase));
+    red[wave * 64 + lane] = acc;
+    __syncthreads();
+    if (wave == 0) {
+        f32x4_t v = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int w = 0; w < nw; ++w) v += red[w * 64 + lane];
+        store_block(v);
+    }
+}
+
 namespace a16_slab {
 
 template <int B, int UPG, int XDT, int YDT, int BI, int BJ>
@@ -384,6 +657,56 @@ hipError_t slab_bits(const cq_weight &w, const void *x, int64_t m, void *y, hipS
     return hipErrorNotSupported;
 }
 
+
+// staged variant: groups of at most 128 codes with at most 256 code bytes per
+// row and sweep (larger ones spill registers in the unrolled sweep loop)
+template <int B, int UPG, int XDT, int YDT>
+hipError_t slab_st_launch(const cq_weight &w, const void *x, int64_t m, void *y, hipStream_t stream) {
+    constexpr int NE = 1 << B;
+    constexpr uint32_t kTab = NE * 256u;
+    constexpr uint32_t CS = 4 * (32 * UPG) * B / 8 + 16;
+    constexpr uint32_t kStage = 16u * CS + 2u * 16u * 4u * 16u;
+    const int64_t tiles_n = (w.n + 15) / 16;
+    const int64_t tiles = (m + 15) / 16 * tiles_n;
+    if (tiles > 0x7fffffff) return hipErrorInvalidValue;
+    const int64_t nsw = w.k / w.group / 4;
+    int64_t s = int64_t(device_cu_count()) * 16 / tiles;
+    if (s > 16) s = 16;
+    if (s > nsw) s = nsw;
+    // LDS: tables below 64 KB, whole workgroup within 128 KB
+    while (s > 1 && (s * kTab > 65536 || s * (kTab + kStage) > 131072)) --s;
+    if (s < 1) s = 1;
+    const size_t lds = size_t(s) * (kTab + kStage) > size_t(s) * 1024 ? size_t(s) * (kTab + kStage) : size_t(s) * 1024;
+    hipLaunchKernelGGL((gemm_a16_slab_st<B, UPG, XDT, YDT>), dim3(unsigned(tiles)), dim3(unsigned(64 * s)), lds,
+                       stream, w.codes, w.scale, w.a, w.b, int(w.n), int(w.k), static_cast<const uint16_t *>(x), int(m),
+                       y, int(tiles_n));
+    return hipGetLastError();
+}
+
+template <int B, int XDT, int YDT>
+hipError_t slab_st_group(const cq_weight &w, const void *x, int64_t m, void *y, hipStream_t stream) {
+    switch (w.group) {
+        case 32: return slab_st_launch<B, 1, XDT, YDT>(w, x, m, y, stream);
+        case 64: return slab_st_launch<B, 2, XDT, YDT>(w, x, m, y, stream);
+        case 128:
+            if constexpr (B <= 4) return slab_st_launch<B, 4, XDT, YDT>(w, x, m, y, stream);
+            break;
+    }
+    return hipErrorNotSupported;
+}
+
+template <int XDT, int YDT>
+hipError_t slab_st_bits(const cq_weight &w, const void *x, int64_t m, void *y, hipStream_t stream) {
+    switch (w.bits) {
+        case 1: return slab_st_group<1, XDT, YDT>(w, x, m, y, stream);
+        case 2: return slab_st_group<2, XDT, YDT>(w, x, m, y, stream);
+        case 3: return slab_st_group<3, XDT, YDT>(w, x, m, y, stream);
+        case 4: return slab_st_group<4, XDT, YDT>(w, x, m, y, stream);
+        case 5: return slab_st_group<5, XDT, YDT>(w, x, m, y, stream);
+    }
+    return hipErrorNotSupported;
+}
+
 // every width, group and dtype pair of one (x-row blocks, weight-row blocks) shape
 template <int BI, int BJ>
 hipError_t slab_dtypes(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
@@ -406,5 +729,9 @@ hipError_t launch_a16_slab_1x2(const cq_weight &w, const void *x, int x_dt, int6
                                hipStream_t stream);
 hipError_t launch_a16_slab_2x1(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                                hipStream_t stream);
+// the staged variant (m <= 16, G <= 128, G B <= 512, a multiple of four groups per row)
+bool a16_slab_st_fits(const cq_weight &w, int64_t m);
+hipError_t launch_a16_slab_st(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                              hipStream_t stream);
 
 }  // namespace cq

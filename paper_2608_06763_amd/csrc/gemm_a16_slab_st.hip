@@ -1,0 +1,41 @@
+// Few-row model-dtype GEMM, staged variant (16 rows of x, 16 weight rows per wave).
+#include "gemm_a16_slab.h"
+
+namespace cq {
+
+bool a16_slab_st_fits(const cq_weight &w, int64_t m) {
+    return m <= 16 && w.bits <= 5 && w.group <= 128 && w.group * w.bits <= 512 && (w.k / w.group) % 4 == 0;
+}
+
+bool gemm_a16_slab_staged_supported(const cq_weight &w, int64_t m) {
+    return gemm_a16_slab_supported(w, m) && a16_slab_st_fits(w, m);
+}
+
+bool gemm_a16_slab_staged_preferred(const cq_weight &w, int64_t m) {
+    if (!gemm_a16_slab_staged_supported(w, m)) return false;
+    // the launch's split of K: about 16 waves per compute unit over the chip
+    const int64_t tiles = (w.n + 15) / 16 * ((m + 15) / 16);
+    int64_t s = int64_t(256) * 16 / tiles;
+    if (s > 16) s = 16;
+    if (s < 1) s = 1;
+    const int64_t nsw = w.k / w.group / 4;
+    return (nsw + s - 1) / s >= 2;
+}
+
+hipError_t launch_gemm_a16_slab_staged(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                                       hipStream_t stream) {
+    return launch_a16_slab_st(w, x, x_dt, m, y, y_dt, stream);
+}
+
+hipError_t launch_a16_slab_st(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
+                              hipStream_t stream) {
+    using namespace a16_slab;
+    if (x_dt == 0) {
+        if (y_dt == 0) return slab_st_bits<0, 0>(w, x, m, y, stream);
+        return slab_st_bits<0, 2>(w, x, m, y, stream);
+    }
+    if (y_dt == 1) return slab_st_bits<1, 1>(w, x, m, y, stream);
+    return slab_st_bits<1, 2>(w, x, m, y, stream);
+}
+
+}  // namespace cq

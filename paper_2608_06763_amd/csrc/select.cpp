@@ -29,6 +29,7 @@ bool family_supported(int path, int family, const cq_weight &w, int64_t m) {
             case CQ_FAMILY_GEMM_MFMA_M128:
             case CQ_FAMILY_GEMM_MFMA_M256: return gemm_a16_mfma_supported(w, m);
             case CQ_FAMILY_GEMM_SLAB: return gemm_a16_slab_supported(w, m);
+            case CQ_FAMILY_GEMM_SLAB_STAGED: return gemm_a16_slab_staged_supported(w, m);
         }
         return false;
     }
@@ -56,7 +57,9 @@ int default_family(int path, const cq_weight &w, int64_t m, int64_t gemv_max_row
             if (gemv_a16_stream_supported(w, m)) return CQ_FAMILY_GEMV_STREAM;
             // 2..16 rows: the lane-decoded matrix-core GEMM measured faster
             // than the table-decode and narrow-row families on every decode
-            // and crossover shape; B >= 6 keeps the GEMV families
+            // and crossover shape, staged when each wave gets at least two
+            // sweeps; B >= 6 keeps the GEMV families
+            if (gemm_a16_slab_staged_preferred(w, m)) return CQ_FAMILY_GEMM_SLAB_STAGED;
             if (gemm_a16_slab_supported(w, m)) return CQ_FAMILY_GEMM_SLAB;
             if (gemv_a16_lut_supported(w, m)) return CQ_FAMILY_GEMV_LUT;
             if (gemv_a16_narrow_supported(w, m)) return CQ_FAMILY_GEMV_NARROW;
@@ -94,6 +97,7 @@ hipError_t run_family_a16(int family, const cq_weight &w, const void *x, int x_d
         case CQ_FAMILY_GEMM_MFMA_M256:
             return launch_gemm_a16_mfma(w, x, x_dt, m, y, y_dt, family_tile_rows(family), stream);
         case CQ_FAMILY_GEMM_SLAB: return launch_gemm_a16_slab(w, x, x_dt, m, y, y_dt, stream);
+        case CQ_FAMILY_GEMM_SLAB_STAGED: return launch_gemm_a16_slab_staged(w, x, x_dt, m, y, y_dt, stream);
     }
     return hipErrorInvalidValue;
 }
@@ -167,9 +171,9 @@ int table_family(int path, const cq_weight &w, int x_dt, int64_t m) {
 
 bool select_entry_valid(const cq_select_entry &e) {
     if (e.path != CQ_PATH_MODEL_DTYPE && e.path != CQ_PATH_A8) return false;
-    if (e.family < CQ_FAMILY_GEMV_STREAM || e.family > CQ_FAMILY_GEMM_SLAB) return false;
+    if (e.family < CQ_FAMILY_GEMV_STREAM || e.family > CQ_FAMILY_GEMM_SLAB_STAGED) return false;
     if (e.path == CQ_PATH_A8 && (e.family == CQ_FAMILY_GEMV_LUT || e.family == CQ_FAMILY_GEMM_MFMA_ROUNDED ||
-                                 e.family == CQ_FAMILY_GEMM_SLAB))
+                                 e.family == CQ_FAMILY_GEMM_SLAB || e.family == CQ_FAMILY_GEMM_SLAB_STAGED))
         return false;
     if (e.bits < 1 || e.bits > 8) return false;
     if (e.group < 32 || e.group > 512 || e.group % 32) return false;

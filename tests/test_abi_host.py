@@ -247,13 +247,14 @@ def clean_table():
     (4, 128, 3, "gemm_slab", "gemv_narrow"),
     (4, 256, 3, "gemm_slab", "gemv_narrow"),
     (4, 128, 8, "gemm_slab", "gemv_narrow"),
-    (4, 32, 8, "gemm_slab", "gemv_generic"),
+    (4, 32, 8, "gemm_slab_staged", "gemv_generic"),
     (3, 128, 1, "gemv_stream", "gemv_stream"),
     (3, 128, 8, "gemm_slab", "gemv_generic"),
     (6, 128, 1, "gemv_stream", "gemv_generic"),
     (6, 128, 8, "gemv_generic", "gemv_generic"),
     (4, 128, 17, "gemm_slab", "gemm_mfma"),
     (4, 128, 33, "gemm_mfma", "gemm_mfma"),
+    (4, 128, 4, "gemm_slab", "gemv_narrow"),
     (3, 64, 300, "gemm_mfma", "gemm_mfma"),
     (3, 32, 300, "gemm_mfma", "gemm_tiled"),
     (6, 128, 300, "gemm_tiled", "gemm_tiled"),
@@ -264,6 +265,15 @@ def test_builtin_rules(clean_table, bits, group, m, md, a8):
     assert cq.cq_select_query(cq.CQ_PATH_A8, d, m) == a8
     assert cq.cq_family_supported(cq.CQ_PATH_MODEL_DTYPE, md, d, m)
     assert cq.cq_family_supported(cq.CQ_PATH_A8, a8, d, m)
+
+
+@pytest.mark.parametrize("n,k,m,want", [
+    (28672, 8192, 4, "gemm_slab_staged"), (28672, 4096, 16, "gemm_slab_staged"), (4096, 14336, 2, "gemm_slab_staged"),
+    (6144, 4096, 4, "gemm_slab"), (4096, 4096, 8, "gemm_slab"), (28672, 8192, 1, "gemv_stream"),
+    (28672, 8192, 24, "gemm_mfma")])
+def test_builtin_slab_variant(clean_table, n, k, m, want):
+    # the staged variant when every wave of the K split gets two sweeps
+    assert cq.cq_select_query(cq.CQ_PATH_MODEL_DTYPE, _fake(4, 128, n, k), m) == want
 
 
 def test_builtin_rules_follow_gemv_threshold(clean_table):
@@ -288,6 +298,11 @@ def test_family_predicates():
     assert cq.cq_family_supported(md, "gemm_slab", d, 1) and cq.cq_family_supported(md, "gemm_slab", d, 32)
     assert not cq.cq_family_supported(md, "gemm_slab", d, 33)
     assert not cq.cq_family_supported(a8, "gemm_slab", d, 8)
+    assert cq.cq_family_supported(md, "gemm_slab_staged", d, 16)
+    assert not cq.cq_family_supported(md, "gemm_slab_staged", d, 17)
+    assert not cq.cq_family_supported(md, "gemm_slab_staged", _fake(4, 256, 4096, 4096), 2)
+    assert not cq.cq_family_supported(md, "gemm_slab_staged", _fake(4, 128, 4096, 640), 2)
+    assert not cq.cq_family_supported(a8, "gemm_slab_staged", d, 8)
     assert not cq.cq_family_supported(a8, "gemv_lut", d, 2)
     assert not cq.cq_family_supported(a8, "auto", d, 2)
     assert not cq.cq_family_supported(7, "gemm_tiled", d, 2)
@@ -341,8 +356,9 @@ def test_table_matches_activation_dtype(clean_table):
 
 
 @pytest.mark.parametrize("bad", [
-    dict(path=2), dict(family="auto"), dict(family=13), dict(path=1, family="gemv_lut"),
-    dict(path=1, family="gemm_mfma_rounded"), dict(path=1, family="gemm_slab"), dict(bits=0),
+    dict(path=2), dict(family="auto"), dict(family=14), dict(path=1, family="gemv_lut"),
+    dict(path=1, family="gemm_mfma_rounded"), dict(path=1, family="gemm_slab"),
+    dict(path=1, family="gemm_slab_staged"), dict(bits=0),
     dict(bits=9), dict(group=48), dict(group=1024), dict(n=0), dict(k=0), dict(m_lo=0), dict(m_lo=5, m_hi=4),
     dict(x_dtype=2), dict(path=1, x_dtype=0)])
 def test_table_rejects_malformed_entries(clean_table, bad):
