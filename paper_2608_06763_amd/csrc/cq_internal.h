@@ -62,6 +62,12 @@ bool gemm_a16_slab_staged_supported(const cq_weight &w, int64_t m);
 bool gemm_a16_slab_staged_preferred(const cq_weight &w, int64_t m);
 hipError_t launch_gemm_a16_slab_staged(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                                        hipStream_t stream);
+// Its routed form: one workgroup per (expert, 16 weight rows) over the grouped
+// route list, 16 routes at a time (G <= 128, G B <= 512, K / G a multiple of 4).
+bool gemm_a16_slab_routed_supported(const cq_weight &w, int64_t tokens);
+hipError_t launch_gemm_a16_slab_routed(const cq_weight &w, int n_experts, const void *x, int x_dt, int64_t tokens,
+                                       const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
+                                       int y_dt, hipStream_t stream);
 
 // Dynamic-A8 activation quantizer.
 hipError_t launch_quant_a8(const void *x, int x_dt, int64_t m, int64_t k, int8_t *x8, float *dx,

@@ -344,11 +344,17 @@ __global__ void __launch_bounds__(1024) gemm_a16_slab(
 // way once per four sweeps.  Only the wave itself touches its staging area,
 // so program order orders the writes and reads.  Requires a multiple of four
 // groups per row and at most 512 code bytes per row and sweep.
-template <int B, int UPG, int XDT, int YDT>
-__global__ void __launch_bounds__(1024) gemm_a16_slab_st(
+//
+// ROUTED: a bank of experts of n weight rows each, stacked; workgroup
+// (e, 16 weight rows) serves every route of expert e that the grouping pass
+// listed (rorder[roff[e] .. roff[e + 1])), 16 routes at a time: a route's x
+// row is its token and its output is row `route` of y.
+template <int B, int UPG, int XDT, int YDT, bool ROUTED>
+__global__ void __launch_bounds__(ROUTED ? 512 : 1024) gemm_a16_slab_st(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
-    int n, int k, const uint16_t *__restrict__ x, int m, void *__restrict__ y, int tiles_n) {
+    int n, int k, const uint16_t *__restrict__ x, int m, void *__restrict__ y, int tiles_n,
+    const int32_t *__restrict__ rtok, const int32_t *__restrict__ rorder, const int32_t *__restrict__ roff) {
     using namespace a16_slab;
     typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
     typedef __attribute__((address_space(3))) float lds_f32;
@@ -373,16 +379,30 @@ __global__ void __launch_bounds__(1024) gemm_a16_slab_st(
     const int nw = blockDim.x >> 6;
     const int nl = lane & 15, q = lane >> 4;
     const int tm = blockIdx.x / tiles_n, tn = blockIdx.x - tm * tiles_n;
-    const int m0 = tm * 16, n0 = tn * 16;
-
+    const int n0 = tn * 16;
     const int ng = k / G;                     // a multiple of 4
+    const uint32_t row_bytes = uint32_t(k) * B / 8u;
+    // rows of x served by this workgroup, 16 at a time: rows tm * 16 .. + 15,
+    // or (routed: tm is the expert) the expert's routes, whose x rows are their
+    // tokens and whose outputs are rows of y in route order
+    int c_begin, c_end;
+    if constexpr (ROUTED) {
+        c_begin = roff[tm];
+        c_end = roff[tm + 1];
+        codes += size_t(tm) * n * row_bytes;
+        scale += size_t(tm) * n * ng;
+        a16 += size_t(tm) * n * ng;
+        b16 += size_t(tm) * n * ng;
+    } else {
+        c_begin = tm * 16;
+        c_end = min(c_begin + 16, m);
+    }
     const int nsw = ng >> 2;
     const int per = (nsw + nw - 1) / nw;      // contiguous sweeps per wave
     const int sa = min(wave * per, nsw);
     const int sb = min(sa + per, nsw);
     const int nmy = sb - sa;
     const int nch = nmy * UPG;
-    const uint32_t row_bytes = uint32_t(k) * B / 8u;
     const auto rc = make_rsrc(codes, uint32_t(n) * row_bytes);
     const auto rs = make_rsrc(scale, uint32_t(n) * ng * 4u);
     const auto ra = make_rsrc(a16, uint32_t(n) * ng * 2u);
@@ -441,12 +461,14 @@ __global__ void __launch_bounds__(1024) gemm_a16_slab_st(
             u32x4{__builtin_amdgcn_perm(mb2[0], ma2[0], 0x05040100u), __builtin_amdgcn_perm(mb2[0], ma2[0], 0x07060302u),
                   __builtin_amdgcn_perm(mb2[1], ma2[1], 0x05040100u), __builtin_amdgcn_perm(mb2[1], ma2[1], 0x07060302u)};
     };
+    // x row of this lane's MFMA row in the current 16 rows (-1: none)
+    int xr = -1;
     // activations of chunk c (sweep sa + c / UPG, unit c % UPG of the lane's group)
     auto load_x = [&](int c, auto slot_c) {
         constexpr int SL = decltype(slot_c)::value;
         const int sw = sa + c / UPG, u = c % UPG;
-        const int row = m0 + nl;
-        const bool ok = row < m && sw < sb;
+        const int row = xr;
+        const bool ok = row >= 0 && sw < sb;
         load_words<16>(rx, ok ? (uint32_t(row) * uint32_t(k) + uint32_t(4 * sw + q) * G + uint32_t(u) * 32u) * 2u
                               : kOobOffset,
                        xw[SL]);
@@ -485,7 +507,7 @@ __global__ void __launch_bounds__(1024) gemm_a16_slab_st(
     uint32_t nmask;
     __asm__("v_mov_b32 %0, 0x0f0f0f0f" : "=v"(nmask));
     const uint32_t tag = uint32_t(wave) * 0x10101010u;
-    f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    f32x4_t acc;
 
     // decode unit u of the staged sweep and multiply with activation slot SL
     auto compute = [&](int u, auto slot_c) {
@@ -536,6 +558,10 @@ __global__ void __launch_bounds__(1024) gemm_a16_slab_st(
         }
     };
 
+  for (int c0 = c_begin; c0 < c_end; c0 += 16) {
+    if constexpr (ROUTED) xr = c0 + nl < c_end ? rtok[rorder[c0 + nl]] : -1;
+    else xr = c0 + nl < c_end ? c0 + nl : -1;
+    acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
     if (nmy > 0) {
         if constexpr (B >= 2) {
             lds_st(col, 0u);
@@ -584,14 +610,17 @@ __global__ void __launch_bounds__(1024) gemm_a16_slab_st(
     auto store_block = [&](const f32x4_t &v) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const int row = m0 + 4 * q + e;
+            const int rr = c0 + 4 * q + e;
             const int cl = n0 + nl;
-            if (row < m && cl < n) store_out<YDT>(y, int64_t(row) * n + cl, v[e]);
+            if (rr < c_end && cl < n) {
+                const int row = ROUTED ? rorder[rr] : rr;
+                store_out<YDT>(y, int64_t(row) * n + cl, v[e]);
+            }
         }
     };
     if (nw == 1) {
         store_block(acc);
-        return;
+        continue;
     }
     __syncthreads();
     lds_f32x4 *red = reinterpret_cast<lds_f32x4 *>(uintptr_t(tbase));
@@ -602,6 +631,8 @@ __global__ void __launch_bounds__(1024) gemm_a16_slab_st(
         for (int w = 0; w < nw; ++w) v += red[w * 64 + lane];
         store_block(v);
     }
+    __syncthreads();  // the sums are read before the next rows' tables reuse the space
+  }
 }
 
 namespace a16_slab {
@@ -677,9 +708,34 @@ hipError_t slab_st_launch(const cq_weight &w, const void *x, int64_t m, void *y,
     while (s > 1 && (s * kTab > 65536 || s * (kTab + kStage) > 131072)) --s;
     if (s < 1) s = 1;
     const size_t lds = size_t(s) * (kTab + kStage) > size_t(s) * 1024 ? size_t(s) * (kTab + kStage) : size_t(s) * 1024;
-    hipLaunchKernelGGL((gemm_a16_slab_st<B, UPG, XDT, YDT>), dim3(unsigned(tiles)), dim3(unsigned(64 * s)), lds,
-                       stream, w.codes, w.scale, w.a, w.b, int(w.n), int(w.k), static_cast<const uint16_t *>(x), int(m),
-                       y, int(tiles_n));
+    hipLaunchKernelGGL((gemm_a16_slab_st<B, UPG, XDT, YDT, false>), dim3(unsigned(tiles)), dim3(unsigned(64 * s)),
+                       lds, stream, w.codes, w.scale, w.a, w.b, int(w.n), int(w.k), static_cast<const uint16_t *>(x),
+                       int(m), y, int(tiles_n), nullptr, nullptr, nullptr);
+    return hipGetLastError();
+}
+
+// routed: one workgroup per (expert, 16 weight rows); route chunks of 16
+template <int B, int UPG, int XDT, int YDT>
+hipError_t slab_st_routed_launch(const cq_weight &w, int n_experts, const void *x, int64_t tokens,
+                                 const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
+                                 hipStream_t stream) {
+    constexpr int NE = 1 << B;
+    constexpr uint32_t kTab = NE * 256u;
+    constexpr uint32_t CS = 4 * (32 * UPG) * B / 8 + 16;
+    constexpr uint32_t kStage = 16u * CS + 2u * 16u * 4u * 16u;
+    const int64_t tiles_n = (w.n + 15) / 16;
+    const int64_t blocks = tiles_n * n_experts;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    const int64_t nsw = w.k / w.group / 4;
+    int64_t s = int64_t(device_cu_count()) * 16 / blocks;
+    if (s > 8) s = 8;  // the routed kernel's launch bound
+    if (s > nsw) s = nsw;
+    while (s > 1 && (s * kTab > 65536 || s * (kTab + kStage) > 131072)) --s;
+    if (s < 1) s = 1;
+    const size_t lds = size_t(s) * (kTab + kStage) > size_t(s) * 1024 ? size_t(s) * (kTab + kStage) : size_t(s) * 1024;
+    hipLaunchKernelGGL((gemm_a16_slab_st<B, UPG, XDT, YDT, true>), dim3(unsigned(blocks)), dim3(unsigned(64 * s)),
+                       lds, stream, w.codes, w.scale, w.a, w.b, int(w.n), int(w.k), static_cast<const uint16_t *>(x),
+                       int(tokens), y, int(tiles_n), token, order, offsets);
     return hipGetLastError();
 }
 
@@ -691,6 +747,35 @@ hipError_t slab_st_group(const cq_weight &w, const void *x, int64_t m, void *y, 
         case 128:
             if constexpr (B <= 4) return slab_st_launch<B, 4, XDT, YDT>(w, x, m, y, stream);
             break;
+    }
+    return hipErrorNotSupported;
+}
+
+template <int B, int XDT, int YDT>
+hipError_t slab_st_routed_group(const cq_weight &w, int n_experts, const void *x, int64_t tokens,
+                                const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
+                                hipStream_t stream) {
+    switch (w.group) {
+        case 32: return slab_st_routed_launch<B, 1, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        case 64: return slab_st_routed_launch<B, 2, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        case 128:
+            if constexpr (B <= 4)
+                return slab_st_routed_launch<B, 4, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+            break;
+    }
+    return hipErrorNotSupported;
+}
+
+template <int XDT, int YDT>
+hipError_t slab_st_routed_bits(const cq_weight &w, int n_experts, const void *x, int64_t tokens,
+                               const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
+                               hipStream_t stream) {
+    switch (w.bits) {
+        case 1: return slab_st_routed_group<1, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        case 2: return slab_st_routed_group<2, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        case 3: return slab_st_routed_group<3, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        case 4: return slab_st_routed_group<4, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        case 5: return slab_st_routed_group<5, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
     }
     return hipErrorNotSupported;
 }

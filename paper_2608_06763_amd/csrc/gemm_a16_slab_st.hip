@@ -27,6 +27,23 @@ hipError_t launch_gemm_a16_slab_staged(const cq_weight &w, const void *x, int x_
     return launch_a16_slab_st(w, x, x_dt, m, y, y_dt, stream);
 }
 
+bool gemm_a16_slab_routed_supported(const cq_weight &w, int64_t tokens) {
+    return w.bits <= 5 && w.group <= 128 && w.group * w.bits <= 512 && (w.k / w.group) % 4 == 0 &&
+           stream_fits(w.n, w.k, w.bits, w.group) && tokens * w.k * 2 < (int64_t(1) << 31);
+}
+
+hipError_t launch_gemm_a16_slab_routed(const cq_weight &w, int n_experts, const void *x, int x_dt, int64_t tokens,
+                                       const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
+                                       int y_dt, hipStream_t stream) {
+    using namespace a16_slab;
+    if (x_dt == 0) {
+        if (y_dt == 0) return slab_st_routed_bits<0, 0>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        return slab_st_routed_bits<0, 2>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+    }
+    if (y_dt == 1) return slab_st_routed_bits<1, 1>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+    return slab_st_routed_bits<1, 2>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+}
+
 hipError_t launch_a16_slab_st(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                               hipStream_t stream) {
     using namespace a16_slab;

@@ -84,11 +84,13 @@ bool routed_supported(const cq_weight &w, int64_t n_experts, int64_t tokens, int
 hipError_t launch_routed_model_dtype(const cq_weight &w, int n_experts, const void *x, int x_dt, int64_t tokens,
                                      const int32_t *token, const int32_t *expert, int64_t routes, int32_t *workspace,
                                      void *y, int y_dt, hipStream_t stream) {
-    // At most one route per expert on average (decode): every route streams
-    // its expert's weights once, with no grouping pass; the expert-grouped
-    // matrix-core path decodes each weight tile once for all routes of its
-    // expert and wins when experts receive several routes.
-    if (routes <= n_experts && gemv_a16_stream_routed_supported(w, n_experts, tokens, routes))
+    // At most one route per two experts (decode of one or two tokens): every
+    // route streams its expert's weights once, with no grouping pass.  More
+    // routes: the expert-grouped matrix-core path decodes each weight tile
+    // once for up to 16 routes of its expert, which wins as soon as experts
+    // share routes (and on skewed maps, where streaming would read one expert
+    // once per route).
+    if (2 * routes <= n_experts && gemv_a16_stream_routed_supported(w, n_experts, tokens, routes))
         return launch_gemv_a16_stream_routed(w, n_experts, x, x_dt, tokens, token, expert, routes, y, y_dt, stream);
     int32_t *offsets = workspace;
     int32_t *order = workspace + n_experts + 1;
@@ -97,6 +99,8 @@ hipError_t launch_routed_model_dtype(const cq_weight &w, int n_experts, const vo
                        n_experts, int(tokens), offsets, order);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (gemm_a16_slab_routed_supported(w, tokens))
+        return launch_gemm_a16_slab_routed(w, n_experts, x, x_dt, tokens, token, order, offsets, y, y_dt, stream);
     return launch_gemv_a16_routed(w, n_experts, x, x_dt, tokens, token, order, offsets, y, y_dt, stream);
 }
 

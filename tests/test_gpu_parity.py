@@ -545,9 +545,10 @@ def test_gemm_a8_fused_carriers_near_rounding_boundaries(torch_dev, dtype):
 def test_routed_model_dtype(torch_dev, bits, group, experts, tokens):
     # route-major outputs for a skewed top-2 route map (top-1 with one expert);
     # 37 rows per expert (ragged strip, odd: route rows start at odd offsets),
-    # experts with more than 16 routes run several chunks; up to one route per
-    # expert (8 experts, 1 or 4 tokens) takes the streaming mode; every route
-    # against the oracle
+    # experts with more than 16 routes run several chunks; at most one route
+    # per two experts (8 experts, 1 token) takes the streaming mode; the
+    # grouped mode runs the staged slab (G B <= 512) or the narrow kernel
+    # (W5 G128); every route against the oracle
     from oracle import routed as RT
     from workloads import route_map, synthetic_representation
     n, k = 37, 1024
@@ -570,11 +571,11 @@ def test_routed_model_dtype(torch_dev, bits, group, experts, tokens):
         assert torch_dev.equal(y, y2)
 
 
-@pytest.mark.parametrize("experts", [4, 8])
+@pytest.mark.parametrize("experts", [4, 16])
 def test_routed_invalid_routes_untouched(torch_dev, experts):
     # routes naming a missing token or expert are dropped; their rows keep
     # the caller's contents, the others match the oracle (7 routes: grouped
-    # mode with 4 experts, streaming mode with 8)
+    # mode with 4 experts, streaming mode with 16)
     from oracle import routed as RT
     from workloads import synthetic_representation
     bits, group, n, k, tokens = 4, 128, 20, 512, 6
