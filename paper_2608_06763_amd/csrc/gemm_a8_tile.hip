@@ -31,6 +31,7 @@
 #include "stream_common.h"
 #include "a8_carriers.h"
 
+#include <atomic>
 #include <type_traits>
 
 #define CQ_INLINE __attribute__((always_inline))
@@ -47,15 +48,21 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int kKS = 64;              // K step
 constexpr int kStride = kKS + 16;    // LDS bytes per tile row (padded)
 
-template <int WM_, int WN_, int BI_, int BJ_, int R_>
+// KSM: at most this many K-groups per workgroup (the launch picks the count).
+// Each K-group is a full set of the tile's waves with its own LDS buffers and a
+// contiguous range of K steps; all of them pass the same per-step barrier, and
+// their FP32 sums meet in LDS at the end.  More waves per workgroup hide the
+// step's latency chain when a short tile leaves few workgroups on the chip.
+template <int WM_, int WN_, int BI_, int BJ_, int R_, int KSM_>
 struct a8_tile {
-    static constexpr int WM = WM_, WN = WN_, BI = BI_, BJ = BJ_, R = R_;
-    static constexpr int NT = 64 * WM * WN;
+    static constexpr int WM = WM_, WN = WN_, BI = BI_, BJ = BJ_, R = R_, KSM = KSM_;
+    static constexpr int NT = 64 * WM * WN;  // threads of one K-group
     static constexpr int TM = 16 * BI * WM, TN = 16 * BJ * WN;
+    static constexpr int LDS = 2 * (TM + TN) * 80;  // bytes of one K-group's buffers
 };
-using a8_tile32 = a8_tile<1, 4, 2, 1, 8>;    // 32 x 64, four waves of 32 x 16
-using a8_tile64 = a8_tile<1, 4, 4, 1, 8>;    // 64 x 64, four waves of 64 x 16
-using a8_tile128 = a8_tile<2, 4, 4, 2, 8>;   // 128 x 128, eight waves of 64 x 32
+using a8_tile32 = a8_tile<1, 4, 2, 1, 8, 4>;    // 32 x 64, four waves of 32 x 16, up to four K-groups
+using a8_tile64 = a8_tile<1, 4, 4, 1, 8, 2>;    // 64 x 64, four waves of 64 x 16, up to two K-groups
+using a8_tile128 = a8_tile<2, 4, 4, 2, 8, 1>;   // 128 x 128, eight waves of 64 x 32
 
 template <int P0, int PN, typename F>
 __device__ __forceinline__ void unroll_slots(F &&f) {
@@ -71,7 +78,7 @@ __device__ __forceinline__ void vmem_order() { __builtin_amdgcn_sched_barrier(0x
 }  // namespace
 
 template <int B, int SPG, int YDT, bool TB, class T>
-__global__ void __launch_bounds__(T::NT) gemm_a8_tile(
+__global__ void __launch_bounds__(T::NT * T::KSM) gemm_a8_tile(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
     int n, int k, const int8_t *__restrict__ x8, const float *__restrict__ dx, int m,
@@ -86,8 +93,11 @@ __global__ void __launch_bounds__(T::NT) gemm_a8_tile(
     static_assert(XB == 8 || XB == 16, "activation loader shape");
     static_assert(R % SPG == 0 && R % 2 == 0, "group boundaries at fixed ring slots");
     static_assert(B == 3 || B == 4, "W3 and W4");
-    __shared__ __attribute__((aligned(16))) int8_t As[2][TM * kStride];
-    __shared__ __attribute__((aligned(16))) int8_t Bs[2][TN * kStride];
+    // one K-group's double buffers per K-group (dynamic, KS x T::LDS bytes)
+    extern __shared__ __attribute__((aligned(16))) int8_t lds_raw[];
+    static_assert(T::KSM == 1 || 16 * NT * BI * BJ <= T::LDS, "K-group sums fit in a group's buffers");
+    static_assert(T::LDS == 2 * (TM + TN) * kStride, "buffer size");
+    const int KS = int(blockDim.x) / NT;
 
     // ---- tile: the workgroups of one XCD take consecutive indices
     const int nwg = tiles_m * tiles_n;
@@ -96,9 +106,14 @@ __global__ void __launch_bounds__(T::NT) gemm_a8_tile(
     const int m0 = (wg / tiles_n) * TM;
     const int n0 = (wg % tiles_n) * TN;
 
-    const int tid = threadIdx.x;
+    const int kg = T::KSM == 1 ? 0 : __builtin_amdgcn_readfirstlane(int(threadIdx.x) / NT);  // K-group
+    const int tid = int(threadIdx.x) - kg * NT;
     const int lane = tid & 63;
     const int wave = tid >> 6;
+    typedef int8_t tile_buf[2][TM * kStride];
+    typedef int8_t wtile_buf[2][TN * kStride];
+    tile_buf &As = *reinterpret_cast<tile_buf *>(lds_raw + kg * 2 * (TM + TN) * kStride);
+    wtile_buf &Bs = *reinterpret_cast<wtile_buf *>(lds_raw + kg * 2 * (TM + TN) * kStride + 2 * TM * kStride);
     const int wm = (wave / WN) * (16 * BI);
     const int wn = (wave % WN) * (16 * BJ);
 
@@ -242,9 +257,15 @@ __global__ void __launch_bounds__(T::NT) gemm_a8_tile(
 
     using S0 = std::integral_constant<int, 0>;
     const int nsteps = k / kKS;
+    // this K-group's steps: [s0, s1), s0 a multiple of the ring length (so
+    // ring positions and group boundaries stay compile-time); every group runs
+    // `per` steps, the ones past s1 without matrix work
+    const int per = ((nsteps + KS - 1) / KS + R - 1) / R * R;
+    const int s0 = kg * per;
+    const int s1 = min(s0 + per, nsteps);
     unroll_slots<0, R>([&](auto p_c) CQ_INLINE {
         constexpr int P = decltype(p_c)::value;
-        load_slot(min(P, nsteps - 1), P, p_c);
+        load_slot(min(s0 + P, nsteps - 1), s0 + P, p_c);
         vmem_order();
     });
     build_tables(S0{});
@@ -261,7 +282,7 @@ __global__ void __launch_bounds__(T::NT) gemm_a8_tile(
         constexpr int SN = (P + 1) % R;
         load_slot(min(st + R, nsteps - 1), st + R, p_c);
         vmem_order();
-        if (st < nsteps) {
+        if (st < s1) {
             i32x4 af[BI], bf[BJ];
 #pragma unroll
             for (int i = 0; i < BI; ++i)
@@ -292,11 +313,28 @@ __global__ void __launch_bounds__(T::NT) gemm_a8_tile(
         __syncthreads();
     };
 
-    for (int st = 0; st < nsteps; st += R)
+    for (int st = s0; st < s0 + per; st += R)
         unroll_slots<0, R>([&](auto p_c) CQ_INLINE {
             constexpr int P = decltype(p_c)::value;
             do_step(st + P, p_c);
         });
+
+    if (T::KSM > 1 && KS > 1) {
+        // the K-groups' sums meet in LDS (the step buffers are free after the
+        // last barrier); K-group 0 adds them in group order and stores
+        f32x4 *red = reinterpret_cast<f32x4 *>(lds_raw);
+#pragma unroll
+        for (int i = 0; i < BI; ++i)
+#pragma unroll
+            for (int j = 0; j < BJ; ++j) red[((kg * BI + i) * BJ + j) * NT + tid] = accf[i][j];
+        __syncthreads();
+        if (kg != 0) return;
+#pragma unroll
+        for (int i = 0; i < BI; ++i)
+#pragma unroll
+            for (int j = 0; j < BJ; ++j)
+                for (int g = 1; g < KS; ++g) accf[i][j] += red[((g * BI + i) * BJ + j) * NT + tid];
+    }
 
 #pragma unroll
     for (int i = 0; i < BI; ++i)
@@ -315,6 +353,30 @@ __global__ void __launch_bounds__(T::NT) gemm_a8_tile(
 
 namespace {
 
+// K-groups per workgroup: the most (up to KSM, at least 4 K steps each) with
+// which every workgroup is resident in one round, by the runtime's occupancy
+// for that block size (cached per kernel, device and count)
+template <class K, class T>
+int a8_tile_groups(K kernel, int64_t nwg, int64_t nsteps) {
+    static std::atomic<int> fit[64][T::KSM + 1];  // workgroups per CU + 1; 0: not yet asked
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1;
+    const int64_t cus = device_cu_count();
+    for (int ks = T::KSM; ks > 1; ks /= 2) {
+        if (nsteps < 4 * ks) continue;
+        int f = fit[dev][ks].load(std::memory_order_relaxed) - 1;
+        if (f < 0) {
+            int nb = 0;
+            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel, T::NT * ks, size_t(ks) * T::LDS) != hipSuccess)
+                nb = 0;
+            fit[dev][ks].store(nb + 1, std::memory_order_relaxed);
+            f = nb;
+        }
+        if (f > 0 && nwg <= int64_t(f) * cus) return ks;
+    }
+    return 1;
+}
+
 template <int B, int SPG, int YDT, bool TB, class T>
 hipError_t a8_tile_launch(const cq_weight &w, const int8_t *ctab, const int8_t *x8, const float *dx, int64_t m,
                           void *y, hipStream_t stream) {
@@ -322,7 +384,9 @@ hipError_t a8_tile_launch(const cq_weight &w, const int8_t *ctab, const int8_t *
     const int64_t tiles_n = (w.n + T::TN - 1) / T::TN;
     const int64_t nwg = tiles_m * tiles_n;
     if (nwg > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((gemm_a8_tile<B, SPG, YDT, TB, T>), dim3(unsigned(nwg)), dim3(T::NT), 0, stream, w.codes,
+    auto kernel = gemm_a8_tile<B, SPG, YDT, TB, T>;
+    const int ks = T::KSM == 1 ? 1 : a8_tile_groups<decltype(kernel), T>(kernel, nwg, w.k / kKS);
+    hipLaunchKernelGGL(kernel, dim3(unsigned(nwg)), dim3(T::NT * ks), size_t(ks) * T::LDS, stream, w.codes,
                        w.scale, w.a, w.b, int(w.n), int(w.k), x8, dx, int(m), y, int(tiles_m), int(tiles_n), ctab);
     return hipGetLastError();
 }
