@@ -66,8 +66,8 @@ hipError_t launch_gemm_a16_slab_staged(const cq_weight &w, const void *x, int x_
 // route list, 16 routes at a time (G <= 128, G B <= 512, K / G a multiple of 4).
 bool gemm_a16_slab_routed_supported(const cq_weight &w, int64_t tokens);
 hipError_t launch_gemm_a16_slab_routed(const cq_weight &w, int n_experts, const void *x, int x_dt, int64_t tokens,
-                                       const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
-                                       int y_dt, hipStream_t stream);
+                                       int64_t routes, const int32_t *token, const int32_t *order,
+                                       const int32_t *offsets, void *y, int y_dt, hipStream_t stream);
 
 // Dynamic-A8 activation quantizer.
 hipError_t launch_quant_a8(const void *x, int x_dt, int64_t m, int64_t k, int8_t *x8, float *dx,

@@ -349,8 +349,8 @@ __global__ void __launch_bounds__(1024) gemm_a16_slab(
 // (e, 16 weight rows) serves every route of expert e that the grouping pass
 // listed (rorder[roff[e] .. roff[e + 1])), 16 routes at a time: a route's x
 // row is its token and its output is row `route` of y.
-template <int B, int UPG, int XDT, int YDT, bool ROUTED>
-__global__ void __launch_bounds__(ROUTED ? 512 : 1024) gemm_a16_slab_st(
+template <int B, int UPG, int XDT, int YDT, bool ROUTED, bool XT>
+__global__ void __launch_bounds__((ROUTED || XT) ? 512 : 1024) gemm_a16_slab_st(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
     int n, int k, const uint16_t *__restrict__ x, int m, void *__restrict__ y, int tiles_n,
@@ -369,7 +369,8 @@ __global__ void __launch_bounds__(ROUTED ? 512 : 1024) gemm_a16_slab_st(
     constexpr int NB = 4;                     // sweeps per metadata batch
     constexpr uint32_t kTab = NE * 256u;
     constexpr uint32_t kMeta = 16u * NB * 16u;  // one metadata array of a batch (bytes)
-    constexpr uint32_t kStage = 16u * CS + 2u * kMeta;
+    constexpr uint32_t kX = XT ? 64u * 80u : 0u;  // transposed activations of a chunk
+    constexpr uint32_t kStage = 16u * CS + 2u * kMeta + kX;
     constexpr uint32_t kNeg = 0x80008000u;
     static_assert(SEG % 16 == 0 && SEG <= 512, "staged sweep size");
     extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
@@ -416,6 +417,7 @@ __global__ void __launch_bounds__(ROUTED ? 512 : 1024) gemm_a16_slab_st(
     const uint32_t stg = tbase + uint32_t(nw) * kTab + uint32_t(wave) * kStage;
     const uint32_t mst = stg + 16u * CS;      // batch scales [row][sweep][group]
     const uint32_t mab = mst + kMeta;         // batch a | b << 16, same layout
+    const uint32_t xst = mab + kMeta;         // XT: activation pieces [q * 16 + row][80 bytes]
 
     uint32_t cr[T][4];                        // codes of one sweep as loaded
     uint32_t ms4[4], ma2[2], mb2[2];          // metadata of one batch as loaded
@@ -461,17 +463,37 @@ __global__ void __launch_bounds__(ROUTED ? 512 : 1024) gemm_a16_slab_st(
             u32x4{__builtin_amdgcn_perm(mb2[0], ma2[0], 0x05040100u), __builtin_amdgcn_perm(mb2[0], ma2[0], 0x07060302u),
                   __builtin_amdgcn_perm(mb2[1], ma2[1], 0x05040100u), __builtin_amdgcn_perm(mb2[1], ma2[1], 0x07060302u)};
     };
-    // x row of this lane's MFMA row in the current 16 rows (-1: none)
+    // x row of this lane's MFMA row in the current 16 rows (-1: none); with
+    // XT, the rows of the four pieces this lane loads (row 4 i + lane / 16)
     int xr = -1;
-    // activations of chunk c (sweep sa + c / UPG, unit c % UPG of the lane's group)
+    int xrl[4] = {-1, -1, -1, -1};
+    // activations of chunk c (sweep sa + c / UPG, unit c % UPG of each lane's
+    // group).  XT: a wave load brings 64-byte pieces (row r, group q) as four
+    // lanes' 16-byte parts, the parts of one row's four groups lying 2G bytes
+    // apart, instead of one 16-byte part per lane and cache line; the pieces
+    // are handed to their lanes through LDS in compute().
     auto load_x = [&](int c, auto slot_c) {
         constexpr int SL = decltype(slot_c)::value;
         const int sw = sa + c / UPG, u = c % UPG;
-        const int row = xr;
-        const bool ok = row >= 0 && sw < sb;
-        load_words<16>(rx, ok ? (uint32_t(row) * uint32_t(k) + uint32_t(4 * sw + q) * G + uint32_t(u) * 32u) * 2u
-                              : kOobOffset,
-                       xw[SL]);
+        if constexpr (XT) {
+            const int gq = (lane >> 2) & 3, sub = lane & 3;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int row = xrl[i];
+                const bool ok = row >= 0 && sw < sb;
+                load_words<4>(rx,
+                              ok ? (uint32_t(row) * uint32_t(k) + uint32_t(4 * sw + gq) * G + uint32_t(u) * 32u) * 2u +
+                                       16u * uint32_t(sub)
+                                 : kOobOffset,
+                              &xw[SL][4 * i]);
+            }
+        } else {
+            const int row = xr;
+            const bool ok = row >= 0 && sw < sb;
+            load_words<16>(rx, ok ? (uint32_t(row) * uint32_t(k) + uint32_t(4 * sw + q) * G + uint32_t(u) * 32u) * 2u
+                                  : kOobOffset,
+                           xw[SL]);
+        }
     };
 
     // the lane's table for its group of sweep i of the wave (batch slot i % NB)
@@ -512,6 +534,26 @@ __global__ void __launch_bounds__(ROUTED ? 512 : 1024) gemm_a16_slab_st(
     // decode unit u of the staged sweep and multiply with activation slot SL
     auto compute = [&](int u, auto slot_c) {
         constexpr int SL = decltype(slot_c)::value;
+        u32x4 xa[4];  // this lane's activations of the chunk's four MFMAs
+        if constexpr (XT) {
+            // pieces to their slots q * 16 + row (80-byte slots: the 16 lanes
+            // of one block read 16 disjoint 4-bank ranges), then this lane's
+            const int gq = (lane >> 2) & 3, sub = lane & 3;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t slot = uint32_t(gq) * 16u + uint32_t(4 * i + (lane >> 4));
+                *reinterpret_cast<lds_u32x4 *>(uintptr_t(xst + slot * 80u + 16u * uint32_t(sub))) =
+                    u32x4{xw[SL][4 * i], xw[SL][4 * i + 1], xw[SL][4 * i + 2], xw[SL][4 * i + 3]};
+            }
+            wave_lds_fence();
+            const uint32_t mine = xst + (uint32_t(q) * 16u + uint32_t(nl)) * 80u;
+#pragma unroll
+            for (int st = 0; st < 4; ++st) xa[st] = *reinterpret_cast<const lds_u32x4 *>(uintptr_t(mine + 16u * st));
+        } else {
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+                xa[st] = u32x4{xw[SL][4 * st], xw[SL][4 * st + 1], xw[SL][4 * st + 2], xw[SL][4 * st + 3]};
+        }
         const uint32_t ca = stg + uint32_t(nl) * CS + uint32_t(q) * GB + uint32_t(u) * (4u * B);
         uint32_t cw[B];
         if constexpr (B == 4) {
@@ -552,15 +594,24 @@ __global__ void __launch_bounds__(ROUTED ? 512 : 1024) gemm_a16_slab_st(
                 bh[p] = __builtin_amdgcn_perm(ent[8 * st + 2 * p + 1], ent[8 * st + 2 * p], 0x05040100u);
                 bl[p] = __builtin_amdgcn_perm(ent[8 * st + 2 * p + 1], ent[8 * st + 2 * p], 0x07060302u);
             }
-            const u32x4 af = u32x4{xw[SL][4 * st], xw[SL][4 * st + 1], xw[SL][4 * st + 2], xw[SL][4 * st + 3]};
-            acc = mma<XDT>(af, bh, acc);
-            acc = mma<XDT>(af, bl, acc);
+            acc = mma<XDT>(xa[st], bh, acc);
+            acc = mma<XDT>(xa[st], bl, acc);
         }
+        if constexpr (XT) wave_lds_fence();  // the pieces are read before the next chunk's are written
     };
 
   for (int c0 = c_begin; c0 < c_end; c0 += 16) {
-    if constexpr (ROUTED) xr = c0 + nl < c_end ? rtok[rorder[c0 + nl]] : -1;
-    else xr = c0 + nl < c_end ? c0 + nl : -1;
+    if constexpr (XT) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int r = c0 + 4 * i + (lane >> 4);
+            if constexpr (ROUTED) xrl[i] = r < c_end ? rtok[rorder[r]] : -1;
+            else xrl[i] = r < c_end ? r : -1;
+        }
+    } else {
+        if constexpr (ROUTED) xr = c0 + nl < c_end ? rtok[rorder[c0 + nl]] : -1;
+        else xr = c0 + nl < c_end ? c0 + nl : -1;
+    }
     acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
     if (nmy > 0) {
         if constexpr (B >= 2) {
@@ -691,38 +742,46 @@ hipError_t slab_bits(const cq_weight &w, const void *x, int64_t m, void *y, hipS
 
 // staged variant: groups of at most 128 codes with at most 256 code bytes per
 // row and sweep (larger ones spill registers in the unrolled sweep loop)
-template <int B, int UPG, int XDT, int YDT>
-hipError_t slab_st_launch(const cq_weight &w, const void *x, int64_t m, void *y, hipStream_t stream) {
+template <int B, int UPG, int XDT, int YDT, bool XT>
+hipError_t slab_st_launch_x(const cq_weight &w, const void *x, int64_t m, void *y, hipStream_t stream) {
     constexpr int NE = 1 << B;
     constexpr uint32_t kTab = NE * 256u;
     constexpr uint32_t CS = 4 * (32 * UPG) * B / 8 + 16;
-    constexpr uint32_t kStage = 16u * CS + 2u * 16u * 4u * 16u;
+    constexpr uint32_t kStage = 16u * CS + 2u * 16u * 4u * 16u + (XT ? 64u * 80u : 0u);
     const int64_t tiles_n = (w.n + 15) / 16;
     const int64_t tiles = (m + 15) / 16 * tiles_n;
     if (tiles > 0x7fffffff) return hipErrorInvalidValue;
     const int64_t nsw = w.k / w.group / 4;
     int64_t s = int64_t(device_cu_count()) * 16 / tiles;
-    if (s > 16) s = 16;
+    if (s > (XT ? 8 : 16)) s = XT ? 8 : 16;  // the kernel's launch bound
     if (s > nsw) s = nsw;
     // LDS: tables below 64 KB, whole workgroup within 128 KB
     while (s > 1 && (s * kTab > 65536 || s * (kTab + kStage) > 131072)) --s;
     if (s < 1) s = 1;
     const size_t lds = size_t(s) * (kTab + kStage) > size_t(s) * 1024 ? size_t(s) * (kTab + kStage) : size_t(s) * 1024;
-    hipLaunchKernelGGL((gemm_a16_slab_st<B, UPG, XDT, YDT, false>), dim3(unsigned(tiles)), dim3(unsigned(64 * s)),
-                       lds, stream, w.codes, w.scale, w.a, w.b, int(w.n), int(w.k), static_cast<const uint16_t *>(x),
-                       int(m), y, int(tiles_n), nullptr, nullptr, nullptr);
+    hipLaunchKernelGGL((gemm_a16_slab_st<B, UPG, XDT, YDT, false, XT>), dim3(unsigned(tiles)),
+                       dim3(unsigned(64 * s)), lds, stream, w.codes, w.scale, w.a, w.b, int(w.n), int(w.k),
+                       static_cast<const uint16_t *>(x), int(m), y, int(tiles_n), nullptr, nullptr, nullptr);
     return hipGetLastError();
 }
 
-// routed: one workgroup per (expert, 16 weight rows); route chunks of 16
+// more than 8 rows: activations through the transposing LDS pieces (they
+// cost a wave per SIMD of occupancy, which 5..8 rows do not win back)
 template <int B, int UPG, int XDT, int YDT>
-hipError_t slab_st_routed_launch(const cq_weight &w, int n_experts, const void *x, int64_t tokens,
-                                 const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
-                                 hipStream_t stream) {
+hipError_t slab_st_launch(const cq_weight &w, const void *x, int64_t m, void *y, hipStream_t stream) {
+    if (m > 8) return slab_st_launch_x<B, UPG, XDT, YDT, true>(w, x, m, y, stream);
+    return slab_st_launch_x<B, UPG, XDT, YDT, false>(w, x, m, y, stream);
+}
+
+// routed: one workgroup per (expert, 16 weight rows); route chunks of 16
+template <int B, int UPG, int XDT, int YDT, bool XT>
+hipError_t slab_st_routed_launch_x(const cq_weight &w, int n_experts, const void *x, int64_t tokens,
+                                   const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
+                                   hipStream_t stream) {
     constexpr int NE = 1 << B;
     constexpr uint32_t kTab = NE * 256u;
     constexpr uint32_t CS = 4 * (32 * UPG) * B / 8 + 16;
-    constexpr uint32_t kStage = 16u * CS + 2u * 16u * 4u * 16u;
+    constexpr uint32_t kStage = 16u * CS + 2u * 16u * 4u * 16u + (XT ? 64u * 80u : 0u);
     const int64_t tiles_n = (w.n + 15) / 16;
     const int64_t blocks = tiles_n * n_experts;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
@@ -733,10 +792,20 @@ hipError_t slab_st_routed_launch(const cq_weight &w, int n_experts, const void *
     while (s > 1 && (s * kTab > 65536 || s * (kTab + kStage) > 131072)) --s;
     if (s < 1) s = 1;
     const size_t lds = size_t(s) * (kTab + kStage) > size_t(s) * 1024 ? size_t(s) * (kTab + kStage) : size_t(s) * 1024;
-    hipLaunchKernelGGL((gemm_a16_slab_st<B, UPG, XDT, YDT, true>), dim3(unsigned(blocks)), dim3(unsigned(64 * s)),
-                       lds, stream, w.codes, w.scale, w.a, w.b, int(w.n), int(w.k), static_cast<const uint16_t *>(x),
-                       int(tokens), y, int(tiles_n), token, order, offsets);
+    hipLaunchKernelGGL((gemm_a16_slab_st<B, UPG, XDT, YDT, true, XT>), dim3(unsigned(blocks)),
+                       dim3(unsigned(64 * s)), lds, stream, w.codes, w.scale, w.a, w.b, int(w.n), int(w.k),
+                       static_cast<const uint16_t *>(x), int(tokens), y, int(tiles_n), token, order, offsets);
     return hipGetLastError();
+}
+
+// more than 8 routes per expert on average: the transposing activation pieces
+template <int B, int UPG, int XDT, int YDT>
+hipError_t slab_st_routed_launch(const cq_weight &w, int n_experts, const void *x, int64_t tokens, int64_t routes,
+                                 const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
+                                 hipStream_t stream) {
+    if (routes > 8 * int64_t(n_experts))
+        return slab_st_routed_launch_x<B, UPG, XDT, YDT, true>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+    return slab_st_routed_launch_x<B, UPG, XDT, YDT, false>(w, n_experts, x, tokens, token, order, offsets, y, stream);
 }
 
 template <int B, int XDT, int YDT>
@@ -752,30 +821,30 @@ hipError_t slab_st_group(const cq_weight &w, const void *x, int64_t m, void *y, 
 }
 
 template <int B, int XDT, int YDT>
-hipError_t slab_st_routed_group(const cq_weight &w, int n_experts, const void *x, int64_t tokens,
+hipError_t slab_st_routed_group(const cq_weight &w, int n_experts, const void *x, int64_t tokens, int64_t routes,
                                 const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
                                 hipStream_t stream) {
     switch (w.group) {
-        case 32: return slab_st_routed_launch<B, 1, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
-        case 64: return slab_st_routed_launch<B, 2, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        case 32: return slab_st_routed_launch<B, 1, XDT, YDT>(w, n_experts, x, tokens, routes, token, order, offsets, y, stream);
+        case 64: return slab_st_routed_launch<B, 2, XDT, YDT>(w, n_experts, x, tokens, routes, token, order, offsets, y, stream);
         case 128:
             if constexpr (B <= 4)
-                return slab_st_routed_launch<B, 4, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+                return slab_st_routed_launch<B, 4, XDT, YDT>(w, n_experts, x, tokens, routes, token, order, offsets, y, stream);
             break;
     }
     return hipErrorNotSupported;
 }
 
 template <int XDT, int YDT>
-hipError_t slab_st_routed_bits(const cq_weight &w, int n_experts, const void *x, int64_t tokens,
+hipError_t slab_st_routed_bits(const cq_weight &w, int n_experts, const void *x, int64_t tokens, int64_t routes,
                                const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
                                hipStream_t stream) {
     switch (w.bits) {
-        case 1: return slab_st_routed_group<1, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
-        case 2: return slab_st_routed_group<2, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
-        case 3: return slab_st_routed_group<3, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
-        case 4: return slab_st_routed_group<4, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
-        case 5: return slab_st_routed_group<5, XDT, YDT>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        case 1: return slab_st_routed_group<1, XDT, YDT>(w, n_experts, x, tokens, routes, token, order, offsets, y, stream);
+        case 2: return slab_st_routed_group<2, XDT, YDT>(w, n_experts, x, tokens, routes, token, order, offsets, y, stream);
+        case 3: return slab_st_routed_group<3, XDT, YDT>(w, n_experts, x, tokens, routes, token, order, offsets, y, stream);
+        case 4: return slab_st_routed_group<4, XDT, YDT>(w, n_experts, x, tokens, routes, token, order, offsets, y, stream);
+        case 5: return slab_st_routed_group<5, XDT, YDT>(w, n_experts, x, tokens, routes, token, order, offsets, y, stream);
     }
     return hipErrorNotSupported;
 }

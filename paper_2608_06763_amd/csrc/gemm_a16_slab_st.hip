@@ -33,15 +33,15 @@ bool gemm_a16_slab_routed_supported(const cq_weight &w, int64_t tokens) {
 }
 
 hipError_t launch_gemm_a16_slab_routed(const cq_weight &w, int n_experts, const void *x, int x_dt, int64_t tokens,
-                                       const int32_t *token, const int32_t *order, const int32_t *offsets, void *y,
-                                       int y_dt, hipStream_t stream) {
+                                       int64_t routes, const int32_t *token, const int32_t *order,
+                                       const int32_t *offsets, void *y, int y_dt, hipStream_t stream) {
     using namespace a16_slab;
     if (x_dt == 0) {
-        if (y_dt == 0) return slab_st_routed_bits<0, 0>(w, n_experts, x, tokens, token, order, offsets, y, stream);
-        return slab_st_routed_bits<0, 2>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+        if (y_dt == 0) return slab_st_routed_bits<0, 0>(w, n_experts, x, tokens, routes, token, order, offsets, y, stream);
+        return slab_st_routed_bits<0, 2>(w, n_experts, x, tokens, routes, token, order, offsets, y, stream);
     }
-    if (y_dt == 1) return slab_st_routed_bits<1, 1>(w, n_experts, x, tokens, token, order, offsets, y, stream);
-    return slab_st_routed_bits<1, 2>(w, n_experts, x, tokens, token, order, offsets, y, stream);
+    if (y_dt == 1) return slab_st_routed_bits<1, 1>(w, n_experts, x, tokens, routes, token, order, offsets, y, stream);
+    return slab_st_routed_bits<1, 2>(w, n_experts, x, tokens, routes, token, order, offsets, y, stream);
 }
 
 hipError_t launch_a16_slab_st(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,

@@ -100,7 +100,8 @@ hipError_t launch_routed_model_dtype(const cq_weight &w, int n_experts, const vo
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (gemm_a16_slab_routed_supported(w, tokens))
-        return launch_gemm_a16_slab_routed(w, n_experts, x, x_dt, tokens, token, order, offsets, y, y_dt, stream);
+        return launch_gemm_a16_slab_routed(w, n_experts, x, x_dt, tokens, routes, token, order, offsets, y, y_dt,
+                                           stream);
     return launch_gemv_a16_routed(w, n_experts, x, x_dt, tokens, token, order, offsets, y, y_dt, stream);
 }
 

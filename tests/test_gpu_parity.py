@@ -751,7 +751,7 @@ def test_gemm_slab(torch_dev, bits, group, k, m):
 
 @pytest.mark.parametrize("bits", [1, 2, 3, 4, 5])
 @pytest.mark.parametrize("group,k", [(32, 1024), (64, 1024), (128, 2048)])
-@pytest.mark.parametrize("m", [1, 7, 16])
+@pytest.mark.parametrize("m", [1, 7, 12, 16])
 def test_gemm_slab_staged(torch_dev, bits, group, k, m):
     # codes and metadata staged through LDS: 83 weight rows (ragged block),
     # four or more sweeps; W5 stages groups of up to 64 codes
