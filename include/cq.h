@@ -166,13 +166,16 @@ cq_status cq_gemm_a8(const cq_weight *w, const int8_t *x8, const float *dx, int6
  * cq_gemm_a8_fused -- Dynamic-A8 product from model-dtype activations (device).
  *
  * Same result as cq_quantize_act_a8 followed by cq_gemm_a8 (Sec. 5.4): x8 and
- * dx receive the carriers and d_x, bit-exact; y follows eq. a8-output.  For a
- * single row (m == 1, B <= 4, K <= 16384) it is one launch: the GEMV
- * forms the row's carriers itself in a prologue, which removes the separate
+ * dx receive the carriers and d_x, bit-exact; y follows eq. a8-output.  By
+ * default it runs exactly those two calls in order on the stream, which
+ * measured faster on MI355X than the single launch on every decode layer.
+ * With cq_set_a8_fused_launch(1), a single row (m == 1, B <= 4, K <= 16384,
+ * and m within the A8 GEMV threshold) is one launch instead: the GEMV forms
+ * the row's carriers itself in a prologue, which removes the separate
  * encoding pass the paper names as the fixed cost of the single-row A8 path
- * (Sec. 6).  Other shapes run the two calls in order on the stream.  The FP32
- * summation order of the single launch can differ from cq_gemm_a8's for the
- * same row, so y agrees with it to rounding, not bit for bit.
+ * (Sec. 6).  The FP32 summation order of the single launch can differ from
+ * cq_gemm_a8's for the same row, so its y agrees with the two calls' to
+ * rounding, not bit for bit.
  *   x        device [M, K] in x_dtype (CQ_BF16 or CQ_FP16).
  *   x8, dx   device int8 [M, K] and float [M], written (caller-owned).
  *   y        device [M, N] in y_dtype (CQ_BF16, CQ_FP16 or CQ_FP32).
@@ -180,6 +183,15 @@ cq_status cq_gemm_a8(const cq_weight *w, const int8_t *x8, const float *dx, int6
  */
 cq_status cq_gemm_a8_fused(const cq_weight *w, const void *x, cq_dtype x_dtype, int64_t m,
                            int8_t *x8, float *dx, void *y, cq_dtype y_dtype, void *stream);
+
+/*
+ * How cq_gemm_a8_fused runs a single row: 0 (default) the quantizer and the
+ * product as two launches, 1 the single fused launch where it applies.  Other
+ * values are CQ_ERR_ARG.  Host only, process wide; a call already past its
+ * dispatch is not affected.
+ */
+cq_status cq_set_a8_fused_launch(int32_t single);
+int32_t cq_get_a8_fused_launch(void);
 
 /*
  * cq_build_carriers -- load-time INT8 carrier tables (device).

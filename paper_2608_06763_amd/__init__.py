@@ -9,6 +9,7 @@ Entry points (same names as the C ABI):
   cq_pack_groups, cq_decode_ref, cq_gemm_model_dtype, cq_quantize_act_a8,
   cq_gemm_a8, cq_gemm_a8_fused, cq_build_carriers, cq_gemm_a8_carriers,
   cq_gemm_routed_model_dtype, cq_gemm_routed_model_dtype_noalloc, cq_set_gemv_max_rows, cq_get_gemv_max_rows,
+  cq_set_a8_fused_launch, cq_get_a8_fused_launch,
   cq_family_supported, cq_gemm_model_dtype_family, cq_gemm_a8_family,
   cq_select_set, cq_select_query, cq_probe_read (measurement aid, include/cq_measure.h)
 The measured kernel-selection tuner that fills the selection table is in
@@ -32,7 +33,8 @@ EXPORTS = ("cq_status_str", "cq_pack_groups", "cq_decode_ref", "cq_gemm_model_dt
            "cq_gemm_a8", "cq_gemm_a8_fused", "cq_build_carriers", "cq_gemm_a8_carriers",
            "cq_gemm_routed_model_dtype", "cq_set_gemv_max_rows", "cq_get_gemv_max_rows",
            "cq_family_supported", "cq_gemm_model_dtype_family", "cq_gemm_a8_family", "cq_select_set",
-           "cq_select_query", "cq_probe_read", "cq_gemm_routed_model_dtype_noalloc")
+           "cq_select_query", "cq_probe_read", "cq_gemm_routed_model_dtype_noalloc", "cq_set_a8_fused_launch",
+           "cq_get_a8_fused_launch")
 
 CQ_PATH_MODEL_DTYPE, CQ_PATH_A8 = 0, 1
 FAMILIES = {"auto": 0, "gemv_stream": 1, "gemv_lut": 2, "gemv_narrow": 3, "gemv_generic": 4, "gemm_mfma": 5,
@@ -98,6 +100,10 @@ def lib() -> ctypes.CDLL:
                                                      vp, ctypes.c_int, vp]
     L.cq_set_gemv_max_rows.restype = ctypes.c_int
     L.cq_set_gemv_max_rows.argtypes = [i32, i64]
+    L.cq_set_a8_fused_launch.restype = ctypes.c_int
+    L.cq_set_a8_fused_launch.argtypes = [i32]
+    L.cq_get_a8_fused_launch.restype = i32
+    L.cq_get_a8_fused_launch.argtypes = []
     L.cq_get_gemv_max_rows.restype = i64
     L.cq_get_gemv_max_rows.argtypes = [i32]
     L.cq_family_supported.restype = i32
@@ -354,6 +360,14 @@ def cq_set_gemv_max_rows(path: int, max_rows: int):
 
 def cq_get_gemv_max_rows(path: int) -> int:
     return int(lib().cq_get_gemv_max_rows(path))
+
+
+def cq_set_a8_fused_launch(single: int):
+    _check(lib().cq_set_a8_fused_launch(int(single)), "cq_set_a8_fused_launch")
+
+
+def cq_get_a8_fused_launch() -> int:
+    return int(lib().cq_get_a8_fused_launch())
 
 
 # ---------------------------------------------------------------- kernel families and the selection table

@@ -34,6 +34,8 @@ double shape_margin(double a, double b) {
     return m;
 }
 
+// cq_gemm_a8_fused: 1 = single fused launch for one row, 0 = two launches
+std::atomic<int32_t> g_a8_fused_single{0};
 std::atomic<int64_t> g_gemv_max_rows[2] = {{-1}, {-1}};
 constexpr int64_t kDefaultGemvMaxRows[2] = {cq::kGemvMaxRows, cq::kGemvMaxRows};
 
@@ -194,9 +196,11 @@ cq_status cq_gemm_a8_fused(const cq_weight *w, const void *x, cq_dtype x_dtype, 
     if (!aligned16(x) || !aligned16(x8) || !aligned16(dx) || !aligned16(y)) return CQ_ERR_ALIGN;
     if (m > (int64_t(1) << 40) / w->k || m > (int64_t(1) << 40) / w->n) return CQ_ERR_SHAPE;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (m <= gemv_max_rows(1) && cq::gemv_a8_fused_supported(*w, m))
+    if (g_a8_fused_single.load(std::memory_order_relaxed) && m <= gemv_max_rows(1) &&
+        cq::gemv_a8_fused_supported(*w, m))
         return hip_status(cq::launch_gemv_a8_fused(*w, x, int(x_dtype), x8, dx, y, int(y_dtype), s));
-    // every other shape: the two calls, in order on the stream
+    // the default, and every shape the single launch does not take: the two
+    // calls, in order on the stream
     const cq_status q = cq_quantize_act_a8(x, x_dtype, m, w->k, x8, dx, stream);
     if (q != CQ_OK) return q;
     return cq_gemm_a8(w, x8, dx, m, y, y_dtype, nullptr, stream);
@@ -269,6 +273,14 @@ cq_status cq_gemm_a8_carriers(const cq_weight *w, const int8_t *carriers, const 
     if (m > int64_t(65535) * 64) return CQ_ERR_SHAPE;
     return hip_status(cq::launch_gemm_a8_tab(*w, carriers, x8, dx, m, y, int(y_dtype), s));
 }
+
+cq_status cq_set_a8_fused_launch(int32_t single) {
+    if (single != 0 && single != 1) return CQ_ERR_ARG;
+    g_a8_fused_single.store(single, std::memory_order_relaxed);
+    return CQ_OK;
+}
+
+int32_t cq_get_a8_fused_launch(void) { return g_a8_fused_single.load(std::memory_order_relaxed); }
 
 cq_status cq_set_gemv_max_rows(int32_t path, int64_t max_rows) {
     if (path != 0 && path != 1) return CQ_ERR_ARG;

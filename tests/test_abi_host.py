@@ -276,6 +276,15 @@ def test_builtin_slab_variant(clean_table, n, k, m, want):
     assert cq.cq_select_query(cq.CQ_PATH_MODEL_DTYPE, _fake(4, 128, n, k), m) == want
 
 
+def test_a8_fused_launch_knob():
+    assert cq.cq_get_a8_fused_launch() == 0
+    cq.cq_set_a8_fused_launch(1)
+    assert cq.cq_get_a8_fused_launch() == 1
+    cq.cq_set_a8_fused_launch(0)
+    assert cq.cq_get_a8_fused_launch() == 0
+    assert cq.lib().cq_set_a8_fused_launch(2) == 1 and cq.cq_get_a8_fused_launch() == 0
+
+
 def test_builtin_rules_follow_gemv_threshold(clean_table):
     d = _fake(4, 128, 4096, 4096)
     cq.cq_set_gemv_max_rows(0, 0)

@@ -251,7 +251,11 @@ def test_fullsize_fused_a8_decode_layers(torch_dev, layer):
     xb = llama8b_act(1, k, layer)
     xv = bf16_bits_to_f32(xb).astype(np.float64)
     say("fused a8", name)
-    y, x8, dx = cq.cq_gemm_a8_fused(w, _dev_x(torch_dev, xb), y_dtype=torch_dev.float32)
+    cq.cq_set_a8_fused_launch(1)  # the single launch (the default runs the two calls)
+    try:
+        y, x8, dx = cq.cq_gemm_a8_fused(w, _dev_x(torch_dev, xb), y_dtype=torch_dev.float32)
+    finally:
+        cq.cq_set_a8_fused_launch(0)
     x8_ref, d_ref = A8.quantize_act(xv)
     assert np.array_equal(x8.cpu().numpy(), x8_ref)
     assert np.array_equal(dx.cpu().numpy(), d_ref.astype(np.float32))

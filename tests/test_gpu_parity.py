@@ -405,10 +405,35 @@ def test_narrow_rows_both_paths(torch_dev, group, m):
 # ---------------------------------------------------------------- fused single-row A8
 
 
+@pytest.fixture
+def single_launch():
+    # cq_gemm_a8_fused as one launch for a single row (the default is two)
+    cq = _cq()
+    cq.cq_set_a8_fused_launch(1)
+    yield
+    cq.cq_set_a8_fused_launch(0)
+
+
+def test_gemm_a8_fused_default_is_two_calls(torch_dev):
+    # by default the fused call runs the quantizer and the product: its outputs
+    # equal the two calls' bit for bit
+    cq = _cq()
+    assert cq.cq_get_a8_fused_launch() == 0
+    bits, group, k = 4, 128, 4096
+    r = fitted(50, 37, k, bits, group)
+    w = _weight(r, bits, group)
+    xb, xv = act(49, 1, k)
+    x = _x(torch_dev, xb, "bf16")
+    y, x8, dx = cq.cq_gemm_a8_fused(w, x, y_dtype=torch_dev.float32)
+    x8b, dxb = cq.cq_quantize_act_a8(x)
+    assert torch_dev.equal(x8, x8b) and torch_dev.equal(dx, dxb)
+    assert torch_dev.equal(y, cq.cq_gemm_a8(w, x8b, dxb, y_dtype=torch_dev.float32))
+
+
 @pytest.mark.parametrize("bits", [1, 2, 3, 4])
 @pytest.mark.parametrize("group", [32, 128, 512])
 @pytest.mark.parametrize("k", [512, 2048, 4096, 4096 + 2048 + 512, 14336, 16384])
-def test_gemm_a8_fused_single_row(torch_dev, bits, group, k):
+def test_gemm_a8_fused_single_row(torch_dev, single_launch, bits, group, k):
     # m == 1: one launch that quantizes its own activations (one to eight
     # column blocks, the last one ragged for K = 6656); carriers and d_x are
     # compared bit for bit, y against the A8 oracle
@@ -434,9 +459,10 @@ def test_gemm_a8_fused_single_row(torch_dev, bits, group, k):
 
 
 @pytest.mark.parametrize("case", ["rows3", "w6", "k18432", "zero_row", "gemv_rows_0"])
-def test_gemm_a8_fused_fallbacks(torch_dev, case):
-    # shapes the single launch does not take run the two calls; an all-zero
-    # row gives d_x = eps / 127, zero carriers and a zero output
+def test_gemm_a8_fused_fallbacks(torch_dev, single_launch, case):
+    # with the single launch enabled, shapes it does not take run the two
+    # calls; an all-zero row gives d_x = eps / 127, zero carriers and a zero
+    # output
     cq = _cq()
     bits, group, k, m, n = 4, 128, 2048, 1, 21
     if case == "rows3":
@@ -481,7 +507,7 @@ def _encode(vals, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp16"])
-def test_gemm_a8_fused_carriers_near_rounding_boundaries(torch_dev, dtype):
+def test_gemm_a8_fused_carriers_near_rounding_boundaries(torch_dev, single_launch, dtype):
     # the single-row call forms carriers from x * (1/d) and divides only near
     # a rounding boundary; for 24 random row scales, every representable
     # activation whose quotient lies within 2^-15 of a half-integer (plus a
