@@ -329,12 +329,13 @@ int64_t cq_get_gemv_max_rows(int32_t path);
  *                 the K loop) and the waves of a workgroup split K; numerics
  *                 as GEMM_MFMA (hi + lo operand in the activation dtype, FP32
  *                 accumulation).
- *   GEMM_SLAB_STAGED  model dtype only, 1 <= m <= 16, G <= 128, G B <= 512,
+ *   GEMM_SLAB_STAGED  model dtype only, 1 <= m <= 32, G <= 128, G B <= 512,
  *                 K / G a multiple of 4: GEMM_SLAB whose waves each take a
  *                 contiguous K range and bring codes and group metadata in
  *                 through LDS with whole-cache-line loads; same numerics.
- *                 The built-in rules pick it when the K split gives the waves
- *                 two or more sweeps of four groups each.
+ *                 Above 16 rows each wave serves two 16-row blocks of x.
+ *                 The built-in rules pick it when the K split gives the
+ *                 waves two or more sweeps of four groups each.
  * Families that read 32-bit buffer offsets also need tensors below 2 GiB.
  */
 typedef enum { CQ_PATH_MODEL_DTYPE = 0, CQ_PATH_A8 = 1 } cq_path;

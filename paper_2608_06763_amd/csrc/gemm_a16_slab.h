@@ -349,7 +349,7 @@ __global__ void __launch_bounds__(1024) gemm_a16_slab(
 // (e, 16 weight rows) serves every route of expert e that the grouping pass
 // listed (rorder[roff[e] .. roff[e + 1])), 16 routes at a time: a route's x
 // row is its token and its output is row `route` of y.
-template <int B, int UPG, int XDT, int YDT, bool ROUTED, bool XT>
+template <int B, int UPG, int XDT, int YDT, bool ROUTED, bool XT, int XB>
 __global__ void __launch_bounds__((ROUTED || XT) ? 512 : 1024) gemm_a16_slab_st(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
@@ -369,7 +369,8 @@ __global__ void __launch_bounds__((ROUTED || XT) ? 512 : 1024) gemm_a16_slab_st(
     constexpr int NB = 4;                     // sweeps per metadata batch
     constexpr uint32_t kTab = NE * 256u;
     constexpr uint32_t kMeta = 16u * NB * 16u;  // one metadata array of a batch (bytes)
-    constexpr uint32_t kX = XT ? 64u * 80u : 0u;  // transposed activations of a chunk
+    static_assert(XB == 1 || (XB == 2 && XT && !ROUTED), "two x-row blocks take the transposed activations");
+    constexpr uint32_t kX = XT ? XB * 64u * 80u : 0u;  // transposed activations of a chunk
     constexpr uint32_t kStage = 16u * CS + 2u * kMeta + kX;
     constexpr uint32_t kNeg = 0x80008000u;
     static_assert(SEG % 16 == 0 && SEG <= 512, "staged sweep size");
@@ -383,7 +384,7 @@ __global__ void __launch_bounds__((ROUTED || XT) ? 512 : 1024) gemm_a16_slab_st(
     const int n0 = tn * 16;
     const int ng = k / G;                     // a multiple of 4
     const uint32_t row_bytes = uint32_t(k) * B / 8u;
-    // rows of x served by this workgroup, 16 at a time: rows tm * 16 .. + 15,
+    // rows of x served by this workgroup, 16 XB at a time: rows tm * 16 XB ..,
     // or (routed: tm is the expert) the expert's routes, whose x rows are their
     // tokens and whose outputs are rows of y in route order
     int c_begin, c_end;
@@ -395,8 +396,8 @@ __global__ void __launch_bounds__((ROUTED || XT) ? 512 : 1024) gemm_a16_slab_st(
         a16 += size_t(tm) * n * ng;
         b16 += size_t(tm) * n * ng;
     } else {
-        c_begin = tm * 16;
-        c_end = min(c_begin + 16, m);
+        c_begin = tm * 16 * XB;
+        c_end = min(c_begin + 16 * XB, m);
     }
     const int nsw = ng >> 2;
     const int per = (nsw + nw - 1) / nw;      // contiguous sweeps per wave
@@ -417,11 +418,11 @@ __global__ void __launch_bounds__((ROUTED || XT) ? 512 : 1024) gemm_a16_slab_st(
     const uint32_t stg = tbase + uint32_t(nw) * kTab + uint32_t(wave) * kStage;
     const uint32_t mst = stg + 16u * CS;      // batch scales [row][sweep][group]
     const uint32_t mab = mst + kMeta;         // batch a | b << 16, same layout
-    const uint32_t xst = mab + kMeta;         // XT: activation pieces [q * 16 + row][80 bytes]
+    const uint32_t xst = mab + kMeta;         // XT: activation pieces [block][q * 16 + row][80 bytes]
 
     uint32_t cr[T][4];                        // codes of one sweep as loaded
     uint32_t ms4[4], ma2[2], mb2[2];          // metadata of one batch as loaded
-    uint32_t xw[2][16];                       // activations of two chunks
+    uint32_t xw[2][XB][16];                   // activations of two chunks
 
     // codes of sweep sw (out-of-range sweeps and rows read zeros)
     auto load_codes = [&](int sw) {
@@ -466,7 +467,7 @@ __global__ void __launch_bounds__((ROUTED || XT) ? 512 : 1024) gemm_a16_slab_st(
     // x row of this lane's MFMA row in the current 16 rows (-1: none); with
     // XT, the rows of the four pieces this lane loads (row 4 i + lane / 16)
     int xr = -1;
-    int xrl[4] = {-1, -1, -1, -1};
+    int xrl[XB][4];
     // activations of chunk c (sweep sa + c / UPG, unit c % UPG of each lane's
     // group).  XT: a wave load brings 64-byte pieces (row r, group q) as four
     // lanes' 16-byte parts, the parts of one row's four groups lying 2G bytes
@@ -478,21 +479,23 @@ __global__ void __launch_bounds__((ROUTED || XT) ? 512 : 1024) gemm_a16_slab_st(
         if constexpr (XT) {
             const int gq = (lane >> 2) & 3, sub = lane & 3;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int row = xrl[i];
-                const bool ok = row >= 0 && sw < sb;
-                load_words<4>(rx,
-                              ok ? (uint32_t(row) * uint32_t(k) + uint32_t(4 * sw + gq) * G + uint32_t(u) * 32u) * 2u +
-                                       16u * uint32_t(sub)
-                                 : kOobOffset,
-                              &xw[SL][4 * i]);
-            }
+            for (int b = 0; b < XB; ++b)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int row = xrl[b][i];
+                    const bool ok = row >= 0 && sw < sb;
+                    load_words<4>(rx,
+                                  ok ? (uint32_t(row) * uint32_t(k) + uint32_t(4 * sw + gq) * G + uint32_t(u) * 32u) * 2u +
+                                           16u * uint32_t(sub)
+                                     : kOobOffset,
+                                  &xw[SL][b][4 * i]);
+                }
         } else {
             const int row = xr;
             const bool ok = row >= 0 && sw < sb;
             load_words<16>(rx, ok ? (uint32_t(row) * uint32_t(k) + uint32_t(4 * sw + q) * G + uint32_t(u) * 32u) * 2u
                                   : kOobOffset,
-                           xw[SL]);
+                           xw[SL][0]);
         }
     };
 
@@ -529,30 +532,36 @@ __global__ void __launch_bounds__((ROUTED || XT) ? 512 : 1024) gemm_a16_slab_st(
     uint32_t nmask;
     __asm__("v_mov_b32 %0, 0x0f0f0f0f" : "=v"(nmask));
     const uint32_t tag = uint32_t(wave) * 0x10101010u;
-    f32x4_t acc;
+    f32x4_t acc[XB];
 
     // decode unit u of the staged sweep and multiply with activation slot SL
     auto compute = [&](int u, auto slot_c) {
         constexpr int SL = decltype(slot_c)::value;
-        u32x4 xa[4];  // this lane's activations of the chunk's four MFMAs
+        u32x4 xa[XB][4];  // this lane's activations of the chunk's four MFMAs, per x-row block
         if constexpr (XT) {
             // pieces to their slots q * 16 + row (80-byte slots: the 16 lanes
             // of one block read 16 disjoint 4-bank ranges), then this lane's
             const int gq = (lane >> 2) & 3, sub = lane & 3;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const uint32_t slot = uint32_t(gq) * 16u + uint32_t(4 * i + (lane >> 4));
-                *reinterpret_cast<lds_u32x4 *>(uintptr_t(xst + slot * 80u + 16u * uint32_t(sub))) =
-                    u32x4{xw[SL][4 * i], xw[SL][4 * i + 1], xw[SL][4 * i + 2], xw[SL][4 * i + 3]};
-            }
-            wave_lds_fence();
-            const uint32_t mine = xst + (uint32_t(q) * 16u + uint32_t(nl)) * 80u;
+            for (int b = 0; b < XB; ++b)
 #pragma unroll
-            for (int st = 0; st < 4; ++st) xa[st] = *reinterpret_cast<const lds_u32x4 *>(uintptr_t(mine + 16u * st));
+                for (int i = 0; i < 4; ++i) {
+                    const uint32_t slot = uint32_t(64 * b) + uint32_t(gq) * 16u + uint32_t(4 * i + (lane >> 4));
+                    *reinterpret_cast<lds_u32x4 *>(uintptr_t(xst + slot * 80u + 16u * uint32_t(sub))) =
+                        u32x4{xw[SL][b][4 * i], xw[SL][b][4 * i + 1], xw[SL][b][4 * i + 2], xw[SL][b][4 * i + 3]};
+                }
+            wave_lds_fence();
+#pragma unroll
+            for (int b = 0; b < XB; ++b) {
+                const uint32_t mine = xst + (uint32_t(64 * b) + uint32_t(q) * 16u + uint32_t(nl)) * 80u;
+#pragma unroll
+                for (int st = 0; st < 4; ++st)
+                    xa[b][st] = *reinterpret_cast<const lds_u32x4 *>(uintptr_t(mine + 16u * st));
+            }
         } else {
 #pragma unroll
             for (int st = 0; st < 4; ++st)
-                xa[st] = u32x4{xw[SL][4 * st], xw[SL][4 * st + 1], xw[SL][4 * st + 2], xw[SL][4 * st + 3]};
+                xa[0][st] = u32x4{xw[SL][0][4 * st], xw[SL][0][4 * st + 1], xw[SL][0][4 * st + 2], xw[SL][0][4 * st + 3]};
         }
         const uint32_t ca = stg + uint32_t(nl) * CS + uint32_t(q) * GB + uint32_t(u) * (4u * B);
         uint32_t cw[B];
@@ -594,25 +603,31 @@ __global__ void __launch_bounds__((ROUTED || XT) ? 512 : 1024) gemm_a16_slab_st(
                 bh[p] = __builtin_amdgcn_perm(ent[8 * st + 2 * p + 1], ent[8 * st + 2 * p], 0x05040100u);
                 bl[p] = __builtin_amdgcn_perm(ent[8 * st + 2 * p + 1], ent[8 * st + 2 * p], 0x07060302u);
             }
-            acc = mma<XDT>(xa[st], bh, acc);
-            acc = mma<XDT>(xa[st], bl, acc);
+#pragma unroll
+            for (int b = 0; b < XB; ++b) {
+                acc[b] = mma<XDT>(xa[b][st], bh, acc[b]);
+                acc[b] = mma<XDT>(xa[b][st], bl, acc[b]);
+            }
         }
         if constexpr (XT) wave_lds_fence();  // the pieces are read before the next chunk's are written
     };
 
-  for (int c0 = c_begin; c0 < c_end; c0 += 16) {
+  for (int c0 = c_begin; c0 < c_end; c0 += 16 * XB) {
     if constexpr (XT) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int r = c0 + 4 * i + (lane >> 4);
-            if constexpr (ROUTED) xrl[i] = r < c_end ? rtok[rorder[r]] : -1;
-            else xrl[i] = r < c_end ? r : -1;
-        }
+        for (int b = 0; b < XB; ++b)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r = c0 + 16 * b + 4 * i + (lane >> 4);
+                if constexpr (ROUTED) xrl[b][i] = r < c_end ? rtok[rorder[r]] : -1;
+                else xrl[b][i] = r < c_end ? r : -1;
+            }
     } else {
         if constexpr (ROUTED) xr = c0 + nl < c_end ? rtok[rorder[c0 + nl]] : -1;
         else xr = c0 + nl < c_end ? c0 + nl : -1;
     }
-    acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int b = 0; b < XB; ++b) acc[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     if (nmy > 0) {
         if constexpr (B >= 2) {
             lds_st(col, 0u);
@@ -658,10 +673,10 @@ __global__ void __launch_bounds__((ROUTED || XT) ? 512 : 1024) gemm_a16_slab_st(
     }
 
     // ---- cross-wave sum and store
-    auto store_block = [&](const f32x4_t &v) {
+    auto store_block = [&](int b, const f32x4_t &v) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const int rr = c0 + 4 * q + e;
+            const int rr = c0 + 16 * b + 4 * q + e;
             const int cl = n0 + nl;
             if (rr < c_end && cl < n) {
                 const int row = ROUTED ? rorder[rr] : rr;
@@ -670,17 +685,19 @@ __global__ void __launch_bounds__((ROUTED || XT) ? 512 : 1024) gemm_a16_slab_st(
         }
     };
     if (nw == 1) {
-        store_block(acc);
+#pragma unroll
+        for (int b = 0; b < XB; ++b) store_block(b, acc[b]);
         continue;
     }
     __syncthreads();
     lds_f32x4 *red = reinterpret_cast<lds_f32x4 *>(uintptr_t(tbase));
-    red[wave * 64 + lane] = acc;
+#pragma unroll
+    for (int b = 0; b < XB; ++b) red[(wave * XB + b) * 64 + lane] = acc[b];
     __syncthreads();
-    if (wave == 0) {
+    for (int b = wave; b < XB; b += nw) {
         f32x4_t v = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        for (int w = 0; w < nw; ++w) v += red[w * 64 + lane];
-        store_block(v);
+        for (int w = 0; w < nw; ++w) v += red[(w * XB + b) * 64 + lane];
+        store_block(b, v);
     }
     __syncthreads();  // the sums are read before the next rows' tables reuse the space
   }
@@ -742,14 +759,14 @@ hipError_t slab_bits(const cq_weight &w, const void *x, int64_t m, void *y, hipS
 
 // staged variant: groups of at most 128 codes with at most 256 code bytes per
 // row and sweep (larger ones spill registers in the unrolled sweep loop)
-template <int B, int UPG, int XDT, int YDT, bool XT>
+template <int B, int UPG, int XDT, int YDT, bool XT, int XB = 1>
 hipError_t slab_st_launch_x(const cq_weight &w, const void *x, int64_t m, void *y, hipStream_t stream) {
     constexpr int NE = 1 << B;
     constexpr uint32_t kTab = NE * 256u;
     constexpr uint32_t CS = 4 * (32 * UPG) * B / 8 + 16;
-    constexpr uint32_t kStage = 16u * CS + 2u * 16u * 4u * 16u + (XT ? 64u * 80u : 0u);
+    constexpr uint32_t kStage = 16u * CS + 2u * 16u * 4u * 16u + (XT ? XB * 64u * 80u : 0u);
     const int64_t tiles_n = (w.n + 15) / 16;
-    const int64_t tiles = (m + 15) / 16 * tiles_n;
+    const int64_t tiles = (m + 16 * XB - 1) / (16 * XB) * tiles_n;
     if (tiles > 0x7fffffff) return hipErrorInvalidValue;
     const int64_t nsw = w.k / w.group / 4;
     int64_t s = int64_t(device_cu_count()) * 16 / tiles;
@@ -758,17 +775,20 @@ hipError_t slab_st_launch_x(const cq_weight &w, const void *x, int64_t m, void *
     // LDS: tables below 64 KB, whole workgroup within 128 KB
     while (s > 1 && (s * kTab > 65536 || s * (kTab + kStage) > 131072)) --s;
     if (s < 1) s = 1;
-    const size_t lds = size_t(s) * (kTab + kStage) > size_t(s) * 1024 ? size_t(s) * (kTab + kStage) : size_t(s) * 1024;
-    hipLaunchKernelGGL((gemm_a16_slab_st<B, UPG, XDT, YDT, false, XT>), dim3(unsigned(tiles)),
+    const size_t lds = size_t(s) * (kTab + kStage) > size_t(s) * 1024 * XB ? size_t(s) * (kTab + kStage)
+                                                                           : size_t(s) * 1024 * XB;
+    hipLaunchKernelGGL((gemm_a16_slab_st<B, UPG, XDT, YDT, false, XT, XB>), dim3(unsigned(tiles)),
                        dim3(unsigned(64 * s)), lds, stream, w.codes, w.scale, w.a, w.b, int(w.n), int(w.k),
                        static_cast<const uint16_t *>(x), int(m), y, int(tiles_n), nullptr, nullptr, nullptr);
     return hipGetLastError();
 }
 
 // more than 8 rows: activations through the transposing LDS pieces (they
-// cost a wave per SIMD of occupancy, which 5..8 rows do not win back)
+// cost a wave per SIMD of occupancy, which 5..8 rows do not win back); more
+// than 16: two x-row blocks per wave share every decoded weight operand
 template <int B, int UPG, int XDT, int YDT>
 hipError_t slab_st_launch(const cq_weight &w, const void *x, int64_t m, void *y, hipStream_t stream) {
+    if (m > 16) return slab_st_launch_x<B, UPG, XDT, YDT, true, 2>(w, x, m, y, stream);
     if (m > 8) return slab_st_launch_x<B, UPG, XDT, YDT, true>(w, x, m, y, stream);
     return slab_st_launch_x<B, UPG, XDT, YDT, false>(w, x, m, y, stream);
 }
@@ -792,7 +812,7 @@ hipError_t slab_st_routed_launch_x(const cq_weight &w, int n_experts, const void
     while (s > 1 && (s * kTab > 65536 || s * (kTab + kStage) > 131072)) --s;
     if (s < 1) s = 1;
     const size_t lds = size_t(s) * (kTab + kStage) > size_t(s) * 1024 ? size_t(s) * (kTab + kStage) : size_t(s) * 1024;
-    hipLaunchKernelGGL((gemm_a16_slab_st<B, UPG, XDT, YDT, true, XT>), dim3(unsigned(blocks)),
+    hipLaunchKernelGGL((gemm_a16_slab_st<B, UPG, XDT, YDT, true, XT, 1>), dim3(unsigned(blocks)),
                        dim3(unsigned(64 * s)), lds, stream, w.codes, w.scale, w.a, w.b, int(w.n), int(w.k),
                        static_cast<const uint16_t *>(x), int(tokens), y, int(tiles_n), token, order, offsets);
     return hipGetLastError();
@@ -883,7 +903,7 @@ hipError_t launch_a16_slab_1x2(const cq_weight &w, const void *x, int x_dt, int6
                                hipStream_t stream);
 hipError_t launch_a16_slab_2x1(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                                hipStream_t stream);
-// the staged variant (m <= 16, G <= 128, G B <= 512, a multiple of four groups per row)
+// the staged variant (m <= 32, G <= 128, G B <= 512, a multiple of four groups per row)
 bool a16_slab_st_fits(const cq_weight &w, int64_t m);
 hipError_t launch_a16_slab_st(const cq_weight &w, const void *x, int x_dt, int64_t m, void *y, int y_dt,
                               hipStream_t stream);

@@ -4,7 +4,7 @@
 namespace cq {
 
 bool a16_slab_st_fits(const cq_weight &w, int64_t m) {
-    return m <= 16 && w.bits <= 5 && w.group <= 128 && w.group * w.bits <= 512 && (w.k / w.group) % 4 == 0;
+    return m <= 32 && w.bits <= 5 && w.group <= 128 && w.group * w.bits <= 512 && (w.k / w.group) % 4 == 0;
 }
 
 bool gemm_a16_slab_staged_supported(const cq_weight &w, int64_t m) {
@@ -13,10 +13,16 @@ bool gemm_a16_slab_staged_supported(const cq_weight &w, int64_t m) {
 
 bool gemm_a16_slab_staged_preferred(const cq_weight &w, int64_t m) {
     if (!gemm_a16_slab_staged_supported(w, m)) return false;
-    // the launch's split of K: about 16 waves per compute unit over the chip
-    const int64_t tiles = (w.n + 15) / 16 * ((m + 15) / 16);
+    // the second x-row block pays for itself on short K too once it is
+    // mostly full (measured on 4096 and 6144 weight rows over K = 4096)
+    if (m >= 28 || (m >= 24 && w.n > 4096)) return true;
+    // the launch's split of K: about 16 waves per compute unit over the chip,
+    // at most 8 with the transposing activation loads (above 8 rows); above
+    // 16 rows a wave serves 32
+    const int64_t tiles = (w.n + 15) / 16 * (m > 16 ? 1 : (m + 15) / 16);
     int64_t s = int64_t(256) * 16 / tiles;
-    if (s > 16) s = 16;
+    const int64_t s_max = m > 8 ? 8 : 16;
+    if (s > s_max) s = s_max;
     if (s < 1) s = 1;
     const int64_t nsw = w.k / w.group / 4;
     return (nsw + s - 1) / s >= 2;

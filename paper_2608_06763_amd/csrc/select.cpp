@@ -66,9 +66,11 @@ int default_family(int path, const cq_weight &w, int64_t m, int64_t gemv_max_row
             return CQ_FAMILY_GEMV_GENERIC;
         }
         // 17..32 rows: the lane-decoded GEMM splits K over the waves of a
-        // workgroup, which the tiled GEMM lacks; it wins by 2-3x on layers
-        // of up to 14336 weight rows and ties on 28672 rows
-        if (m > kGemvMaxRows && w.n < 16384 && gemm_a16_slab_supported(w, m)) return CQ_FAMILY_GEMM_SLAB;
+        // workgroup, which the tiled GEMM lacks (2-3x on up to 14336 weight
+        // rows); its staged two-block form leads wherever the K split leaves
+        // each wave two or more sweeps (28672 weight rows included)
+        if (m > kGemvMaxRows && gemm_a16_slab_staged_preferred(w, m)) return CQ_FAMILY_GEMM_SLAB_STAGED;
+        if (m > kGemvMaxRows && gemm_a16_slab_supported(w, m)) return CQ_FAMILY_GEMM_SLAB;
         return gemm_a16_mfma_supported(w, m) ? CQ_FAMILY_GEMM_MFMA : CQ_FAMILY_GEMM_TILED;
     }
     // Dynamic A8: a partials dump is written by the generic GEMV, the W4

@@ -270,7 +270,10 @@ def test_builtin_rules(clean_table, bits, group, m, md, a8):
 @pytest.mark.parametrize("n,k,m,want", [
     (28672, 8192, 4, "gemm_slab_staged"), (28672, 4096, 16, "gemm_slab_staged"), (4096, 14336, 2, "gemm_slab_staged"),
     (6144, 4096, 4, "gemm_slab"), (4096, 4096, 8, "gemm_slab"), (28672, 8192, 1, "gemv_stream"),
-    (28672, 8192, 24, "gemm_mfma")])
+    (28672, 8192, 24, "gemm_slab_staged"), (4096, 4096, 17, "gemm_slab"), (6144, 4096, 21, "gemm_slab"), (6144, 4096, 24, "gemm_slab_staged"), (4096, 4096, 24, "gemm_slab"),
+    (4096, 4096, 32, "gemm_slab_staged"),
+    (4096, 14336, 17, "gemm_slab_staged"),
+    (28672, 8192, 33, "gemm_mfma")])
 def test_builtin_slab_variant(clean_table, n, k, m, want):
     # the staged variant when every wave of the K split gets two sweeps
     assert cq.cq_select_query(cq.CQ_PATH_MODEL_DTYPE, _fake(4, 128, n, k), m) == want
@@ -289,7 +292,7 @@ def test_builtin_rules_follow_gemv_threshold(clean_table):
     d = _fake(4, 128, 4096, 4096)
     cq.cq_set_gemv_max_rows(0, 0)
     assert cq.cq_select_query(cq.CQ_PATH_MODEL_DTYPE, d, 1) == "gemm_mfma"
-    assert cq.cq_select_query(cq.CQ_PATH_MODEL_DTYPE, _fake(4, 128, 28672, 4096), 24) == "gemm_mfma"
+    assert cq.cq_select_query(cq.CQ_PATH_MODEL_DTYPE, _fake(4, 128, 28672, 4096), 24) == "gemm_slab_staged"
     assert cq.cq_select_query(cq.CQ_PATH_A8, d, 1) == "gemv_stream"
 
 
@@ -308,7 +311,8 @@ def test_family_predicates():
     assert not cq.cq_family_supported(md, "gemm_slab", d, 33)
     assert not cq.cq_family_supported(a8, "gemm_slab", d, 8)
     assert cq.cq_family_supported(md, "gemm_slab_staged", d, 16)
-    assert not cq.cq_family_supported(md, "gemm_slab_staged", d, 17)
+    assert cq.cq_family_supported(md, "gemm_slab_staged", d, 32)
+    assert not cq.cq_family_supported(md, "gemm_slab_staged", d, 33)
     assert not cq.cq_family_supported(md, "gemm_slab_staged", _fake(4, 256, 4096, 4096), 2)
     assert not cq.cq_family_supported(md, "gemm_slab_staged", _fake(4, 128, 4096, 640), 2)
     assert not cq.cq_family_supported(a8, "gemm_slab_staged", d, 8)

@@ -777,7 +777,7 @@ def test_gemm_slab(torch_dev, bits, group, k, m):
 
 @pytest.mark.parametrize("bits", [1, 2, 3, 4, 5])
 @pytest.mark.parametrize("group,k", [(32, 1024), (64, 1024), (128, 2048)])
-@pytest.mark.parametrize("m", [1, 7, 12, 16])
+@pytest.mark.parametrize("m", [1, 7, 12, 16, 21, 32])
 def test_gemm_slab_staged(torch_dev, bits, group, k, m):
     # codes and metadata staged through LDS: 83 weight rows (ragged block),
     # four or more sweeps; W5 stages groups of up to 64 codes
@@ -798,7 +798,8 @@ def test_gemm_slab_staged(torch_dev, bits, group, k, m):
     assert R.eps_comp(_np(y16), y_ref, "bf16") <= TOL
 
 
-@pytest.mark.parametrize("bits,group,k,m", [(4, 32, 4096, 5), (4, 128, 8192, 16), (3, 64, 8192, 2)])
+@pytest.mark.parametrize("bits,group,k,m", [(4, 32, 4096, 5), (4, 128, 8192, 16), (3, 64, 8192, 2),
+                                             (4, 128, 8192, 24), (3, 64, 8192, 32), (5, 64, 4096, 19)])
 def test_gemm_slab_staged_many_sweeps(torch_dev, bits, group, k, m):
     # 8200 weight rows (513 row blocks, few waves per block): every wave walks
     # several sweeps and crosses metadata batches; sampled output columns
@@ -821,7 +822,7 @@ def test_gemm_slab_staged_many_sweeps(torch_dev, bits, group, k, m):
     assert np.max(np.abs(y - y1)) <= 1e-4 * np.max(np.abs(y1))
 
 
-@pytest.mark.parametrize("n,k,m", [(40, 8192, 5), (300, 4096, 32), (16, 1024, 1), (1024, 4096, 16)])
+@pytest.mark.parametrize("n,k,m", [(40, 8192, 5), (300, 4096, 32), (16, 1024, 1), (1024, 4096, 16), (72, 8192, 23)])
 def test_gemm_slab_split_k_and_fp16(torch_dev, n, k, m):
     # few weight rows over long K: up to 16 waves per workgroup split K and
     # meet in LDS; FP16 activations carry the weight as an FP16 hi + lo pair
@@ -839,6 +840,9 @@ def test_gemm_slab_split_k_and_fp16(torch_dev, n, k, m):
         assert R.eps_comp(_np(y16), y_ref, dtype) <= TOL
         y2 = cq.cq_gemm_model_dtype_family(w, _x(torch_dev, xb, dtype), "gemm_slab", y_dtype=torch_dev.float32)
         assert torch_dev.equal(y, y2)
+        # the staged variant (two x-row blocks per wave above 16 rows)
+        ys = cq.cq_gemm_model_dtype_family(w, _x(torch_dev, xb, dtype), "gemm_slab_staged", y_dtype=torch_dev.float32)
+        assert R.eps_comp(_np(ys), y_ref, "fp32") <= 2e-4
 
 
 @pytest.mark.parametrize("bits,group", [(4, 128), (3, 64), (4, 512), (3, 256)])
