@@ -336,6 +336,13 @@ int64_t cq_get_gemv_max_rows(int32_t path);
  *                 Above 16 rows each wave serves two 16-row blocks of x.
  *                 The built-in rules pick it when the K split gives the
  *                 waves two or more sweeps of four groups each.
+ *   GEMV_ROWS     model dtype only, m == 1, K <= 16384: GEMV_STREAM with one
+ *                 wave per 2048-code column block of K in every workgroup;
+ *                 each wave converts its slice of x once and streams only
+ *                 codes and metadata over many row tiles, and the waves'
+ *                 sums meet in LDS; numerics as GEMV_STREAM.  The built-in
+ *                 rules pick it when every workgroup gets three or more row
+ *                 tiles.
  * Families that read 32-bit buffer offsets also need tensors below 2 GiB.
  */
 typedef enum { CQ_PATH_MODEL_DTYPE = 0, CQ_PATH_A8 = 1 } cq_path;
@@ -353,7 +360,8 @@ typedef enum {
     CQ_FAMILY_GEMM_MFMA_M128 = 10,
     CQ_FAMILY_GEMM_MFMA_M256 = 11,
     CQ_FAMILY_GEMM_SLAB = 12,
-    CQ_FAMILY_GEMM_SLAB_STAGED = 13
+    CQ_FAMILY_GEMM_SLAB_STAGED = 13,
+    CQ_FAMILY_GEMV_ROWS = 14
 } cq_family;
 
 /*

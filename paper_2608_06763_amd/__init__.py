@@ -40,7 +40,7 @@ CQ_PATH_MODEL_DTYPE, CQ_PATH_A8 = 0, 1
 FAMILIES = {"auto": 0, "gemv_stream": 1, "gemv_lut": 2, "gemv_narrow": 3, "gemv_generic": 4, "gemm_mfma": 5,
             "gemm_tiled": 6, "gemm_mfma_rounded": 7, "gemm_mfma_m32": 8, "gemm_mfma_m64": 9, "gemm_mfma_m128": 10,
             "gemm_mfma_m256": 11, "gemm_slab": 12,
-            "gemm_slab_staged": 13}
+            "gemm_slab_staged": 13, "gemv_rows": 14}
 FAMILY_NAMES = {v: k for k, v in FAMILIES.items()}
 
 

@@ -23,6 +23,12 @@ hipError_t launch_gemv_a16_generic(const cq_weight &w, const void *x, int x_dt, 
 bool gemv_a16_stream_supported(const cq_weight &w, int64_t m);
 hipError_t launch_gemv_a16_stream(const cq_weight &w, const void *x, int x_dt, void *y, int y_dt,
                                   hipStream_t stream);
+// The same kernel with the activation slice resident in registers (one wave
+// per 2048-code column block, K <= 16384).
+bool gemv_a16_rows_supported(const cq_weight &w, int64_t m);
+bool gemv_a16_rows_preferred(const cq_weight &w, int64_t m);
+hipError_t launch_gemv_a16_rows(const cq_weight &w, const void *x, int x_dt, void *y, int y_dt,
+                                hipStream_t stream);
 
 // Model-dtype table-decode GEMV (m <= 4); see gemv_a16_lut.hip.
 bool gemv_a16_lut_supported(const cq_weight &w, int64_t m);

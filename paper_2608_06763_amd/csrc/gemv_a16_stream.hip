@@ -27,6 +27,8 @@
 // weight, and the reads are issued 16 weights ahead of the products that
 // consume them.  B >= 6 evaluates the cubic in registers instead of keeping a
 // 64..256-entry table.
+#include <algorithm>
+
 #include "cq_device.h"
 #include "cq_internal.h"
 #include "stream_common.h"
@@ -52,17 +54,26 @@ __device__ __forceinline__ void wave_lds_fence() {
 
 }  // namespace
 
+// XRES (resident activations, not routed): the workgroup has one wave per
+// column block and every wave keeps its block for the whole launch, so the
+// wave converts its slice of x to FP32 once and then streams only codes and
+// metadata, tile after tile; the per-tile sums of the waves meet in LDS in
+// batches of kResBatch tiles (two alternating buffers, one barrier a batch).
+//
 // ROUTED: a bank of n_experts matrices of n rows each (expert e at row e * n)
 // and `routes` (token, expert) pairs; route r computes x[token] W_expert^T
 // into row r of y, every route streaming its expert's weights (the decode
 // case of a few routes per expert).  Routes naming a token or expert out of
 // range are skipped and their output row is not written.
-template <int B, int UPG, int RW, int XDT, int YDT, bool ROUTED>
-__global__ void __launch_bounds__(256) gemv_a16_stream(
+constexpr int kResBatch = 4;
+
+template <int B, int UPG, int RW, int XDT, int YDT, bool ROUTED, bool XRES>
+__global__ void __launch_bounds__(XRES ? 512 : 256) gemv_a16_stream(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
     int n, int k, const uint16_t *__restrict__ x, void *__restrict__ y,
     const int32_t *__restrict__ rtok, const int32_t *__restrict__ rexp, int routes, int tokens, int n_experts) {
+    static_assert(!(XRES && ROUTED), "resident activations serve the single-matrix product");
     constexpr int G = UPG * 32;
     constexpr int M = max_code(B);
     constexpr bool LUT = (B <= 5);
@@ -77,7 +88,8 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));  // uniform: rows stay scalar
-    const int nwaves = blockDim.x >> 6;  // the host keeps nwaves <= ncb
+    const int nwaves = blockDim.x >> 6;  // the host keeps nwaves <= ncb (XRES: == ncb)
+    // cross-wave sums: [nwaves][RW], XRES [2][nwaves][kResBatch * RW]
     float *red = tab + nwaves * RW * NT * 64;
     const int ntiles = (n + RW - 1) / RW;
     // item space: the row tiles, or (route, row tile) pairs, route-major
@@ -121,7 +133,7 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
         uint32_t w[RW][B];
         float s[RW];
         uint32_t a[RW], b[RW];
-        uint32_t x[16];
+        uint32_t x[XRES ? 1 : 16];
         bool ok;  // routed: the route names a valid token and expert
     };
     // route and row tile of an item (routed), else the row tile itself
@@ -165,23 +177,43 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
             it.a[r] = load_u16_s(ra, vh, gi * 2u);
             it.b[r] = load_u16_s(rb, vh, gi * 2u);
         }
-        load_words_s<16>(rx, xo, x_base, it.x);
+        if constexpr (!XRES) load_words_s<16>(rx, xo, x_base, it.x);
     };
+
+    // XRES: the wave's slice of x (column block `wave`), FP32, for the launch
+    float xr[XRES ? 32 : 1];
+    if constexpr (XRES) {
+        const int u = wave * 64 + lane;
+        uint32_t xw[16];
+        load_words_s<16>(rx, u < units ? uint32_t(u) * 64u : kOobOffset, 0u, xw);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            xr[2 * e] = act_to_f32<XDT>(uint16_t(xw[e] & 0xffffu));
+            xr[2 * e + 1] = act_to_f32<XDT>(uint16_t(xw[e] >> 16));
+        }
+    }
+    int slot = 0, flushes = 0;  // XRES: tiles recorded in the current batch, batches done
 
     float acc[RW];
 #pragma unroll
     for (int i = 0; i < RW; ++i) acc[i] = 0.f;
 
-    auto process = [&](const Item &it, int ti, bool last_cb) CQ_INLINE {
+    auto process = [&](const Item &it, int ti, bool last_cb, bool final) CQ_INLINE {
         int route, tile;
         split(ti, route, tile);
         // ---- activations of this unit, FP32 in registers
-        float xf[32];
+        float xu[XRES ? 1 : 32];
+        if constexpr (!XRES) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            xf[2 * e] = act_to_f32<XDT>(uint16_t(it.x[e] & 0xffffu));
-            xf[2 * e + 1] = act_to_f32<XDT>(uint16_t(it.x[e] >> 16));
+            for (int e = 0; e < 16; ++e) {
+                xu[2 * e] = act_to_f32<XDT>(uint16_t(it.x[e] & 0xffffu));
+                xu[2 * e + 1] = act_to_f32<XDT>(uint16_t(it.x[e] >> 16));
+            }
         }
+        auto xf = [&](int i) CQ_INLINE {
+            if constexpr (XRES) return xr[i];
+            else return xu[i];
+        };
         // ---- level tables of all rows of the tile first (one slot per row), so
         // that the LDS writes of one row overlap the reads of the previous one
         float al_r[RW], be_r[RW], ga_r[RW];
@@ -273,7 +305,7 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                 for (int e = 0; e < BT; ++e) {
                     const int wi = c * BT + e;
                     const int r = wi / 32, i = wi % 32;
-                    pp[r][i & 1] = __builtin_fmaf(xf[i], src[e], pp[r][i & 1]);
+                    pp[r][i & 1] = __builtin_fmaf(xf(i), src[e], pp[r][i & 1]);
                 }
             };
             reads(0, lvb[0]);
@@ -316,8 +348,8 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                     }
 #pragma unroll
                     for (int e = 0; e < 8; e += 2) {
-                        p0 = __builtin_fmaf(xf[i8 * 8 + e], lv[e], p0);
-                        p1 = __builtin_fmaf(xf[i8 * 8 + e + 1], lv[e + 1], p1);
+                        p0 = __builtin_fmaf(xf(i8 * 8 + e), lv[e], p0);
+                        p1 = __builtin_fmaf(xf(i8 * 8 + e + 1), lv[e + 1], p1);
                     }
                 }
                 acc[r] = __builtin_fmaf(it.s[r], p0 + p1, acc[r]);
@@ -339,7 +371,32 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
                     store_row_pair<YDT>(y, row0, v0, v1, row0 + 1 < n);
                 }
             };
-            if (nwaves == 1) {
+            if constexpr (XRES) {
+                // record the wave's sums of this tile; every kResBatch tiles
+                // (and after the last) the first wave adds the waves' sums
+                float *rb = red + (flushes & 1) * (nwaves * kResBatch * RW);
+#pragma unroll
+                for (int r = 0; r < RW; ++r) {
+                    const float v = wave_sum(acc[r]);
+                    acc[r] = 0.f;
+                    if (lane == 0) rb[wave * (kResBatch * RW) + slot * RW + r] = v;
+                }
+                ++slot;
+                if (slot == kResBatch || final) {
+                    __syncthreads();
+                    if (wave == 0 && lane < slot * RW) {
+                        float v = 0.f;
+                        for (int wv = 0; wv < nwaves; ++wv) v += rb[wv * (kResBatch * RW) + lane];
+                        const int j = lane / RW, r = lane - j * RW;
+                        const int row = (tile - (slot - 1 - j) * int(gridDim.x)) * RW + r;
+                        if (row < n) store_out<YDT>(y, row, v);
+                    }
+                    // the other buffer takes the next batch: the barrier of
+                    // that batch orders these reads before its reuse
+                    ++flushes;
+                    slot = 0;
+                }
+            } else if (nwaves == 1) {
                 const float v0 = wave_sum(acc[0]);
                 const float v1 = wave_sum(acc[1]);
                 acc[0] = 0.f;
@@ -408,14 +465,14 @@ __global__ void __launch_bounds__(256) gemv_a16_stream(
         const bool last0 = t1 != tile;
         const bool have1 = t1 < nitems_t;
         fetch(ib, t1, c1, have1);
-        process(ia, tile, last0);
+        process(ia, tile, last0, !have1);
         if (!have1) break;
         int t2 = t1, c2 = c1;
         advance(t2, c2);
         const bool last1 = t2 != t1;
         const bool have2 = t2 < nitems_t;
         fetch(ia, t2, c2, have2);
-        process(ib, t1, last1);
+        process(ib, t1, last1, !have2);
         if (!have2) break;
         tile = t2;
         cb = c2;
@@ -445,9 +502,35 @@ static hipError_t stream_waves(const cq_weight &w, const void *x, void *y, const
     // one workgroup per tile up to 64 per CU; the kernel strides over the rest
     int64_t blocks = int64_t(device_cu_count()) * 64;
     if (blocks > tiles) blocks = tiles;
-    hipLaunchKernelGGL((gemv_a16_stream<B, UPG, RW, XDT, YDT, ROUTED>), dim3(unsigned(blocks)), dim3(nw * 64), lds,
+    hipLaunchKernelGGL((gemv_a16_stream<B, UPG, RW, XDT, YDT, ROUTED, false>), dim3(unsigned(blocks)), dim3(nw * 64), lds,
                        stream, w.codes, w.scale, w.a, w.b, int(w.n), int(w.k), static_cast<const uint16_t *>(x), y,
                        rt.tok, rt.exp, rt.routes, rt.tokens, rt.n_experts);
+    return hipGetLastError();
+}
+
+// Resident-activation launch: one wave per column block (at most 8), and
+// about 16 waves per compute unit, each workgroup walking a multiple of
+// kResBatch row tiles.
+constexpr int kRowsRW = 2;
+
+static size_t rows_lds_bytes(int bits, int64_t ncb) {
+    const int64_t nt = bits <= 5 ? (int64_t(1) << bits) : 1;
+    return sizeof(float) * size_t(ncb * kRowsRW * nt * 64 + 2 * ncb * kResBatch * kRowsRW);
+}
+
+template <int B, int UPG, int XDT, int YDT>
+static hipError_t rows_waves(const cq_weight &w, const void *x, void *y, hipStream_t stream) {
+    const int64_t ncb = ((w.k >> 5) + 63) >> 6;
+    const int64_t tiles = (w.n + kRowsRW - 1) / kRowsRW;
+    if (tiles < 1) return hipSuccess;
+    int64_t nb = int64_t(device_cu_count()) * 16 / ncb;
+    if (nb < 1) nb = 1;
+    int64_t per = (tiles + nb - 1) / nb;
+    per = (per + kResBatch - 1) / kResBatch * kResBatch;
+    const int64_t blocks = (tiles + per - 1) / per;
+    hipLaunchKernelGGL((gemv_a16_stream<B, UPG, kRowsRW, XDT, YDT, false, true>), dim3(unsigned(blocks)),
+                       dim3(unsigned(ncb * 64)), rows_lds_bytes(B, ncb), stream, w.codes, w.scale, w.a, w.b, int(w.n),
+                       int(w.k), static_cast<const uint16_t *>(x), y, nullptr, nullptr, 0, 0, 0);
     return hipGetLastError();
 }
 
@@ -457,6 +540,33 @@ static hipError_t stream_rows(const cq_weight &w, const void *x, void *y, const 
     // two rows per workgroup: the smallest tile keeps the most workgroups in
     // flight, which is what hides the load latency of a streaming GEMV
     return stream_waves<B, UPG, 2, XDT, YDT, ROUTED>(w, x, y, rt, stream);
+}
+
+template <int B, int XDT, int YDT>
+static hipError_t rows_group(const cq_weight &w, const void *x, void *y, hipStream_t stream) {
+    switch (w.group) {
+        case 32: return rows_waves<B, 1, XDT, YDT>(w, x, y, stream);
+        case 64: return rows_waves<B, 2, XDT, YDT>(w, x, y, stream);
+        case 128: return rows_waves<B, 4, XDT, YDT>(w, x, y, stream);
+        case 256: return rows_waves<B, 8, XDT, YDT>(w, x, y, stream);
+        case 512: return rows_waves<B, 16, XDT, YDT>(w, x, y, stream);
+    }
+    return hipErrorNotSupported;
+}
+
+template <int XDT, int YDT>
+static hipError_t rows_bits(const cq_weight &w, const void *x, void *y, hipStream_t stream) {
+    switch (w.bits) {
+        case 1: return rows_group<1, XDT, YDT>(w, x, y, stream);
+        case 2: return rows_group<2, XDT, YDT>(w, x, y, stream);
+        case 3: return rows_group<3, XDT, YDT>(w, x, y, stream);
+        case 4: return rows_group<4, XDT, YDT>(w, x, y, stream);
+        case 5: return rows_group<5, XDT, YDT>(w, x, y, stream);
+        case 6: return rows_group<6, XDT, YDT>(w, x, y, stream);
+        case 7: return rows_group<7, XDT, YDT>(w, x, y, stream);
+        case 8: return rows_group<8, XDT, YDT>(w, x, y, stream);
+    }
+    return hipErrorNotSupported;
 }
 
 template <int B, int XDT, int YDT, bool ROUTED>
@@ -506,6 +616,34 @@ bool gemv_a16_stream_supported(const cq_weight &w, int64_t m) {
 hipError_t launch_gemv_a16_stream(const cq_weight &w, const void *x, int x_dt, void *y, int y_dt,
                                   hipStream_t stream) {
     return stream_dtypes<false>(w, x, x_dt, y, y_dt, StreamRoutes{}, stream);
+}
+
+bool gemv_a16_rows_supported(const cq_weight &w, int64_t m) {
+    // a wave per column block within one workgroup of at most 8 waves (and
+    // the W4 table slot tag), tables and batch sums within 64 KB of LDS
+    const int64_t ncb = ((w.k >> 5) + 63) >> 6;
+    return m == 1 && stream_fits(w.n, w.k, w.bits, w.group) && ncb <= 8 &&
+           rows_lds_bytes(w.bits, ncb) <= size_t(64) * 1024;
+}
+
+bool gemv_a16_rows_preferred(const cq_weight &w, int64_t m) {
+    if (!gemv_a16_rows_supported(w, m)) return false;
+    // the resident slice pays off once each workgroup walks three or more row
+    // tiles (measured on Llama-3-8B-shaped layers: faster on 4096 x 28672 and
+    // 14336 x 4096, slower on 4096 x 4096 and 4096 x 6144)
+    const int64_t ncb = ((w.k >> 5) + 63) >> 6;
+    const int64_t nb = std::max<int64_t>(1, int64_t(256) * 16 / ncb);
+    return (w.n + kRowsRW - 1) / kRowsRW >= 3 * nb;
+}
+
+hipError_t launch_gemv_a16_rows(const cq_weight &w, const void *x, int x_dt, void *y, int y_dt,
+                                hipStream_t stream) {
+    if (x_dt == 0) {
+        if (y_dt == 0) return rows_bits<0, 0>(w, x, y, stream);
+        return rows_bits<0, 2>(w, x, y, stream);
+    }
+    if (y_dt == 1) return rows_bits<1, 1>(w, x, y, stream);
+    return rows_bits<1, 2>(w, x, y, stream);
 }
 
 bool gemv_a16_stream_routed_supported(const cq_weight &w, int64_t n_experts, int64_t tokens, int64_t routes) {

@@ -30,6 +30,7 @@ bool family_supported(int path, int family, const cq_weight &w, int64_t m) {
             case CQ_FAMILY_GEMM_MFMA_M256: return gemm_a16_mfma_supported(w, m);
             case CQ_FAMILY_GEMM_SLAB: return gemm_a16_slab_supported(w, m);
             case CQ_FAMILY_GEMM_SLAB_STAGED: return gemm_a16_slab_staged_supported(w, m);
+            case CQ_FAMILY_GEMV_ROWS: return gemv_a16_rows_supported(w, m);
         }
         return false;
     }
@@ -54,6 +55,9 @@ int default_family(int path, const cq_weight &w, int64_t m, int64_t gemv_max_row
     const bool gemv = m <= gemv_max_rows && m <= kGemvMaxRows;
     if (path == CQ_PATH_MODEL_DTYPE) {
         if (gemv) {
+            // one row: the resident-activation form on layers with enough
+            // row tiles per workgroup, else the streaming GEMV
+            if (gemv_a16_rows_preferred(w, m)) return CQ_FAMILY_GEMV_ROWS;
             if (gemv_a16_stream_supported(w, m)) return CQ_FAMILY_GEMV_STREAM;
             // 2..16 rows: the lane-decoded matrix-core GEMM measured faster
             // than the table-decode and narrow-row families on every decode
@@ -100,6 +104,7 @@ hipError_t run_family_a16(int family, const cq_weight &w, const void *x, int x_d
             return launch_gemm_a16_mfma(w, x, x_dt, m, y, y_dt, family_tile_rows(family), stream);
         case CQ_FAMILY_GEMM_SLAB: return launch_gemm_a16_slab(w, x, x_dt, m, y, y_dt, stream);
         case CQ_FAMILY_GEMM_SLAB_STAGED: return launch_gemm_a16_slab_staged(w, x, x_dt, m, y, y_dt, stream);
+        case CQ_FAMILY_GEMV_ROWS: return launch_gemv_a16_rows(w, x, x_dt, y, y_dt, stream);
     }
     return hipErrorInvalidValue;
 }
@@ -173,9 +178,10 @@ int table_family(int path, const cq_weight &w, int x_dt, int64_t m) {
 
 bool select_entry_valid(const cq_select_entry &e) {
     if (e.path != CQ_PATH_MODEL_DTYPE && e.path != CQ_PATH_A8) return false;
-    if (e.family < CQ_FAMILY_GEMV_STREAM || e.family > CQ_FAMILY_GEMM_SLAB_STAGED) return false;
+    if (e.family < CQ_FAMILY_GEMV_STREAM || e.family > CQ_FAMILY_GEMV_ROWS) return false;
     if (e.path == CQ_PATH_A8 && (e.family == CQ_FAMILY_GEMV_LUT || e.family == CQ_FAMILY_GEMM_MFMA_ROUNDED ||
-                                 e.family == CQ_FAMILY_GEMM_SLAB || e.family == CQ_FAMILY_GEMM_SLAB_STAGED))
+                                 e.family == CQ_FAMILY_GEMM_SLAB || e.family == CQ_FAMILY_GEMM_SLAB_STAGED ||
+                                 e.family == CQ_FAMILY_GEMV_ROWS))
         return false;
     if (e.bits < 1 || e.bits > 8) return false;
     if (e.group < 32 || e.group > 512 || e.group % 32) return false;

@@ -29,7 +29,7 @@ from . import (CQ_BF16, CQ_FP16, CQ_PATH_A8, CQ_PATH_MODEL_DTYPE, FAMILIES, CQWe
                cq_gemm_a8, cq_gemm_a8_family, cq_gemm_model_dtype, cq_gemm_model_dtype_family, cq_quantize_act_a8,
                cq_select_set)
 
-MODEL_DTYPE_FAMILIES = ("gemv_stream", "gemv_lut", "gemv_narrow", "gemv_generic", "gemm_slab", "gemm_slab_staged",
+MODEL_DTYPE_FAMILIES = ("gemv_stream", "gemv_rows", "gemv_lut", "gemv_narrow", "gemv_generic", "gemm_slab", "gemm_slab_staged",
                         "gemm_mfma",
                         "gemm_mfma_m32", "gemm_mfma_m64", "gemm_mfma_m128", "gemm_mfma_m256", "gemm_tiled")
 # Families timed only when a caller asks for them: the single-rounded operand

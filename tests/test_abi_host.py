@@ -269,7 +269,8 @@ def test_builtin_rules(clean_table, bits, group, m, md, a8):
 
 @pytest.mark.parametrize("n,k,m,want", [
     (28672, 8192, 4, "gemm_slab_staged"), (28672, 4096, 16, "gemm_slab_staged"), (4096, 14336, 2, "gemm_slab_staged"),
-    (6144, 4096, 4, "gemm_slab"), (4096, 4096, 8, "gemm_slab"), (28672, 8192, 1, "gemv_stream"),
+    (6144, 4096, 4, "gemm_slab"), (4096, 4096, 8, "gemm_slab"), (28672, 8192, 1, "gemv_rows"),
+    (4096, 14336, 1, "gemv_rows"), (6144, 4096, 1, "gemv_stream"),
     (28672, 8192, 24, "gemm_slab_staged"), (4096, 4096, 17, "gemm_slab"), (6144, 4096, 21, "gemm_slab"), (6144, 4096, 24, "gemm_slab_staged"), (4096, 4096, 24, "gemm_slab"),
     (4096, 4096, 32, "gemm_slab_staged"),
     (4096, 14336, 17, "gemm_slab_staged"),
@@ -316,6 +317,13 @@ def test_family_predicates():
     assert not cq.cq_family_supported(md, "gemm_slab_staged", _fake(4, 256, 4096, 4096), 2)
     assert not cq.cq_family_supported(md, "gemm_slab_staged", _fake(4, 128, 4096, 640), 2)
     assert not cq.cq_family_supported(a8, "gemm_slab_staged", d, 8)
+    assert cq.cq_family_supported(md, "gemv_rows", d, 1)
+    assert not cq.cq_family_supported(md, "gemv_rows", d, 2)
+    assert not cq.cq_family_supported(a8, "gemv_rows", d, 1)
+    assert cq.cq_family_supported(md, "gemv_rows", _fake(4, 128, 4096, 14336), 1)
+    assert not cq.cq_family_supported(md, "gemv_rows", _fake(4, 128, 4096, 18432), 1)  # nine column blocks
+    assert not cq.cq_family_supported(md, "gemv_rows", _fake(5, 128, 4096, 16384), 1)  # tables above 64 KB
+    assert cq.cq_family_supported(md, "gemv_rows", _fake(6, 128, 4096, 16384), 1)
     assert not cq.cq_family_supported(a8, "gemv_lut", d, 2)
     assert not cq.cq_family_supported(a8, "auto", d, 2)
     assert not cq.cq_family_supported(7, "gemm_tiled", d, 2)
@@ -369,7 +377,7 @@ def test_table_matches_activation_dtype(clean_table):
 
 
 @pytest.mark.parametrize("bad", [
-    dict(path=2), dict(family="auto"), dict(family=14), dict(path=1, family="gemv_lut"),
+    dict(path=2), dict(family="auto"), dict(family=15), dict(path=1, family="gemv_lut"),
     dict(path=1, family="gemm_mfma_rounded"), dict(path=1, family="gemm_slab"),
     dict(path=1, family="gemm_slab_staged"), dict(bits=0),
     dict(bits=9), dict(group=48), dict(group=1024), dict(n=0), dict(k=0), dict(m_lo=0), dict(m_lo=5, m_hi=4),

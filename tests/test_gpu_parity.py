@@ -677,7 +677,7 @@ def test_gemm_a8_carriers_equals_gemm_a8(torch_dev, bits, group, m):
 
 # ---------------------------------------------------------------- kernel families and the selection table
 
-MD_FAMILIES = ("gemv_stream", "gemv_lut", "gemv_narrow", "gemv_generic", "gemm_slab", "gemm_slab_staged", "gemm_mfma",
+MD_FAMILIES = ("gemv_stream", "gemv_rows", "gemv_lut", "gemv_narrow", "gemv_generic", "gemm_slab", "gemm_slab_staged", "gemm_mfma",
                "gemm_mfma_m32",
                "gemm_mfma_m64", "gemm_mfma_m128", "gemm_mfma_m256", "gemm_tiled", "gemm_mfma_rounded")
 A8_FAMILIES = ("gemv_stream", "gemv_narrow", "gemv_generic", "gemm_mfma", "gemm_mfma_m32", "gemm_mfma_m64",
@@ -820,6 +820,55 @@ def test_gemm_slab_staged_many_sweeps(torch_dev, bits, group, k, m):
     assert R.eps_comp(y[:, rows], y_ref, "fp32") <= 2e-4
     assert R.eps_comp(y1[:, rows], y_ref, "fp32") <= 2e-4
     assert np.max(np.abs(y - y1)) <= 1e-4 * np.max(np.abs(y1))
+
+
+@pytest.mark.parametrize("bits", [1, 2, 3, 4, 5, 6, 7, 8])
+@pytest.mark.parametrize("group", [32, 128, 512])
+def test_gemv_rows(torch_dev, bits, group):
+    # resident-activation single-row GEMV: 4608 codes per row are 2.25 column
+    # blocks (three waves, the last one partly past the row), 1601 rows are
+    # 801 row pairs (the last one single), walked in batches of four tiles by
+    # each workgroup; every row against the oracle, and against the streaming
+    # family (the same products summed in another order)
+    from workloads import synthetic_representation
+    n, k = 1601, 4608
+    cq = _cq()
+    codes, sc, a, b = synthetic_representation(600 + bits, n, k, bits, group)
+    w = cq.CQWeight.from_codes(codes, sc, a, b, bits, group)
+    xb, xv = act(601 + bits, 1, k)
+    x = _x(torch_dev, xb, "bf16")
+    say("gemv_rows", bits, group)
+    y = _np(cq.cq_gemm_model_dtype_family(w, x, "gemv_rows", y_dtype=torch_dev.float32))
+    y_ref = R.gemm_model_dtype(xv, codes, bits, group, sc, a, b)
+    assert R.eps_comp(y, y_ref, "fp32") <= 2e-4
+    assert R.eps_comp(_np(cq.cq_gemm_model_dtype_family(w, x, "gemv_rows")), y_ref, "bf16") <= TOL
+    ys = _np(cq.cq_gemm_model_dtype_family(w, x, "gemv_stream", y_dtype=torch_dev.float32))
+    assert np.max(np.abs(y - ys)) <= 1e-5 * np.max(np.abs(ys))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+def test_gemv_rows_many_tiles(torch_dev, dtype):
+    # 20001 rows over 7168 codes (3.5 column blocks): each workgroup walks
+    # about twelve row tiles, three batches, the last partly filled; sampled
+    # rows against the oracle, every row against the streaming family
+    from workloads import synthetic_representation
+    n, k, bits, group = 20001, 7168, 4, 128
+    cq = _cq()
+    codes, sc, a, b = synthetic_representation(610, n, k, bits, group)
+    w = cq.CQWeight.from_codes(codes, sc, a, b, bits, group)
+    xb, xv = act(611, 1, k, dtype)
+    x = _x(torch_dev, xb, dtype)
+    say("gemv_rows many tiles", dtype)
+    assert cq.cq_select_query(cq.CQ_PATH_MODEL_DTYPE, w, 1) == "gemv_rows"
+    y = _np(cq.cq_gemm_model_dtype(w, x, y_dtype=torch_dev.float32))
+    rows = np.sort(np.random.default_rng(612).choice(n, size=64, replace=False))
+    rows = np.concatenate([rows, [0, 1, 2, 3, n - 2, n - 1]])
+    y_ref = R.gemm_model_dtype(xv, codes[rows], bits, group, sc[rows], a[rows], b[rows])
+    assert R.eps_comp(y[:, rows], y_ref, "fp32") <= 2e-4
+    ys = _np(cq.cq_gemm_model_dtype_family(w, x, "gemv_stream", y_dtype=torch_dev.float32))
+    assert np.max(np.abs(y - ys)) <= 1e-5 * np.max(np.abs(ys))
+    y16 = _np(cq.cq_gemm_model_dtype(w, x))
+    assert R.eps_comp(y16[:, rows], y_ref, dtype) <= TOL
 
 
 @pytest.mark.parametrize("n,k,m", [(40, 8192, 5), (300, 4096, 32), (16, 1024, 1), (1024, 4096, 16), (72, 8192, 23)])
