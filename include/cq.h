@@ -300,7 +300,7 @@ int64_t cq_get_gemv_max_rows(int32_t path);
  *
  * Paths: CQ_PATH_MODEL_DTYPE (cq_gemm_model_dtype), CQ_PATH_A8 (cq_gemm_a8).
  * Families (CQ_FAMILY_AUTO = the built-in rules):
- *   GEMV_STREAM   single-row streaming GEMV (m == 1; A8: B <= 4)
+ *   GEMV_STREAM   single-row streaming GEMV (m == 1)
  *   GEMV_LUT      model dtype only, per-wave level tables (m <= 4, G <= 128;
  *                 m == 1 at G == 256)
  *   GEMV_NARROW   matrix-core narrow-row GEMV (2 <= m <= 16; model dtype

@@ -1,5 +1,5 @@
 // Dynamic-A8 single-row GEMV, streaming byte-permute family (Sec. 5.4) for
-// m == 1 and B in {1, 2, 3, 4}.
+// m == 1 and every B.
 //
 // Numerics are those of eq. a8-output: every weight contributes the INT8
 // carrier r(k) = sign(k) RNE(127 q(|k|/M)) (eq. carrier, Appendix A item 7)
@@ -21,9 +21,11 @@
 // the two interior carriers itself; a field indexes the 8-byte pair
 // [r0 r1 r2 r3 | 0 -r3 -r2 -r1] directly once four fields are spread into
 // bytes, and the carriers come out in field order.  W2 and W1 use constant
-// tables ({0, 127, 0, -127} and {-127, 127}).
+// tables ({0, 127, 0, -127} and {-127, 127}).  W5..W8 (16..128 magnitudes per
+// group, more than a group's 32-code unit uses) evaluate each weight's carrier
+// from its own magnitude, exact near ties as everywhere else.
 //
-// Fused quantization (FX >= 0): the kernel takes the BF16/FP16 activation row
+// Fused quantization (FX >= 0, B <= 4): the kernel takes the BF16/FP16 activation row
 // itself and forms its carriers in a prologue, so that a single-row A8 product
 // is one launch (the activation encoding is the fixed cost of the single-row
 // A8 path, Sec. 6).  Every workgroup reduces the whole row to its maximum
@@ -61,7 +63,7 @@ __device__ __forceinline__ void transpose4(const uint32_t in[4], uint32_t out[4]
 // order in which the decode produces carriers.
 template <int B>
 __device__ __forceinline__ void arrange_x(const uint32_t xw[8], uint32_t xa[8]) {
-    if constexpr (B == 3) {
+    if constexpr (B == 3 || B >= 5) {
         // carriers come out in field order
 #pragma unroll
         for (int i = 0; i < 8; ++i) xa[i] = xw[i];
@@ -155,7 +157,7 @@ __global__ void __launch_bounds__(FX >= 0 ? 64 * kMaxFusedWaves : 256) gemv_a8_s
             const uint32_t gi = uint32_t(row) * ng + uint32_t(u) / UPG;
             load_words<B>(rc, ok ? uint32_t(row) * row_bytes + uint32_t(u) * (4 * B) : kOobOffset, wn[r]);
             sn[r] = load_f32(rs, ok ? gi * 4u : kOobOffset);
-            if constexpr (B == 4 || B == 3) {
+            if constexpr (B >= 3) {
                 an[r] = load_u16(ra, ok ? gi * 2u : kOobOffset);
                 bn[r] = load_u16(rb, ok ? gi * 2u : kOobOffset);
             }
@@ -311,6 +313,63 @@ __global__ void __launch_bounds__(FX >= 0 ? 64 * kMaxFusedWaves : 256) gemv_a8_s
                         (x & 7u) | ((x << 5) & 0x700u) | ((x << 10) & 0x70000u) | ((x << 15) & 0x7000000u);
                     p = __builtin_amdgcn_sdot4(int(perm(tb, ta, sel)), int(xa[q]), p, false);
                 }
+            } else if constexpr (B >= 5) {
+                // 16..128 magnitudes per group: every weight's carrier comes
+                // from its own code, four fields to a word in field order.
+                // The FP32 estimate 127 q(|k|/M) sign(k) uses coefficients
+                // prescaled by 127 / M^j (its error stays below a third of
+                // the doubled margin); when any estimate of the unit lies
+                // within the margin of a half-integer, the unit's carriers
+                // are formed again with the exact test of carrier_u8.
+                const float a = f16_to_f32(uint16_t(av[r]));
+                const float b = f16_to_f32(uint16_t(bv[r]));
+                const float c = 1.f - a - b;
+                const float margin = 2.f * carrier_margin(a, b, c);
+                const float ca = a * (127.0f / float(M));
+                const float cb = b * (127.0f / float(M * M));
+                const float cc = c * (127.0f / float(M * M * M));
+                auto field = [&](int i) __attribute__((always_inline)) {
+                    const int bit = i * B, wi = bit >> 5, sh = bit & 31;
+                    uint32_t v;
+                    if (sh + B <= 32) v = w[r][wi] >> sh;
+                    else v = __builtin_amdgcn_alignbit(w[r][wi + 1], w[r][wi], sh);
+                    const int kk = __builtin_amdgcn_sbfe(int(v), 0, B);
+                    return kk == -(M + 1) ? 0 : kk;  // the reserved pattern carries 0
+                };
+                uint32_t words[8];
+                float worst = 0.f;
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    uint32_t word = 0;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float kf = float(field(4 * q + e));
+                        const float ak = __builtin_fabsf(kf);
+                        const float f = kf * __builtin_fmaf(ak, __builtin_fmaf(ak, cc, cb), ca);
+                        const float rr = __builtin_rintf(f);
+                        worst = __builtin_fmaxf(worst, __builtin_fabsf(f - rr));
+                        const int cr = int(__builtin_fminf(__builtin_fmaxf(rr, -127.f), 127.f));
+                        word |= (uint32_t(cr) & 0xffu) << (8 * e);
+                    }
+                    words[q] = word;
+                }
+                if (__builtin_expect(worst > 0.5f - margin, 0)) {
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) {
+                        uint32_t word = 0;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int kk = field(4 * q + e);
+                            const int mag = kk < 0 ? -kk : kk;
+                            const int cr = int(carrier_u8<M>(mag, float(mag) / float(M), a, b, c,
+                                                             carrier_margin(a, b, c)));
+                            word |= (uint32_t(kk < 0 ? -cr : cr) & 0xffu) << (8 * e);
+                        }
+                        words[q] = word;
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < 8; ++q) p = __builtin_amdgcn_sdot4(int(words[q]), int(xa[q]), p, false);
             } else if constexpr (B == 2) {
                 // fields 0 -> 0, 1 -> +127, 2 (reserved) -> 0, 3 -> -127
                 constexpr uint32_t T = 0x81007f00u;
@@ -415,6 +474,14 @@ static hipError_t a8_stream_bits(const cq_weight &w, const void *xin, float *dxv
         case 3: return a8_stream_group<3, YDT, FX>(w, xin, dxv, x8_out, y, stream);
         case 4: return a8_stream_group<4, YDT, FX>(w, xin, dxv, x8_out, y, stream);
     }
+    if constexpr (FX < 0) {
+        switch (w.bits) {
+            case 5: return a8_stream_group<5, YDT, FX>(w, xin, dxv, x8_out, y, stream);
+            case 6: return a8_stream_group<6, YDT, FX>(w, xin, dxv, x8_out, y, stream);
+            case 7: return a8_stream_group<7, YDT, FX>(w, xin, dxv, x8_out, y, stream);
+            case 8: return a8_stream_group<8, YDT, FX>(w, xin, dxv, x8_out, y, stream);
+        }
+    }
     return hipErrorNotSupported;
 }
 
@@ -427,11 +494,11 @@ static hipError_t a8_stream_ydt(const cq_weight &w, const void *xin, float *dxv,
 }
 
 bool gemv_a8_stream_supported(const cq_weight &w, int64_t m) {
-    return m == 1 && w.bits <= 4 && stream_fits(w.n, w.k, w.bits, w.group);
+    return m == 1 && stream_fits(w.n, w.k, w.bits, w.group);
 }
 
 bool gemv_a8_fused_supported(const cq_weight &w, int64_t m) {
-    return gemv_a8_stream_supported(w, m) && (((w.k >> 5) + 63) >> 6) <= kMaxFusedWaves;
+    return gemv_a8_stream_supported(w, m) && w.bits <= 4 && (((w.k >> 5) + 63) >> 6) <= kMaxFusedWaves;
 }
 
 hipError_t launch_gemv_a8_stream(const cq_weight &w, const int8_t *x8, const float *dx, void *y, int y_dt,

@@ -301,11 +301,12 @@ def test_edge_shapes(torch_dev, n, k, g, m):
 # ---------------------------------------------------------------- single-row A8 streaming family
 
 
-@pytest.mark.parametrize("bits", [1, 2, 3, 4])
+@pytest.mark.parametrize("bits", [1, 2, 3, 4, 5, 6, 7, 8])
 @pytest.mark.parametrize("group", GROUPS)
 @pytest.mark.parametrize("k", [768, 4096 + 2048 + 512])
 def test_gemv_a8_stream(torch_dev, bits, group, k):
-    # m == 1 without a partials dump takes the streaming byte-permute kernel
+    # m == 1 without a partials dump takes the streaming kernel (W1..W4 carrier
+    # tables in registers, W5..W8 one carrier per weight)
     if k % group:
         pytest.skip("K must be a multiple of G")
     r = fitted(23, 67, k, bits, group)
