@@ -740,7 +740,8 @@ def main():
         "eager": {"ms_per_step": round(ms_eager, 5),
                   "gbs": round((bytes_a16 + bytes_a8) / ms_eager / 1e6, 1)},
         "per_layer": per_layer,
-        "roofline": {"bound": "hbm", "kernel": "gemv_a16_stream (model-dtype GEMV, W4 G128, M=1)",
+        "roofline": {"bound": "hbm", "kernel": "gemv_a16_stream (model-dtype GEMV, W4 G128, M=1; streaming form on qkv and o_proj, "
+                     "resident-activation form, family gemv_rows, on gate+up and down)",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "avg_launch_us": round(gemv_ms * 1e3, 3),
                      "timing": "HIP events around K back-to-back passes of its four launches",
