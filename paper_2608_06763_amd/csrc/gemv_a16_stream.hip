@@ -22,8 +22,10 @@
 // all lanes of a group would put those lanes' stores of different fields on
 // the same four banks).  W4/W5 at G = 128 evaluate a quarter of the
 // magnitudes per lane and gather the group's others through DPP, other
-// widths and groups evaluate all of them; W1/W2 tables are constant and
-// written once.  For W4 the address is assembled by one byte permute per
+// widths and groups evaluate all of them.  W1 and W2, whose levels are -1,
+// 0 and +1 for every shape, skip the table: a code pair's levels are formed
+// in the activation dtype from the code bits and meet the activation pair in
+// a two-term dot product (Sec. 5.2 strategy 1).  For W4 the address is assembled by one byte permute per
 // weight, and the reads are issued 16 weights ahead of the products that
 // consume them.  B >= 6 evaluates the cubic in registers instead of keeping a
 // 64..256-entry table.
@@ -40,6 +42,8 @@ namespace cq {
 namespace {
 
 typedef __attribute__((address_space(3))) float lds_f;
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ float lds_ld(uint32_t a) { return *reinterpret_cast<const lds_f *>(uintptr_t(a)); }
 __device__ __forceinline__ void lds_st(uint32_t a, float v) { *reinterpret_cast<lds_f *>(uintptr_t(a)) = v; }
@@ -76,7 +80,10 @@ __global__ void __launch_bounds__(XRES ? 512 : 256) gemv_a16_stream(
     static_assert(!(XRES && ROUTED), "resident activations serve the single-matrix product");
     constexpr int G = UPG * 32;
     constexpr int M = max_code(B);
-    constexpr bool LUT = (B <= 5);
+    // W1/W2 levels are -1, 0, +1 whatever the shape: mapped directly (DIRECT),
+    // no table; W3..W5 use the LDS tables; B >= 6 evaluates the cubic
+    constexpr bool DIRECT = (B <= 2);
+    constexpr bool LUT = (B >= 3 && B <= 5);
     constexpr int NT = LUT ? (1 << B) : 1;
     // every lane owns a full column of the table (no replicated stores, whose
     // lanes of one group all hit the same four banks)
@@ -180,16 +187,30 @@ __global__ void __launch_bounds__(XRES ? 512 : 256) gemv_a16_stream(
         if constexpr (!XRES) load_words_s<16>(rx, xo, x_base, it.x);
     };
 
-    // XRES: the wave's slice of x (column block `wave`), FP32, for the launch
-    float xr[XRES ? 32 : 1];
+    // DIRECT: the unit's activations as 16 pairs (x_j, x_{j+16}) in the
+    // activation dtype, the operands of a two-term dot product whose other
+    // operand holds the levels of codes j and j + 16
+    auto pair_x = [&](const uint32_t (&xw)[16], uint32_t (&xp)[16]) CQ_INLINE {
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+            xp[j] = __builtin_amdgcn_perm(xw[8 + j / 2], xw[j / 2], (j & 1) ? 0x07060302u : 0x05040100u);
+    };
+    // XRES: the wave's slice of x (column block `wave`), FP32 (DIRECT: pairs),
+    // for the launch
+    float xr[XRES && !DIRECT ? 32 : 1];
+    uint32_t xrp[XRES && DIRECT ? 16 : 1];
     if constexpr (XRES) {
         const int u = wave * 64 + lane;
         uint32_t xw[16];
         load_words_s<16>(rx, u < units ? uint32_t(u) * 64u : kOobOffset, 0u, xw);
+        if constexpr (DIRECT) {
+            pair_x(xw, xrp);
+        } else {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            xr[2 * e] = act_to_f32<XDT>(uint16_t(xw[e] & 0xffffu));
-            xr[2 * e + 1] = act_to_f32<XDT>(uint16_t(xw[e] >> 16));
+            for (int e = 0; e < 16; ++e) {
+                xr[2 * e] = act_to_f32<XDT>(uint16_t(xw[e] & 0xffffu));
+                xr[2 * e + 1] = act_to_f32<XDT>(uint16_t(xw[e] >> 16));
+            }
         }
     }
     int slot = 0, flushes = 0;  // XRES: tiles recorded in the current batch, batches done
@@ -202,8 +223,8 @@ __global__ void __launch_bounds__(XRES ? 512 : 256) gemv_a16_stream(
         int route, tile;
         split(ti, route, tile);
         // ---- activations of this unit, FP32 in registers
-        float xu[XRES ? 1 : 32];
-        if constexpr (!XRES) {
+        float xu[XRES || DIRECT ? 1 : 32];
+        if constexpr (!XRES && !DIRECT) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
                 xu[2 * e] = act_to_f32<XDT>(uint16_t(it.x[e] & 0xffffu));
@@ -214,6 +235,59 @@ __global__ void __launch_bounds__(XRES ? 512 : 256) gemv_a16_stream(
             if constexpr (XRES) return xr[i];
             else return xu[i];
         };
+        if constexpr (DIRECT) {
+            // Levels -1, 0, +1 (Sec. 5.2 strategy 1): the pair of levels of
+            // codes j and j + 16 is built in the activation dtype from the
+            // code bits and fed with the pair (x_j, x_{j+16}) to a two-term
+            // dot product with FP32 accumulation (products of a level +-1 or 0
+            // are exact).  W1: code 1 -> +1, 0 -> -1; bit j and bit j + 16 of
+            // the unit's word go to the two sign bits with one shift.  W2:
+            // codes 0, 1, 2 (reserved), 3 -> 0, +1, 0, -1; the two 2-bit codes
+            // (as bytes f, f + 4) select the level bytes from two 4-byte tables.
+            uint32_t xpl[XRES ? 1 : 16];
+            if constexpr (!XRES) pair_x(it.x, xpl);
+            auto xpair = [&](int j) CQ_INLINE {
+                if constexpr (XRES) return xrp[j];
+                else return xpl[j];
+            };
+            constexpr uint32_t kOne = XDT == 0 ? 0x3f803f80u : 0x3c003c00u;
+            constexpr uint32_t kLo = XDT == 0 ? 0x80008000u : 0u;          // low bytes of 0, +1, 0, -1
+            constexpr uint32_t kHi = XDT == 0 ? 0xbf003f00u : 0xbc003c00u;  // high bytes
+            auto dot2 = [&](uint32_t xa, uint32_t lv, float c) CQ_INLINE {
+                if constexpr (XDT == 0)
+                    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, xa),
+                                                           __builtin_bit_cast(bf16x2_t, lv), c, false);
+                else
+                    return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2_t, xa), __builtin_bit_cast(f16x2_t, lv),
+                                                  c, false);
+            };
+#pragma unroll
+            for (int r = 0; r < RW; ++r) {
+                float p0 = 0.f, p1 = 0.f;
+                if constexpr (B == 1) {
+                    const uint32_t nw = ~it.w[r][0];
+#pragma unroll
+                    for (int j = 0; j < 16; ++j) {
+                        const uint32_t lv = ((nw << (15 - j)) & 0x80008000u) | kOne;
+                        if (j & 1) p1 = dot2(xpair(j), lv, p1);
+                        else p0 = dot2(xpair(j), lv, p0);
+                    }
+                } else {
+                    // codes j < 8 and j + 16 in the low and high halves of c0,
+                    // codes 8..15 and 24..31 in those of c1
+                    const uint32_t c0 = __builtin_amdgcn_perm(it.w[r][1], it.w[r][0], 0x05040100u);
+                    const uint32_t c1 = __builtin_amdgcn_perm(it.w[r][1], it.w[r][0], 0x07060302u);
+#pragma unroll
+                    for (int j = 0; j < 16; ++j) {
+                        const uint32_t f = ((j < 8 ? c0 : c1) >> (2 * (j & 7))) & 0x00030003u;
+                        const uint32_t lv = __builtin_amdgcn_perm(kHi, kLo, f * 0x0101u + 0x04000400u);
+                        if (j & 1) p1 = dot2(xpair(j), lv, p1);
+                        else p0 = dot2(xpair(j), lv, p0);
+                    }
+                }
+                acc[r] = __builtin_fmaf(it.s[r], p0 + p1, acc[r]);
+            }
+        }
         // ---- level tables of all rows of the tile first (one slot per row), so
         // that the LDS writes of one row overlap the reads of the previous one
         float al_r[RW], be_r[RW], ga_r[RW];
@@ -232,8 +306,7 @@ __global__ void __launch_bounds__(XRES ? 512 : 256) gemv_a16_stream(
             if constexpr (OWN) {
                 // every lane writes its own column: +q at field i and -q at field
                 // NT - i for i = 1 .. M - 1 (fields 0 and NT/2 hold 0 and fields M
-                // and NT - M hold +1 and -1, and W1/W2 tables are constant, all
-                // written once before the loop)
+                // and NT - M hold +1 and -1, all written once before the loop)
                 if constexpr (B >= 3) {
                     float qa[M + 1];
                     if constexpr (B >= 4 && UPG == 4) {
@@ -271,7 +344,8 @@ __global__ void __launch_bounds__(XRES ? 512 : 256) gemv_a16_stream(
         }
         if constexpr (LUT) wave_lds_fence();
         // ---- decode
-        if constexpr (B == 4) {
+        if constexpr (DIRECT) {
+        } else if constexpr (B == 4) {
             // The 64 weights of the item (both rows) in chunks of 16: the table
             // reads of chunk c + 1 are issued before the products of chunk c, so
             // a wave keeps 16 to 32 LDS reads in flight.
@@ -441,15 +515,7 @@ __global__ void __launch_bounds__(XRES ? 512 : 256) gemv_a16_stream(
 #pragma unroll
         for (int r = 0; r < RW; ++r) {
             const uint32_t own = col + uint32_t(r) * (NT * 256u);
-            if constexpr (B == 1) {
-                lds_st(own, -1.f);
-                lds_st(own + 256u, 1.f);
-            } else if constexpr (B == 2) {
-                lds_st(own, 0.f);
-                lds_st(own + 256u, 1.f);
-                lds_st(own + 512u, 0.f);
-                lds_st(own + 768u, -1.f);
-            } else {
+            {
                 lds_st(own, 0.f);
                 lds_st(own + uint32_t(NT / 2) * 256u, 0.f);
                 lds_st(own + uint32_t(M) * 256u, 1.f);
@@ -489,7 +555,7 @@ template <int B, int UPG, int RW, int XDT, int YDT, bool ROUTED>
 static hipError_t stream_waves(const cq_weight &w, const void *x, void *y, const StreamRoutes &rt,
                                hipStream_t stream) {
     const int64_t ncb = ((w.k >> 5) + 63) >> 6;
-    constexpr int NT = B <= 5 ? (1 << B) : 1;
+    constexpr int NT = (B >= 3 && B <= 5) ? (1 << B) : 1;
     constexpr int kMaxW = NT >= 32 ? 2 : 4;  // keep the tables within 32 KB and the W4 slot tag in 4 bits
     // Rows of up to two column blocks: one wave per tile walks them in turn
     // (no cross-wave reduction); longer rows split their column blocks over two
@@ -514,7 +580,7 @@ static hipError_t stream_waves(const cq_weight &w, const void *x, void *y, const
 constexpr int kRowsRW = 2;
 
 static size_t rows_lds_bytes(int bits, int64_t ncb) {
-    const int64_t nt = bits <= 5 ? (int64_t(1) << bits) : 1;
+    const int64_t nt = (bits >= 3 && bits <= 5) ? (int64_t(1) << bits) : 1;
     return sizeof(float) * size_t(ncb * kRowsRW * nt * 64 + 2 * ncb * kResBatch * kRowsRW);
 }
 
