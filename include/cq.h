@@ -304,7 +304,7 @@ int64_t cq_get_gemv_max_rows(int32_t path);
  *   GEMV_LUT      model dtype only, per-wave level tables (m <= 4, G <= 128;
  *                 m == 1 at G == 256)
  *   GEMV_NARROW   matrix-core narrow-row GEMV (2 <= m <= 16; model dtype
- *                 B <= 5, A8 W4 with G >= 64)
+ *                 B <= 5, A8 W3 and W4 with G >= 64)
  *   GEMV_GENERIC  conservative one-wave-per-row GEMV (m <= 16, every B, G)
  *   GEMM_MFMA     tiled matrix-core GEMM (model dtype B <= 5; A8 W3/W4 with
  *                 G >= 64)

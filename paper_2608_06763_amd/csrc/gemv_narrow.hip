@@ -83,14 +83,20 @@ struct route_groups {
 
 }  // namespace
 
-// ---------------------------------------------------------------- Dynamic-A8, W4
+// ---------------------------------------------------------------- Dynamic-A8, W3 and W4
 
-template <int UPG, int YDT>
+// W3: a lane's 16 codes of a step are 6 bytes at an even byte offset, inside
+// one aligned 8-byte window; every lane evaluates the two interior carriers
+// r(1), r(2) of its group itself, and four fields at a time, spread into
+// selector bytes, index the pair [r0 r1 r2 r3 | 0 -r3 -r2 -r1] with one byte
+// permute (the reserved pattern selects the 0), giving carriers in field order.
+template <int B, int UPG, int YDT>
 __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
     int n, int k, const int8_t *__restrict__ x8, const float *__restrict__ dx, int m, void *__restrict__ y) {
-    constexpr int M = 7;
+    static_assert(B == 3 || B == 4, "narrow-row A8 widths");
+    constexpr int M = max_code(B);
     constexpr int SPG = UPG / 2;  // 64-slot steps per group
     __shared__ float red[kMaxWaves][16][17];
     __shared__ float fac[16];
@@ -105,7 +111,7 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
     const bool wok = wrow < n;
     const bool xok = col < m;
     const int ng = k / (32 * UPG);
-    const uint32_t row_bytes = uint32_t(k) / 2u;
+    const uint32_t row_bytes = uint32_t(k) * B / 8u;
     const auto rc = make_rsrc(codes, uint32_t(n) * row_bytes);
     const auto rs = make_rsrc(scale, uint32_t(n) * ng * 4u);
     const auto ra = make_rsrc(a16, uint32_t(n) * ng * 2u);
@@ -133,7 +139,9 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
 #pragma unroll
         for (int q = 0; q < SPG; ++q) {
             const uint32_t kk = uint32_t(g) * (32u * UPG) + 64u * q + 16u * part;
-            load_words<2>(rc, wok ? uint32_t(wrow) * row_bytes + kk / 2u : kOobOffset, st.cw[q]);
+            // W3: the aligned window holding the 6 code bytes (shifted out in process)
+            const uint32_t cb = uint32_t(wrow) * row_bytes + kk * B / 8u;
+            load_words<2>(rc, wok ? (B == 3 ? cb & ~3u : cb) : kOobOffset, st.cw[q]);
             uint32_t xv[4];
             load_words<4>(rx, xok ? uint32_t(col) * uint32_t(k) + kk : kOobOffset, xv);
             st.xa[q] = u32x4_t{xv[0], xv[1], xv[2], xv[3]};
@@ -144,20 +152,48 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
         const float a = st.a, b = st.b;
         const float c = 1.f - a - b;
         const float mg = carrier_margin(a, b, c);
-        const uint32_t pr = carrier_u8<M>(i0, t0, a, b, c, mg) | (carrier_u8<M>(i0 + 1, t1, a, b, c, mg) << 8);
-        const uint32_t p0 = lane_read(pr, col), p1 = lane_read(pr, col + 16);
-        const uint32_t p2 = lane_read(pr, col + 32), p3 = lane_read(pr, col + 48);
-        const uint32_t ta0 = p0 | (p1 << 16), ta1 = p2 | (p3 << 16);
-        uint32_t tb0, tb1;
-        w4_negative_table(ta0, ta1, tb0, tb1);
         i32x4_t acc = {0, 0, 0, 0};
+        if constexpr (B == 4) {
+            const uint32_t pr = carrier_u8<M>(i0, t0, a, b, c, mg) | (carrier_u8<M>(i0 + 1, t1, a, b, c, mg) << 8);
+            const uint32_t p0 = lane_read(pr, col), p1 = lane_read(pr, col + 16);
+            const uint32_t p2 = lane_read(pr, col + 32), p3 = lane_read(pr, col + 48);
+            const uint32_t ta0 = p0 | (p1 << 16), ta1 = p2 | (p3 << 16);
+            uint32_t tb0, tb1;
+            w4_negative_table(ta0, ta1, tb0, tb1);
 #pragma unroll
-        for (int q = 0; q < SPG; ++q) {
-            uint32_t cr[4];
-            w4_word_carriers(st.cw[q][0], ta0, ta1, tb0, tb1, cr[0], cr[1]);
-            w4_word_carriers(st.cw[q][1], ta0, ta1, tb0, tb1, cr[2], cr[3]);
-            const i32x4_t bop = {int(cr[0]), int(cr[1]), int(cr[2]), int(cr[3])};
-            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4_t, st.xa[q]), bop, acc, 0, 0, 0);
+            for (int q = 0; q < SPG; ++q) {
+                uint32_t cr[4];
+                w4_word_carriers(st.cw[q][0], ta0, ta1, tb0, tb1, cr[0], cr[1]);
+                w4_word_carriers(st.cw[q][1], ta0, ta1, tb0, tb1, cr[2], cr[3]);
+                const i32x4_t bop = {int(cr[0]), int(cr[1]), int(cr[2]), int(cr[3])};
+                acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4_t, st.xa[q]), bop, acc, 0, 0, 0);
+            }
+        } else {
+            const uint32_t r12 = carrier_u8<M>(1, 1.f / 3.f, a, b, c, mg) | (carrier_u8<M>(2, 2.f / 3.f, a, b, c, mg) << 8);
+            const uint32_t ta = (r12 << 8) | 0x7f000000u;             // r0 r1 r2 r3
+            const uint32_t neg = (0x80808080u - ta) ^ 0x80808080u;  // 0 -r1 -r2 -r3
+            const uint32_t tb = perm(neg, neg, 0x01020300u);        // 0 -r3 -r2 -r1
+            // the window starts at the 6 code bytes, or 2 bytes before them
+            const uint32_t sh = (part & 1) ? 16u : 0u;
+#pragma unroll
+            for (int q = 0; q < SPG; ++q) {
+                const uint32_t lo = __builtin_amdgcn_alignbit(st.cw[q][1], st.cw[q][0], sh);  // fields 0..10
+                const uint32_t hi = st.cw[q][1] >> sh;                                        // bits 32..47
+                uint32_t cr[4];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    uint32_t x;
+                    if (t < 2) x = lo >> (12 * t);
+                    else if (t == 2) x = __builtin_amdgcn_alignbit(hi, lo, 24);
+                    else x = hi >> 4;
+                    x &= 0xfffu;  // fields 4t .. 4t + 3
+                    const uint32_t sel =
+                        (x & 7u) | ((x << 5) & 0x700u) | ((x << 10) & 0x70000u) | ((x << 15) & 0x7000000u);
+                    cr[t] = perm(tb, ta, sel);
+                }
+                const i32x4_t bop = {int(cr[0]), int(cr[1]), int(cr[2]), int(cr[3])};
+                acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4_t, st.xa[q]), bop, acc, 0, 0, 0);
+            }
         }
         // rows of acc are activation rows, its column this lane's weight row
 #pragma unroll
@@ -375,39 +411,47 @@ static int narrow_waves(const cq_weight &w, int max_waves = kMaxWaves) {
     return nw;
 }
 
-template <int UPG, int YDT>
+template <int B, int UPG, int YDT>
 static hipError_t a8_narrow_launch(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
                                    hipStream_t stream) {
     const int64_t blocks = (w.n + 15) / 16;
     // G = 512 keeps two stages of eight 64-code steps in registers: at most 8 waves
     const int nw = narrow_waves(w, UPG >= 16 ? 8 : kMaxWaves);
-    hipLaunchKernelGGL((gemv_a8_narrow<UPG, YDT>), dim3(unsigned(blocks)), dim3(64 * nw), 0, stream, w.codes, w.scale, w.a,
+    hipLaunchKernelGGL((gemv_a8_narrow<B, UPG, YDT>), dim3(unsigned(blocks)), dim3(64 * nw), 0, stream, w.codes, w.scale, w.a,
                        w.b, int(w.n), int(w.k), x8, dx, int(m), y);
     return hipGetLastError();
 }
 
-template <int YDT>
+template <int B, int YDT>
 static hipError_t a8_narrow_group(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
                                   hipStream_t stream) {
     switch (w.group) {
-        case 64: return a8_narrow_launch<2, YDT>(w, x8, dx, m, y, stream);
-        case 128: return a8_narrow_launch<4, YDT>(w, x8, dx, m, y, stream);
-        case 256: return a8_narrow_launch<8, YDT>(w, x8, dx, m, y, stream);
-        case 512: return a8_narrow_launch<16, YDT>(w, x8, dx, m, y, stream);
+        case 64: return a8_narrow_launch<B, 2, YDT>(w, x8, dx, m, y, stream);
+        case 128: return a8_narrow_launch<B, 4, YDT>(w, x8, dx, m, y, stream);
+        case 256: return a8_narrow_launch<B, 8, YDT>(w, x8, dx, m, y, stream);
+        case 512: return a8_narrow_launch<B, 16, YDT>(w, x8, dx, m, y, stream);
     }
     return hipErrorNotSupported;
 }
 
+template <int YDT>
+static hipError_t a8_narrow_bits(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
+                                 hipStream_t stream) {
+    if (w.bits == 3) return a8_narrow_group<3, YDT>(w, x8, dx, m, y, stream);
+    if (w.bits == 4) return a8_narrow_group<4, YDT>(w, x8, dx, m, y, stream);
+    return hipErrorNotSupported;
+}
+
 bool gemv_a8_narrow_supported(const cq_weight &w, int64_t m) {
-    return m >= 2 && m <= 16 && w.bits == 4 && w.group >= 64 && stream_fits(w.n, w.k, w.bits, w.group) &&
+    return m >= 2 && m <= 16 && (w.bits == 3 || w.bits == 4) && w.group >= 64 && stream_fits(w.n, w.k, w.bits, w.group) &&
            m * w.k < (int64_t(1) << 31);
 }
 
 hipError_t launch_gemv_a8_narrow(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y, int y_dt,
                                  hipStream_t stream) {
-    if (y_dt == 0) return a8_narrow_group<0>(w, x8, dx, m, y, stream);
-    if (y_dt == 1) return a8_narrow_group<1>(w, x8, dx, m, y, stream);
-    return a8_narrow_group<2>(w, x8, dx, m, y, stream);
+    if (y_dt == 0) return a8_narrow_bits<0>(w, x8, dx, m, y, stream);
+    if (y_dt == 1) return a8_narrow_bits<1>(w, x8, dx, m, y, stream);
+    return a8_narrow_bits<2>(w, x8, dx, m, y, stream);
 }
 
 template <int B, int UPG, int XDT, int YDT>

@@ -249,7 +249,7 @@ def clean_table():
     (4, 128, 8, "gemm_slab", "gemv_narrow"),
     (4, 32, 8, "gemm_slab_staged", "gemv_generic"),
     (3, 128, 1, "gemv_stream", "gemv_stream"),
-    (3, 128, 8, "gemm_slab", "gemv_generic"),
+    (3, 128, 8, "gemm_slab", "gemv_narrow"),
     (6, 128, 1, "gemv_stream", "gemv_stream"),
     (6, 128, 8, "gemv_generic", "gemv_generic"),
     (4, 128, 17, "gemm_slab", "gemm_mfma"),

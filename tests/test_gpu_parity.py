@@ -346,6 +346,46 @@ def test_a8_near_tie_carriers_exact(torch_dev, bits, family):
     assert np.array_equal(_np(y).astype(np.float64), p.sum(axis=-1).astype(np.float64))
 
 
+@pytest.mark.parametrize("bits", [3, 4])
+@pytest.mark.parametrize("m", [2, 5, 16])
+def test_a8_narrow_near_tie_carriers_exact(torch_dev, bits, m):
+    # the narrow-row A8 kernel (W3 and W4) on the near-tie rows: the probe's
+    # activation row repeated m times, every output row the exact integer sum
+    # of the oracle's P_g (unit scales, d_x = 127), bit for bit
+    codes, s, a, b, x8, dx, p = carrier_probe(bits, 128)
+    say("a8_narrow_near_tie", bits, m, len(a))
+    cq = _cq()
+    w = cq.CQWeight.from_codes(codes, s, a, b, bits, 128)
+    x8_t = torch_dev.from_numpy(np.repeat(x8, m, axis=0)).cuda()
+    dx_t = torch_dev.from_numpy(np.repeat(dx, m)).cuda()
+    assert cq.cq_family_supported(cq.CQ_PATH_A8, "gemv_narrow", w, m)
+    y = _np(cq.cq_gemm_a8_family(w, x8_t, dx_t, "gemv_narrow", y_dtype=torch_dev.float32))
+    want = p.sum(axis=-1).astype(np.float64).reshape(1, -1)
+    assert np.array_equal(y, np.repeat(want, m, axis=0))
+
+
+@pytest.mark.parametrize("group", [64, 128, 256, 512])
+@pytest.mark.parametrize("m", [2, 7, 16])
+def test_gemv_a8_narrow_w3(torch_dev, group, m):
+    # W3 narrow-row A8 against the A8 oracle: 300 weight rows (a ragged last
+    # strip), K = 2048 + one group (at least 128 codes: W3 rows are whole
+    # 16-byte units), fitted weights
+    bits, n = 3, 300
+    k = 2048 + max(group, 128)
+    r = fitted(620 + group, n, k, bits, group)
+    xb, xv = act(621 + m, m, k)
+    x8_ref, d_ref, y_ref, _ = ref_a8(xv, r, bits, group)
+    cq = _cq()
+    w = _weight(r, bits, group)
+    x8 = torch_dev.from_numpy(x8_ref).cuda()
+    dx = torch_dev.from_numpy(d_ref).cuda()
+    say("gemv_a8_narrow w3", group, m)
+    assert cq.cq_select_query(cq.CQ_PATH_A8, w, m) == "gemv_narrow"
+    y = cq.cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32)
+    assert R.eps_comp(_np(y), y_ref, "fp32") <= 1e-5
+    assert R.eps_comp(_np(cq.cq_gemm_a8(w, x8, dx)), y_ref, "bf16") <= TOL
+
+
 # ---------------------------------------------------------------- many-row matrix-core GEMMs
 
 
