@@ -123,33 +123,94 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
     const int i0 = 2 * part;
     const float t0 = float(i0) / float(M), t1 = float(i0 + 1) / float(M);
 
-    // A wave walks its groups g = wave, wave + 4, ...; the codes, activations
-    // and metadata of its next group are requested before the current group is
-    // decoded (two register stages, the loop unrolled by two).
+    // A wave takes a contiguous run of groups.  Per group it loads the
+    // strip's code bytes as whole pieces (PS bytes; consecutive lanes on
+    // consecutive bytes of a row, so each quad of lanes reads one run of a
+    // row), writes them to its own LDS staging rows and reads each lane's
+    // slice back; only the wave touches its staging rows, so program order
+    // orders the writes and reads.  The group metadata of the strip come in
+    // batches of four groups (lane l: row l / 4, group l % 4) and reach their
+    // lanes by ds_bpermute.  The codes and activations of the next group, and
+    // the metadata of the next batch, are requested before the current group
+    // is decoded (two register stages, the loop unrolled by two).
+    constexpr int GB = 32 * UPG * B / 8;         // code bytes of one row in one group
+    constexpr int PS = GB % 16 == 0 ? 16 : 8;    // bytes per piece
+    constexpr int PPR = GB / PS;                 // pieces per row
+    constexpr int NP = 16 * PPR;                 // pieces per group
+    constexpr int NL = (NP + 63) / 64;           // piece loads per lane
+    constexpr int RS = GB + 16;                  // staged row stride (bytes)
+    constexpr int kStgWaves = UPG >= 16 ? 8 : kMaxWaves;
+    __shared__ __attribute__((aligned(16))) uint32_t stg[kStgWaves * 16 * RS / 4];
+    uint8_t *const mystg = reinterpret_cast<uint8_t *>(stg) + wave * (16 * RS);
+    const int gper = (ng + nwaves - 1) / nwaves;
+    const int gbeg = min(ng, wave * gper), gend = min(ng, gbeg + gper);
+
     struct Stage {
-        uint32_t cw[SPG][2];
+        uint32_t pc[NL][PS / 4];
         u32x4_t xa[SPG];
-        float s, a, b;
     };
     auto load = [&](int g, Stage &st) {
-        const uint32_t gi = uint32_t(wrow) * ng + g;
-        st.s = load_f32(rs, wok ? gi * 4u : kOobOffset);
-        st.a = f16_to_f32(uint16_t(load_u16(ra, wok ? gi * 2u : kOobOffset)));
-        st.b = f16_to_f32(uint16_t(load_u16(rb, wok ? gi * 2u : kOobOffset)));
+#pragma unroll
+        for (int t = 0; t < NL; ++t) {
+            const int pi = t * 64 + lane;
+            const int wr = n0 + pi / PPR;
+            const bool ok = pi < NP && wr < n;
+            load_words<PS / 4>(rc, ok ? uint32_t(wr) * row_bytes + uint32_t(g) * GB + uint32_t(pi % PPR) * PS
+                                      : kOobOffset, st.pc[t]);
+        }
 #pragma unroll
         for (int q = 0; q < SPG; ++q) {
             const uint32_t kk = uint32_t(g) * (32u * UPG) + 64u * q + 16u * part;
-            // W3: the aligned window holding the 6 code bytes (shifted out in process)
-            const uint32_t cb = uint32_t(wrow) * row_bytes + kk * B / 8u;
-            load_words<2>(rc, wok ? (B == 3 ? cb & ~3u : cb) : kOobOffset, st.cw[q]);
             uint32_t xv[4];
             load_words<4>(rx, xok ? uint32_t(col) * uint32_t(k) + kk : kOobOffset, xv);
             st.xa[q] = u32x4_t{xv[0], xv[1], xv[2], xv[3]};
         }
     };
+    // metadata of groups gb .. gb + 3 of the strip: scale, and a | b << 16
+    float ms_c = 0.f, ms_n = 0.f;
+    uint32_t mab_c = 0, mab_n = 0;
+    auto load_meta = [&](int gb, float &ms, uint32_t &mab) {
+        const int r = n0 + (lane >> 2), gg = gb + (lane & 3);
+        const bool ok = r < n && gg < ng;
+        const uint32_t gi = uint32_t(r) * ng + gg;
+        ms = load_f32(rs, ok ? gi * 4u : kOobOffset);
+        mab = load_u16(ra, ok ? gi * 2u : kOobOffset) | (load_u16(rb, ok ? gi * 2u : kOobOffset) << 16);
+    };
     float accf[4] = {0.f, 0.f, 0.f, 0.f};
-    auto process = [&](const Stage &st) {
-        const float a = st.a, b = st.b;
+    auto process = [&](int g, const Stage &st) {
+        const int j = (g - gbeg) & 3;
+        if (j == 0 && g != gbeg) {
+            ms_c = ms_n;
+            mab_c = mab_n;
+            if (g + 4 < gend) load_meta(g + 4, ms_n, mab_n);
+        }
+        const float s = __int_as_float(int(lane_read(__float_as_uint(ms_c), 4 * col + j)));
+        const uint32_t ab = lane_read(mab_c, 4 * col + j);
+        const float a = f16_to_f32(uint16_t(ab & 0xffffu)), b = f16_to_f32(uint16_t(ab >> 16));
+        // stage the group's code pieces, then read this lane's slices
+#pragma unroll
+        for (int t = 0; t < NL; ++t) {
+            const int pi = t * 64 + lane;
+            if (pi < NP) {
+                uint8_t *dst = mystg + (pi / PPR) * RS + (pi % PPR) * PS;
+                if constexpr (PS == 16)
+                    *reinterpret_cast<u32x4_t *>(dst) = u32x4_t{st.pc[t][0], st.pc[t][1], st.pc[t][2], st.pc[t][3]};
+                else
+                    *reinterpret_cast<uint2 *>(dst) = make_uint2(st.pc[t][0], st.pc[t][1]);
+            }
+        }
+        wave_lds_order();
+        uint32_t cw[SPG][2];
+#pragma unroll
+        for (int q = 0; q < SPG; ++q) {
+            // W4: 8 code bytes at 32 q + 8 part; W3: the aligned window of the
+            // 6 code bytes at 24 q + 6 part
+            const int o = B == 4 ? 32 * q + 8 * part : (24 * q + 6 * part) & ~3;
+            const uint32_t *src = reinterpret_cast<const uint32_t *>(mystg + col * RS + o);
+            cw[q][0] = src[0];
+            cw[q][1] = src[1];
+        }
+        wave_lds_order();
         const float c = 1.f - a - b;
         const float mg = carrier_margin(a, b, c);
         i32x4_t acc = {0, 0, 0, 0};
@@ -163,8 +224,8 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
 #pragma unroll
             for (int q = 0; q < SPG; ++q) {
                 uint32_t cr[4];
-                w4_word_carriers(st.cw[q][0], ta0, ta1, tb0, tb1, cr[0], cr[1]);
-                w4_word_carriers(st.cw[q][1], ta0, ta1, tb0, tb1, cr[2], cr[3]);
+                w4_word_carriers(cw[q][0], ta0, ta1, tb0, tb1, cr[0], cr[1]);
+                w4_word_carriers(cw[q][1], ta0, ta1, tb0, tb1, cr[2], cr[3]);
                 const i32x4_t bop = {int(cr[0]), int(cr[1]), int(cr[2]), int(cr[3])};
                 acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4_t, st.xa[q]), bop, acc, 0, 0, 0);
             }
@@ -177,8 +238,8 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
             const uint32_t sh = (part & 1) ? 16u : 0u;
 #pragma unroll
             for (int q = 0; q < SPG; ++q) {
-                const uint32_t lo = __builtin_amdgcn_alignbit(st.cw[q][1], st.cw[q][0], sh);  // fields 0..10
-                const uint32_t hi = st.cw[q][1] >> sh;                                        // bits 32..47
+                const uint32_t lo = __builtin_amdgcn_alignbit(cw[q][1], cw[q][0], sh);  // fields 0..10
+                const uint32_t hi = cw[q][1] >> sh;                                     // bits 32..47
                 uint32_t cr[4];
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
@@ -197,20 +258,20 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
         }
         // rows of acc are activation rows, its column this lane's weight row
 #pragma unroll
-        for (int i = 0; i < 4; ++i) accf[i] = __builtin_fmaf(st.s, float(acc[i]), accf[i]);
+        for (int i = 0; i < 4; ++i) accf[i] = __builtin_fmaf(s, float(acc[i]), accf[i]);
     };
     Stage s0, s1;
-    int g = wave;
-    if (g < ng) load(g, s0);
-    while (g < ng) {
-        const int g1 = g + nwaves;
-        if (g1 < ng) load(g1, s1);
-        process(s0);
-        if (g1 >= ng) break;
-        const int g2 = g1 + nwaves;
-        if (g2 < ng) load(g2, s0);
-        process(s1);
-        g = g2;
+    if (gbeg < gend) {
+        load_meta(gbeg, ms_c, mab_c);
+        if (gbeg + 4 < gend) load_meta(gbeg + 4, ms_n, mab_n);
+        load(gbeg, s0);
+    }
+    for (int g = gbeg; g < gend; g += 2) {
+        if (g + 1 < gend) load(g + 1, s1);
+        process(g, s0);
+        if (g + 1 >= gend) break;
+        if (g + 2 < gend) load(g + 2, s0);
+        process(g + 1, s1);
     }
     // the scale loaded above is this lane's column (weight row), so the
     // rescale above is s_{n,g} P_g for output (row 4 part + i, column col)
