@@ -146,7 +146,7 @@ def _cpu_baseline_run(layers_np, bits, group, budget_s, blas_threads, gpu_out):
         if spent > budget_s:
             break
     return {"value": done_bytes / spent / 1e9, "unit": "GB/s", "cores": int(blas_threads), "kind": "oracle",
-            "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
+            "cpu_model": cpu_model(), "cpu_mhz": cpu_mhz(), "host_cpus": os.cpu_count(),
             "sample": f"oracle unpack+decode(fp64)+product on {rows_done} weight rows "
                       f"(first half of each decode layer, M=1), {spent:.1f} s; elementwise numpy on 1 thread, "
                       f"product on {blas_threads} BLAS threads",
@@ -441,6 +441,19 @@ def cpu_model():
     except OSError:
         pass
     return None
+
+
+def cpu_mhz():
+    """Mean current clock of this host's cores in MHz (from /proc/cpuinfo), or None."""
+    vals = []
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("cpu MHz"):
+                    vals.append(float(line.split(":", 1)[1]))
+    except (OSError, ValueError):
+        return None
+    return round(sum(vals) / len(vals), 1) if vals else None
 
 
 def fitted_timing(torch, cq, fitted_rep, bits=4, group=128, k=4096, n=4096):
