@@ -138,8 +138,11 @@ __global__ void __launch_bounds__(1024) gemm_a16_slab(
     // ring of R chunk slots
     uint32_t cw[R][BJ][B];
     uint32_t xw[R][BI][16];
+    // group metadata of a sweep, loaded by lane l for row l / 4 of the block
+    // and group l % 4 of the sweep (each quad of lanes reads one run of a
+    // row), then handed to lane (row, group slot) by ds_bpermute
     float sv[R][BJ];
-    uint32_t av[R][BJ], bv[R][BJ];
+    uint32_t abv[R][BJ];
 
     // chunk c of this wave: sweep wave + nw (c / UPG), unit c % UPG of the group
     auto load_slot = [&](int c, auto slot_c, auto meta_c) {
@@ -157,9 +160,12 @@ __global__ void __launch_bounds__(1024) gemm_a16_slab(
             load_words<B>(rc, ok ? uint32_t(row) * row_bytes + (uint32_t(g) * UPG + uint32_t(u)) * (4u * B) : kOobOffset,
                           cw[SL][j]);
             if constexpr (META) {
-                sv[SL][j] = load_f32(rs, ok ? gi * 4u : kOobOffset);
-                av[SL][j] = load_u16(ra, ok ? gi * 2u : kOobOffset);
-                bv[SL][j] = load_u16(rb, ok ? gi * 2u : kOobOffset);
+                const int mrow = n0 + 16 * j + (lane >> 2);
+                const int mg = 4 * sw + (lane & 3);
+                const bool mok = mrow < n && mg < ng;
+                const uint32_t mi = uint32_t(mrow) * uint32_t(ng) + uint32_t(mg);
+                sv[SL][j] = load_f32(rs, mok ? mi * 4u : kOobOffset);
+                abv[SL][j] = load_u16(ra, mok ? mi * 2u : kOobOffset) | (load_u16(rb, mok ? mi * 2u : kOobOffset) << 16);
             }
         }
 #pragma unroll
@@ -187,7 +193,8 @@ __global__ void __launch_bounds__(1024) gemm_a16_slab(
 #pragma unroll
         for (int j = 0; j < BJ; ++j) {
             const uint32_t cj = col0 + j * kTab;
-            const float s = sv[SL][j];
+            const int src = (4 * nl + q) << 2;
+            const float s = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(sv[SL][j])));
             const uint32_t es = operand_entry<XDT>(s);  // q(1) = 1
             if constexpr (B == 1) {
                 lds_st(cj, es ^ kNeg);
@@ -196,8 +203,9 @@ __global__ void __launch_bounds__(1024) gemm_a16_slab(
                 lds_st(cj + uint32_t(M) * 256u, es);
                 lds_st(cj + uint32_t(NE - M) * 256u, es ^ kNeg);
                 if constexpr (B >= 3) {
-                    const float a = f16_to_f32(uint16_t(av[SL][j]));
-                    const float b = f16_to_f32(uint16_t(bv[SL][j]));
+                    const uint32_t ab = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(abv[SL][j])));
+                    const float a = f16_to_f32(uint16_t(ab & 0xffffu));
+                    const float b = f16_to_f32(uint16_t(ab >> 16));
                     const float cc = 1.f - a - b;
 #pragma unroll
                     for (int i = 1; i < M; ++i) {
