@@ -212,8 +212,9 @@ cq_status cq_build_carriers(const cq_weight *w, int8_t *carriers, void *stream);
  * Same result as cq_gemm_a8 (without the partials dump), bit for bit: the
  * kernels read the carriers of cq_build_carriers for the same weight instead
  * of forming them (the many-row W4 matrix-core GEMM and the generic kernels
- * of the other widths; the W4 single- and narrow-row kernels keep their
- * register decode, which gives the same carriers).
+ * of the other widths; the single-row kernels and the W3/W4 narrow-row
+ * kernels, up to 32 rows, keep their register decode, which gives the same
+ * carriers).
  *   carriers  the table of cq_build_carriers (NULL allowed for W1).
  * Errors as cq_gemm_a8.
  */
@@ -303,8 +304,9 @@ int64_t cq_get_gemv_max_rows(int32_t path);
  *   GEMV_STREAM   single-row streaming GEMV (m == 1)
  *   GEMV_LUT      model dtype only, per-wave level tables (m <= 4, G <= 128;
  *                 m == 1 at G == 256)
- *   GEMV_NARROW   matrix-core narrow-row GEMV (2 <= m <= 16; model dtype
- *                 B <= 5, A8 W3 and W4 with G >= 64)
+ *   GEMV_NARROW   matrix-core narrow-row GEMV (model dtype 2 <= m <= 16,
+ *                 B <= 5; A8 2 <= m <= 32, W3 and W4 with G >= 64, two
+ *                 16-row blocks of x per decoded operand above 16 rows)
  *   GEMV_GENERIC  conservative one-wave-per-row GEMV (m <= 16, every B, G)
  *   GEMM_MFMA     tiled matrix-core GEMM (model dtype B <= 5; A8 W3/W4 with
  *                 G >= 64)

@@ -270,6 +270,10 @@ cq_status cq_gemm_a8_carriers(const cq_weight *w, const int8_t *carriers, const 
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (m <= gemv_max_rows(1) && m <= cq::kGemvMaxRows)
         return hip_status(cq::launch_gemv_a8_tab(*w, carriers, x8, dx, m, y, int(y_dtype), s));
+    // 17..32 rows: the narrow-row kernel of the built-in rules (its register
+    // decode forms the same carriers as the table)
+    if (gemv_max_rows(1) >= cq::kGemvMaxRows && cq::gemv_a8_narrow_supported(*w, m))
+        return hip_status(cq::launch_gemv_a8_narrow(*w, x8, dx, m, y, int(y_dtype), s));
     if (m > int64_t(65535) * 64) return CQ_ERR_SHAPE;
     return hip_status(cq::launch_gemm_a8_tab(*w, carriers, x8, dx, m, y, int(y_dtype), s));
 }

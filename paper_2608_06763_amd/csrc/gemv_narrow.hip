@@ -92,16 +92,20 @@ struct route_groups {
 // r(1), r(2) of its group itself, and four fields at a time, spread into
 // selector bytes, index the pair [r0 r1 r2 r3 | 0 -r3 -r2 -r1] with one byte
 // permute (the reserved pattern selects the 0), giving carriers in field order.
-template <int B, int UPG, int YDT>
-__global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
+// XB = 2 (17..32 rows): every decoded weight operand feeds the MFMAs of two
+// 16-row blocks of x; at most 8 waves per strip.
+template <int B, int UPG, int YDT, int XB>
+__global__ void __launch_bounds__(UPG >= 16 || XB == 2 ? 512 : 1024) gemv_a8_narrow(
     const uint8_t *__restrict__ codes, const float *__restrict__ scale,
     const uint16_t *__restrict__ a16, const uint16_t *__restrict__ b16,
     int n, int k, const int8_t *__restrict__ x8, const float *__restrict__ dx, int m, void *__restrict__ y) {
     static_assert(B == 3 || B == 4, "narrow-row A8 widths");
+    static_assert(XB == 1 || XB == 2, "one or two 16-row blocks of x");
     constexpr int M = max_code(B);
     constexpr int SPG = UPG / 2;  // 64-slot steps per group
-    __shared__ float red[kMaxWaves][16][17];
-    __shared__ float fac[16];
+    constexpr int kRedWaves = (UPG >= 16 || XB == 2) ? 8 : kMaxWaves;
+    __shared__ float red[kRedWaves][16 * XB][17];
+    __shared__ float fac[16 * XB];
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -111,7 +115,6 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
     const int part = lane >> 4;    // K part of a step
     const int wrow = n0 + col;
     const bool wok = wrow < n;
-    const bool xok = col < m;
     const int ng = k / (32 * UPG);
     const uint32_t row_bytes = uint32_t(k) * B / 8u;
     const auto rc = make_rsrc(codes, uint32_t(n) * row_bytes);
@@ -119,7 +122,7 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
     const auto ra = make_rsrc(a16, uint32_t(n) * ng * 2u);
     const auto rb = make_rsrc(b16, uint32_t(n) * ng * 2u);
     const auto rx = make_rsrc(x8, uint32_t(m) * uint32_t(k));
-    if (threadIdx.x < 16) fac[threadIdx.x] = threadIdx.x < m ? dx[threadIdx.x] / 127.0f : 0.f;
+    if (threadIdx.x < 16 * XB) fac[threadIdx.x] = int(threadIdx.x) < m ? dx[threadIdx.x] / 127.0f : 0.f;
 
     // carriers of pair `part` of the row: magnitudes 2 part, 2 part + 1
     const int i0 = 2 * part;
@@ -141,7 +144,7 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
     constexpr int NP = 16 * PPR;                 // pieces per group
     constexpr int NL = (NP + 63) / 64;           // piece loads per lane
     constexpr int RS = GB + 16;                  // staged row stride (bytes)
-    constexpr int kStgWaves = UPG >= 16 ? 8 : kMaxWaves;
+    constexpr int kStgWaves = kRedWaves;
     __shared__ __attribute__((aligned(16))) uint32_t stg[kStgWaves * 16 * RS / 4];
     uint8_t *const mystg = reinterpret_cast<uint8_t *>(stg) + wave * (16 * RS);
     const int gper = (ng + nwaves - 1) / nwaves;
@@ -149,7 +152,7 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
 
     struct Stage {
         uint32_t pc[NL][PS / 4];
-        u32x4_t xa[SPG];
+        u32x4_t xa[XB][SPG];
     };
     auto load = [&](int g, Stage &st) {
 #pragma unroll
@@ -161,11 +164,15 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
                                       : kOobOffset, st.pc[t]);
         }
 #pragma unroll
-        for (int q = 0; q < SPG; ++q) {
-            const uint32_t kk = uint32_t(g) * (32u * UPG) + 64u * q + 16u * part;
-            uint32_t xv[4];
-            load_words<4>(rx, xok ? uint32_t(col) * uint32_t(k) + kk : kOobOffset, xv);
-            st.xa[q] = u32x4_t{xv[0], xv[1], xv[2], xv[3]};
+        for (int bx = 0; bx < XB; ++bx) {
+            const int xrow = 16 * bx + col;
+#pragma unroll
+            for (int q = 0; q < SPG; ++q) {
+                const uint32_t kk = uint32_t(g) * (32u * UPG) + 64u * q + 16u * part;
+                uint32_t xv[4];
+                load_words<4>(rx, xrow < m ? uint32_t(xrow) * uint32_t(k) + kk : kOobOffset, xv);
+                st.xa[bx][q] = u32x4_t{xv[0], xv[1], xv[2], xv[3]};
+            }
         }
     };
     // metadata of groups gb .. gb + 3 of the strip: scale, and a | b << 16
@@ -178,7 +185,11 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
         ms = load_f32(rs, ok ? gi * 4u : kOobOffset);
         mab = load_u16(ra, ok ? gi * 2u : kOobOffset) | (load_u16(rb, ok ? gi * 2u : kOobOffset) << 16);
     };
-    float accf[4] = {0.f, 0.f, 0.f, 0.f};
+    float accf[XB][4];
+#pragma unroll
+    for (int bx = 0; bx < XB; ++bx)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) accf[bx][i] = 0.f;
     auto process = [&](int g, const Stage &st) {
         const int j = (g - gbeg) & 3;
         if (j == 0 && g != gbeg) {
@@ -215,7 +226,9 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
         wave_lds_order();
         const float c = 1.f - a - b;
         const float mg = carrier_margin(a, b, c);
-        i32x4_t acc = {0, 0, 0, 0};
+        i32x4_t acc[XB];
+#pragma unroll
+        for (int bx = 0; bx < XB; ++bx) acc[bx] = i32x4_t{0, 0, 0, 0};
         if constexpr (B == 4) {
             const uint32_t pr = carrier_u8<M>(i0, t0, a, b, c, mg) | (carrier_u8<M>(i0 + 1, t1, a, b, c, mg) << 8);
             const uint32_t p0 = lane_read(pr, col), p1 = lane_read(pr, col + 16);
@@ -229,7 +242,10 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
                 w4_word_carriers(cw[q][0], ta0, ta1, tb0, tb1, cr[0], cr[1]);
                 w4_word_carriers(cw[q][1], ta0, ta1, tb0, tb1, cr[2], cr[3]);
                 const i32x4_t bop = {int(cr[0]), int(cr[1]), int(cr[2]), int(cr[3])};
-                acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4_t, st.xa[q]), bop, acc, 0, 0, 0);
+#pragma unroll
+                for (int bx = 0; bx < XB; ++bx)
+                    acc[bx] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4_t, st.xa[bx][q]), bop, acc[bx],
+                                                                    0, 0, 0);
             }
         } else {
             const uint32_t r12 = carrier_u8<M>(1, 1.f / 3.f, a, b, c, mg) | (carrier_u8<M>(2, 2.f / 3.f, a, b, c, mg) << 8);
@@ -255,12 +271,17 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
                     cr[t] = perm(tb, ta, sel);
                 }
                 const i32x4_t bop = {int(cr[0]), int(cr[1]), int(cr[2]), int(cr[3])};
-                acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4_t, st.xa[q]), bop, acc, 0, 0, 0);
+#pragma unroll
+                for (int bx = 0; bx < XB; ++bx)
+                    acc[bx] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4_t, st.xa[bx][q]), bop, acc[bx],
+                                                                    0, 0, 0);
             }
         }
         // rows of acc are activation rows, its column this lane's weight row
 #pragma unroll
-        for (int i = 0; i < 4; ++i) accf[i] = __builtin_fmaf(s, float(acc[i]), accf[i]);
+        for (int bx = 0; bx < XB; ++bx)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) accf[bx][i] = __builtin_fmaf(s, float(acc[bx][i]), accf[bx][i]);
     };
     Stage s0, s1;
     if (gbeg < gend) {
@@ -276,8 +297,21 @@ __global__ void __launch_bounds__(UPG >= 16 ? 512 : 1024) gemv_a8_narrow(
         process(g + 1, s1);
     }
     // the scale loaded above is this lane's column (weight row), so the
-    // rescale above is s_{n,g} P_g for output (row 4 part + i, column col)
-    reduce_store<YDT>(red, accf, lane, wave, nwaves, n0, n, m, fac, y);
+    // rescale above is s_{n,g} P_g for output (row 16 bx + 4 part + i, column
+    // col); the waves' tiles meet in LDS
+#pragma unroll
+    for (int bx = 0; bx < XB; ++bx)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) red[wave][16 * bx + 4 * part + i][col] = accf[bx][i];
+    __syncthreads();
+    for (int e = threadIdx.x; e < 256 * XB; e += blockDim.x) {
+        const int r = e >> 4, c = e & 15;
+        if (r < m && n0 + c < n) {
+            float sum = 0.f;
+            for (int wv = 0; wv < nwaves; ++wv) sum += red[wv][r][c];
+            store_out<YDT>(y, int64_t(r) * n + n0 + c, sum * fac[r]);
+        }
+    }
 }
 
 // ---------------------------------------------------------------- model dtype, B <= 5
@@ -474,20 +508,27 @@ static int narrow_waves(const cq_weight &w, int max_waves = kMaxWaves) {
     return nw;
 }
 
-template <int B, int UPG, int YDT>
-static hipError_t a8_narrow_launch(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
-                                   hipStream_t stream) {
+template <int B, int UPG, int YDT, int XB>
+static hipError_t a8_narrow_launch_x(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
+                                     hipStream_t stream) {
     const int64_t blocks = (w.n + 15) / 16;
     // G = 512 keeps two stages of eight 64-code steps in registers: at most 8 waves;
     // each wave takes a contiguous run of groups, and its metadata come in
     // batches of four: at most one wave per four groups (measured: qkv-sized
     // layers 20% faster with four groups per wave than with two)
     const int64_t ng = w.k / w.group;
-    const int cap = int(std::min<int64_t>(UPG >= 16 ? 8 : kMaxWaves, std::max<int64_t>(4, ng / 4)));
+    const int cap = int(std::min<int64_t>(UPG >= 16 || XB == 2 ? 8 : kMaxWaves, std::max<int64_t>(4, ng / 4)));
     const int nw = narrow_waves(w, cap);
-    hipLaunchKernelGGL((gemv_a8_narrow<B, UPG, YDT>), dim3(unsigned(blocks)), dim3(64 * nw), 0, stream, w.codes, w.scale, w.a,
-                       w.b, int(w.n), int(w.k), x8, dx, int(m), y);
+    hipLaunchKernelGGL((gemv_a8_narrow<B, UPG, YDT, XB>), dim3(unsigned(blocks)), dim3(64 * nw), 0, stream, w.codes, w.scale,
+                       w.a, w.b, int(w.n), int(w.k), x8, dx, int(m), y);
     return hipGetLastError();
+}
+
+template <int B, int UPG, int YDT>
+static hipError_t a8_narrow_launch(const cq_weight &w, const int8_t *x8, const float *dx, int64_t m, void *y,
+                                   hipStream_t stream) {
+    if (m > 16) return a8_narrow_launch_x<B, UPG, YDT, 2>(w, x8, dx, m, y, stream);
+    return a8_narrow_launch_x<B, UPG, YDT, 1>(w, x8, dx, m, y, stream);
 }
 
 template <int B, int YDT>
@@ -511,7 +552,7 @@ static hipError_t a8_narrow_bits(const cq_weight &w, const int8_t *x8, const flo
 }
 
 bool gemv_a8_narrow_supported(const cq_weight &w, int64_t m) {
-    return m >= 2 && m <= 16 && (w.bits == 3 || w.bits == 4) && w.group >= 64 && stream_fits(w.n, w.k, w.bits, w.group) &&
+    return m >= 2 && m <= 32 && (w.bits == 3 || w.bits == 4) && w.group >= 64 && stream_fits(w.n, w.k, w.bits, w.group) &&
            m * w.k < (int64_t(1) << 31);
 }
 

@@ -84,6 +84,11 @@ int default_family(int path, const cq_weight &w, int64_t m, int64_t gemv_max_row
         if (!partials && gemv_a8_narrow_supported(w, m)) return CQ_FAMILY_GEMV_NARROW;
         return CQ_FAMILY_GEMV_GENERIC;
     }
+    // 17..32 rows (with the GEMV threshold at its maximum): the narrow-row
+    // kernel with two 16-row blocks of x per decoded operand (measured ahead
+    // of the 32-row tile on every decode and crossover shape, 1.2-3.4x)
+    if (!partials && m > kGemvMaxRows && gemv_max_rows >= kGemvMaxRows && gemv_a8_narrow_supported(w, m))
+        return CQ_FAMILY_GEMV_NARROW;
     return gemm_a8_mfma_supported(w, m) && (w.bits == 4 || !partials) ? CQ_FAMILY_GEMM_MFMA : CQ_FAMILY_GEMM_TILED;
 }
 

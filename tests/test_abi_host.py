@@ -252,7 +252,8 @@ def clean_table():
     (3, 128, 8, "gemm_slab", "gemv_narrow"),
     (6, 128, 1, "gemv_stream", "gemv_stream"),
     (6, 128, 8, "gemv_generic", "gemv_generic"),
-    (4, 128, 17, "gemm_slab", "gemm_mfma"),
+    (4, 128, 17, "gemm_slab", "gemv_narrow"),
+    (4, 128, 32, "gemm_slab_staged", "gemv_narrow"),
     (4, 128, 33, "gemm_mfma", "gemm_mfma"),
     (4, 128, 4, "gemm_slab", "gemv_narrow"),
     (3, 64, 300, "gemm_mfma", "gemm_mfma"),

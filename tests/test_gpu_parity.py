@@ -347,7 +347,7 @@ def test_a8_near_tie_carriers_exact(torch_dev, bits, family):
 
 
 @pytest.mark.parametrize("bits", [3, 4])
-@pytest.mark.parametrize("m", [2, 5, 16])
+@pytest.mark.parametrize("m", [2, 5, 16, 17, 32])
 def test_a8_narrow_near_tie_carriers_exact(torch_dev, bits, m):
     # the narrow-row A8 kernel (W3 and W4) on the near-tie rows: the probe's
     # activation row repeated m times, every output row the exact integer sum
@@ -365,7 +365,7 @@ def test_a8_narrow_near_tie_carriers_exact(torch_dev, bits, m):
 
 
 @pytest.mark.parametrize("group", [64, 128, 256, 512])
-@pytest.mark.parametrize("m", [2, 7, 16])
+@pytest.mark.parametrize("m", [2, 7, 16, 19, 32])
 def test_gemv_a8_narrow_w3(torch_dev, group, m):
     # W3 narrow-row A8 against the A8 oracle: 300 weight rows (a ragged last
     # strip), K = 2048 + one group (at least 128 codes: W3 rows are whole
@@ -384,6 +384,29 @@ def test_gemv_a8_narrow_w3(torch_dev, group, m):
     y = cq.cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32)
     assert R.eps_comp(_np(y), y_ref, "fp32") <= 1e-5
     assert R.eps_comp(_np(cq.cq_gemm_a8(w, x8, dx)), y_ref, "bf16") <= TOL
+
+
+@pytest.mark.parametrize("group", [64, 128, 256, 512])
+@pytest.mark.parametrize("m", [17, 24, 32])
+def test_gemv_a8_narrow_two_blocks_w4(torch_dev, group, m):
+    # W4 narrow-row A8 above 16 rows (two 16-row blocks of x per decoded
+    # operand) against the A8 oracle and the 32-row tiled GEMM; 300 weight
+    # rows (a ragged last strip), K = 2048 + one group
+    bits, n = 4, 300
+    k = 2048 + group
+    r = fitted(630 + group, n, k, bits, group)
+    xb, xv = act(631 + m, m, k)
+    x8_ref, d_ref, y_ref, _ = ref_a8(xv, r, bits, group)
+    cq = _cq()
+    w = _weight(r, bits, group)
+    x8 = torch_dev.from_numpy(x8_ref).cuda()
+    dx = torch_dev.from_numpy(d_ref).cuda()
+    say("gemv_a8_narrow two blocks", group, m)
+    assert cq.cq_select_query(cq.CQ_PATH_A8, w, m) == "gemv_narrow"
+    y = cq.cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32)
+    assert R.eps_comp(_np(y), y_ref, "fp32") <= 1e-5
+    yt = cq.cq_gemm_a8_family(w, x8, dx, "gemm_mfma_m32", y_dtype=torch_dev.float32)
+    assert R.eps_comp(_np(yt), y_ref, "fp32") <= 1e-5
 
 
 # ---------------------------------------------------------------- many-row matrix-core GEMMs
@@ -960,7 +983,12 @@ def test_gemm_a8_tile_heights_bit_equal(torch_dev, bits, group, m):
         assert torch_dev.equal(cq.cq_gemm_a8_family(w, x8, dx, f, y_dtype=torch_dev.float32), outs[f])
     assert torch_dev.equal(outs["gemm_mfma_m128"], outs["gemm_mfma_m256"])
     tab = cq.cq_build_carriers(w)
-    assert torch_dev.equal(cq.cq_gemm_a8_carriers(w, tab, x8, dx, y_dtype=torch_dev.float32), outs["gemm_mfma"]) or m <= 16
+    # the table call runs the built-in rules' kernel (above 16 rows: the
+    # narrow-row kernel up to 32, the tiled GEMM beyond) and equals cq_gemm_a8
+    auto = cq.cq_gemm_a8(w, x8, dx, y_dtype=torch_dev.float32)
+    assert torch_dev.equal(cq.cq_gemm_a8_carriers(w, tab, x8, dx, y_dtype=torch_dev.float32), auto) or m <= 16
+    if m > 32:
+        assert torch_dev.equal(auto, outs["gemm_mfma"])
 
 
 def test_selection_table_drives_dispatch(torch_dev):
