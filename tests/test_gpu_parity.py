@@ -113,6 +113,29 @@ def test_gemv_model_dtype(torch_dev, bits, group, m):
     assert R.eps_comp(_np(y32), y_ref, "fp32") <= 1e-5
 
 
+@pytest.mark.parametrize("bits", [1, 2])
+@pytest.mark.parametrize("group", [32, 128, 512])
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+def test_gemv_w1_w2_direct(torch_dev, bits, group, dtype):
+    # W1/W2 single rows take the table-free decode (level pairs in the
+    # activation dtype, two-term dot products): both single-row forms, BF16
+    # and FP16 activations, 2560 codes (a ragged second column block), 301
+    # rows (a lone last row), FP32 and activation-dtype outputs
+    n, k = 301, 2560
+    r = fitted(640 + bits, n, k, bits, group)
+    xb, xv = act(641 + bits, 1, k, dtype)
+    y_ref = ref_model_dtype(xv, r, bits, group)
+    cq = _cq()
+    w = _weight(r, bits, group)
+    x = _x(torch_dev, xb, dtype)
+    for fam in ("gemv_stream", "gemv_rows"):
+        say("gemv w1/w2 direct", bits, group, dtype, fam)
+        y32 = cq.cq_gemm_model_dtype_family(w, x, fam, y_dtype=torch_dev.float32)
+        assert R.eps_comp(_np(y32), y_ref, "fp32") <= 1e-5, fam
+        yd = cq.cq_gemm_model_dtype_family(w, x, fam)
+        assert R.eps_comp(_np(yd), y_ref, dtype) <= TOL, fam
+
+
 @pytest.mark.parametrize("bits", [2, 3, 4, 8])
 @pytest.mark.parametrize("m", [1, 16])
 def test_gemv_model_dtype_fp16(torch_dev, bits, m):
