@@ -170,8 +170,9 @@ def routed_sweep(torch, cq, bits=4, group=128, token_counts=(1, 4, 16, 64)):
         banks.append(banks[0].clone())  # two banks alternate (together above the 256 MB Infinity Cache)
         del w1
         cases = [(t, route_map(7100 + t, t, MOE_EXPERTS, MOE_TOPK)) for t in token_counts]
-        # a skewed map: 8 tokens all routed to one expert (8 routes <= 8 experts,
-        # so the streaming mode runs and streams that expert once per route)
+        # a skewed map: 8 tokens all routed to one expert (more routes than half
+        # the experts, so the expert-grouped mode decodes that expert's tiles
+        # once for all 8 routes)
         cases.append((8, (np.arange(8, dtype=np.int32), np.zeros(8, dtype=np.int32))))
         for t, (tok, exp) in cases:
             tt = torch.from_numpy(tok).cuda()

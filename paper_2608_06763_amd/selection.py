@@ -9,7 +9,8 @@ For one operator signature (path, B, G, N, K, activation dtype) the tuner
      selected),
   3. times the valid ones with HIP events on the launch stream over rotated
      copies of the weight, so that every timed call streams its weight from
-     HBM,
+     HBM, in three rounds over all valid families (alternating order) and
+     keeps each family's median round,
   4. maps every row count to its fastest family: each representative row
      count owns the rows up to the geometric midpoint towards the next one,
      and neighbouring regimes with the same family merge.
@@ -51,18 +52,15 @@ def device_signature() -> dict:
             "hip": torch.version.hip}
 
 
-def _timed(torch, fn, calls: int) -> float:
-    """Median over three batches of the mean time per call, microseconds."""
+def _batch(torch, fn, calls: int) -> float:
+    """Mean time per call of one batch of ``calls`` back-to-back calls, microseconds."""
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    out = []
-    for _ in range(3):
-        e0.record()
-        for i in range(calls):
-            fn(i)
-        e1.record()
-        e1.synchronize()
-        out.append(e0.elapsed_time(e1) * 1e3 / calls)
-    return float(np.median(out))
+    e0.record()
+    for i in range(calls):
+        fn(i)
+    e1.record()
+    e1.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / calls
 
 
 def regimes(ms, choice):
@@ -112,6 +110,7 @@ def tune(w: CQWeight, path: int, ms, x_dtype=None, activations=None, target_ms: 
             run = lambda f, c, out: cq_gemm_a8_family(c, x8, dx, f, out=out)
         scale = float(ref.abs().max()) or 1.0
         timings[m] = {}
+        calls = {}
         for f in names:
             if not cq_family_supported(path, f, w, m):
                 continue
@@ -122,9 +121,16 @@ def tune(w: CQWeight, path: int, ms, x_dtype=None, activations=None, target_ms: 
                 continue
             run(f, copies[0], y)
             torch.cuda.synchronize()
-            t0 = _timed(torch, lambda i: run(f, copies[i % len(copies)], y), 2)
-            calls = int(min(max_calls, max(len(copies), target_ms * 1e3 / max(t0, 1e-3))))
-            timings[m][f] = _timed(torch, lambda i: run(f, copies[i % len(copies)], y), calls)
+            t0 = min(_batch(torch, lambda i: run(f, copies[i % len(copies)], y), 2) for _ in range(3))
+            calls[f] = int(min(max_calls, max(len(copies), target_ms * 1e3 / max(t0, 1e-3))))
+        # three rounds over all candidates, the order reversed every other round,
+        # so that no family is timed only right after the host work between row
+        # counts (clock ramp); the median batch per family is kept
+        samples = {f: [] for f in calls}
+        for r in range(3):
+            for f in (list(calls) if r % 2 == 0 else list(calls)[::-1]):
+                samples[f].append(_batch(torch, lambda i: run(f, copies[i % len(copies)], y), calls[f]))
+        timings[m] = {f: float(np.median(v)) for f, v in samples.items()}
         choice[m] = min(timings[m], key=lambda f: timings[m][f])
         if log:
             log(f"[select] path {path} m={m}: " + ", ".join(f"{f} {t:.1f} us" for f, t in timings[m].items())
