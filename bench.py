@@ -122,7 +122,7 @@ def _cpu_baseline_run(layers_np, bits, group, budget_s, blas_threads, gpu_out):
     from oracle import a8 as A8
     from oracle import format as F
     from oracle import ref as R
-    frac = 1.0 / 2
+    frac = 1.0  # every row: about 26 s of oracle work on a 16-core host
     done_bytes, spent, rows_done = 0.0, 0.0, 0
     parity = {"model_dtype_eps_comp_max": 0.0, "rows_checked": 0, "a8_x8_dx_bitexact": True}
     for li, (name, k, n, codes, s, a, b, x_vals) in enumerate(layers_np):
@@ -147,8 +147,9 @@ def _cpu_baseline_run(layers_np, bits, group, budget_s, blas_threads, gpu_out):
             break
     return {"value": done_bytes / spent / 1e9, "unit": "GB/s", "cores": int(blas_threads), "kind": "oracle",
             "cpu_model": cpu_model(), "cpu_mhz": cpu_mhz(), "host_cpus": os.cpu_count(),
-            "sample": f"oracle unpack+decode(fp64)+product on {rows_done} weight rows "
-                      f"(first half of each decode layer, M=1), {spent:.1f} s; elementwise numpy on 1 thread, "
+            "sample": f"oracle unpack+decode(fp64)+product on {rows_done} of the "
+                      f"{sum(l[2] for l in layers_np)} weight rows of the decode layers (whole layers in order "
+                      f"until {budget_s:.0f} s are spent, M=1), {spent:.1f} s; elementwise numpy on 1 thread, "
                       f"product on {blas_threads} BLAS threads",
             "parity": None if gpu_out is None else
             dict(parity, bar="eps_comp <= 2e-3 (bf16 output) on the sampled rows of the timed step's outputs; "
