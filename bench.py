@@ -122,7 +122,7 @@ def _cpu_baseline_run(layers_np, bits, group, budget_s, blas_threads, gpu_out):
     from oracle import a8 as A8
     from oracle import format as F
     from oracle import ref as R
-    frac = 1.0  # every row: about 26 s of oracle work on a 16-core host
+    frac = 1.0  # every row: 26-28 s of oracle work on a 16-core host
     done_bytes, spent, rows_done = 0.0, 0.0, 0
     parity = {"model_dtype_eps_comp_max": 0.0, "rows_checked": 0, "a8_x8_dx_bitexact": True}
     for li, (name, k, n, codes, s, a, b, x_vals) in enumerate(layers_np):
