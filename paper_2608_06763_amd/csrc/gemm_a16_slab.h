@@ -777,7 +777,18 @@ hipError_t slab_st_launch_x(const cq_weight &w, const void *x, int64_t m, void *
     const int64_t tiles = (m + 16 * XB - 1) / (16 * XB) * tiles_n;
     if (tiles > 0x7fffffff) return hipErrorInvalidValue;
     const int64_t nsw = w.k / w.group / 4;
-    int64_t s = int64_t(device_cu_count()) * 16 / tiles;
+    // waves per workgroup: about 8 waves per compute unit over the grid,
+    // rounded up with up to 4 rows and down above, then down to a power of
+    // two (two x-row blocks: 16 per compute unit), so that each wave walks a
+    // longer run of sweeps than with 16 (measured, W4 G128, K x N: 4096 x
+    // 28672 and 8192 x 28672 at 8-16 rows 7-15% faster with one wave instead
+    // of two, at 2-4 rows keeping two; 14336 x 4096 at 2-8 rows 8-18% faster
+    // with 8 instead of 16; 8192 x 8192 at 2-4 rows 25-30% faster with 4
+    // instead of 8; 4096 x 14336 at 2-4 rows 2 better than 3 or 4)
+    const int64_t cus = device_cu_count();
+    int64_t s = XB == 2 ? cus * 16 / tiles : m <= 4 ? (cus * 8 + tiles - 1) / tiles : cus * 8 / tiles;
+    if (XB == 1)
+        while (s & (s - 1)) s &= s - 1;
     if (s > (XT ? 8 : 16)) s = XT ? 8 : 16;  // the kernel's launch bound
     if (s > nsw) s = nsw;
     // LDS: tables below 64 KB, whole workgroup within 128 KB
