@@ -778,17 +778,20 @@ hipError_t slab_st_launch_x(const cq_weight &w, const void *x, int64_t m, void *
     if (tiles > 0x7fffffff) return hipErrorInvalidValue;
     const int64_t nsw = w.k / w.group / 4;
     // waves per workgroup: about 8 waves per compute unit over the grid,
-    // rounded up with up to 4 rows and down above, then down to a power of
-    // two (two x-row blocks: 16 per compute unit), so that each wave walks a
-    // longer run of sweeps than with 16 (measured, W4 G128, K x N: 4096 x
-    // 28672 and 8192 x 28672 at 8-16 rows 7-15% faster with one wave instead
-    // of two, at 2-4 rows keeping two; 14336 x 4096 at 2-8 rows 8-18% faster
-    // with 8 instead of 16; 8192 x 8192 at 2-4 rows 25-30% faster with 4
-    // instead of 8; 4096 x 14336 at 2-4 rows 2 better than 3 or 4)
+    // rounded up with up to 4 rows and down above (two x-row blocks: about
+    // 4), then down to a power of two, so that each wave walks a longer run
+    // of sweeps than with 16 per compute unit (measured, W4 G128, K x N:
+    // 4096 x 28672 and 8192 x 28672 at 8-16 rows 7-15% faster with one wave
+    // instead of two, at 2-4 rows keeping two; 14336 x 4096 at 2-8 rows 8-18%
+    // faster with 8 instead of 16; 8192 x 8192 at 2-4 rows 25-30% faster
+    // with 4 instead of 8; 4096 x 14336 at 2-4 rows 2 better than 3 or 4;
+    // two blocks at 24-32 rows: 8192 x 28672 and 4096 x 28672 16-17% faster
+    // with one wave instead of two, 14336 x 4096 10-16% with 4 instead of 8,
+    // 4096 x 6144 21-26% with 2 instead of 7, 8192 x 8192 5-9% with 2
+    // instead of 7)
     const int64_t cus = device_cu_count();
-    int64_t s = XB == 2 ? cus * 16 / tiles : m <= 4 ? (cus * 8 + tiles - 1) / tiles : cus * 8 / tiles;
-    if (XB == 1)
-        while (s & (s - 1)) s &= s - 1;
+    int64_t s = XB == 2 ? cus * 4 / tiles : m <= 4 ? (cus * 8 + tiles - 1) / tiles : cus * 8 / tiles;
+    while (s & (s - 1)) s &= s - 1;
     if (s > (XT ? 8 : 16)) s = XT ? 8 : 16;  // the kernel's launch bound
     if (s > nsw) s = nsw;
     // LDS: tables below 64 KB, whole workgroup within 128 KB
