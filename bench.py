@@ -122,13 +122,16 @@ def _cpu_baseline_run(layers_np, bits, group, budget_s, blas_threads, gpu_out):
     from oracle import a8 as A8
     from oracle import format as F
     from oracle import ref as R
-    frac = 1.0  # every row of the layers that fit the budget
+    frac = 1.0  # every row where the budget allows
     done_bytes, spent, rows_done = 0.0, 0.0, 0
     parity = {"model_dtype_eps_comp_max": 0.0, "rows_checked": 0, "a8_x8_dx_bitexact": True}
     for li, (name, k, n, codes, s, a, b, x_vals) in enumerate(layers_np):
         rows = max(1, int(n * frac))
-        if spent > 0 and spent + spent / done_bytes * a16_bytes(1, rows, k, bits, group) > budget_s:
-            continue  # this layer would take the sample past its budget
+        if spent > 0:
+            # a leading share of the layer where the whole one would take the
+            # sample past its budget (at least 256 rows of every layer)
+            per_row = spent / done_bytes * a16_bytes(1, 1, k, bits, group)
+            rows = min(rows, max(256, int((budget_s - spent) / per_row)))
         packed = F.pack(codes[:rows], bits)  # the packed input the oracle starts from (not timed)
         t0 = time.perf_counter()
         kk = F.unpack(packed, bits, k)
@@ -148,8 +151,9 @@ def _cpu_baseline_run(layers_np, bits, group, budget_s, blas_threads, gpu_out):
     return {"value": done_bytes / spent / 1e9, "unit": "GB/s", "cores": int(blas_threads), "kind": "oracle",
             "cpu_model": cpu_model(), "cpu_mhz": cpu_mhz(), "host_cpus": os.cpu_count(),
             "sample": f"oracle unpack+decode(fp64)+product on {rows_done} of the "
-                      f"{sum(l[2] for l in layers_np)} weight rows of the decode layers (whole layers in order, "
-                      f"each taken while its estimated time keeps the sample within {budget_s:.0f} s, M=1), "
+                      f"{sum(l[2] for l in layers_np)} weight rows of the decode layers (layers in order, "
+                      f"each whole or its leading rows as far as the estimated time keeps the sample within "
+                      f"{budget_s:.0f} s, at least 256 rows each, M=1), "
                       f"{spent:.1f} s; elementwise numpy on 1 thread, "
                       f"product on {blas_threads} BLAS threads",
             "parity": None if gpu_out is None else
