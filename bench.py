@@ -123,14 +123,14 @@ def _cpu_baseline_run(layers_np, bits, group, budget_s, blas_threads, gpu_out):
     from oracle import format as F
     from oracle import ref as R
     frac = 1.0  # every row where the budget allows
-    done_bytes, spent, rows_done = 0.0, 0.0, 0
+    done_bytes, spent, rows_done, done_weights = 0.0, 0.0, 0, 0
     parity = {"model_dtype_eps_comp_max": 0.0, "rows_checked": 0, "a8_x8_dx_bitexact": True}
     for li, (name, k, n, codes, s, a, b, x_vals) in enumerate(layers_np):
         rows = max(1, int(n * frac))
         if spent > 0:
             # a leading share of the layer where the whole one would take the
             # sample past its budget (at least 256 rows of every layer)
-            per_row = spent / done_bytes * a16_bytes(1, 1, k, bits, group)
+            per_row = spent / done_weights * k
             rows = min(rows, max(256, int((budget_s - spent) / per_row)))
         packed = F.pack(codes[:rows], bits)  # the packed input the oracle starts from (not timed)
         t0 = time.perf_counter()
@@ -139,6 +139,7 @@ def _cpu_baseline_run(layers_np, bits, group, budget_s, blas_threads, gpu_out):
         spent += time.perf_counter() - t0
         done_bytes += a16_bytes(1, rows, k, bits, group)
         rows_done += rows
+        done_weights += rows * k
         assert y.shape == (1, rows)
         if gpu_out is not None:
             y_gpu, x8_gpu, dx_gpu = gpu_out[li]
