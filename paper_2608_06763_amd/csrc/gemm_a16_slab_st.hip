@@ -14,11 +14,14 @@ bool gemm_a16_slab_staged_supported(const cq_weight &w, int64_t m) {
 bool gemm_a16_slab_staged_preferred(const cq_weight &w, int64_t m) {
     if (!gemm_a16_slab_staged_supported(w, m)) return false;
     // the second x-row block pays for itself on short K too once it is
-    // mostly full (measured on 4096 and 6144 weight rows over K = 4096)
-    if (m >= 28 || (m >= 24 && w.n > 4096)) return true;
-    // the launch's split of K: about 16 waves per compute unit over the chip,
-    // at most 8 with the transposing activation loads (above 8 rows); above
-    // 16 rows a wave serves 32
+    // mostly full, and from 17 rows on more than 4096 weight rows (measured
+    // on 4096 and 6144 weight rows over K = 4096: 6144 rows at 17-23 rows
+    // 20.1-20.2 us against 21.1-24.4 for the plain kernel, 4096 rows slower)
+    if (m >= 28 || (m > 16 && w.n > 4096)) return true;
+    // two or more sweeps per wave when K is split over about 16 waves per
+    // compute unit, at most 8 with the transposing activation loads (above 8
+    // rows), a wave serving 32 rows above 16 (the test as it was measured;
+    // the launch itself now runs fewer waves with longer runs)
     const int64_t tiles = (w.n + 15) / 16 * (m > 16 ? 1 : (m + 15) / 16);
     int64_t s = int64_t(256) * 16 / tiles;
     const int64_t s_max = m > 8 ? 8 : 16;

@@ -272,7 +272,7 @@ def test_builtin_rules(clean_table, bits, group, m, md, a8):
     (28672, 8192, 4, "gemm_slab_staged"), (28672, 4096, 16, "gemm_slab_staged"), (4096, 14336, 2, "gemm_slab_staged"),
     (6144, 4096, 4, "gemm_slab"), (4096, 4096, 8, "gemm_slab"), (28672, 8192, 1, "gemv_rows"),
     (4096, 14336, 1, "gemv_rows"), (6144, 4096, 1, "gemv_stream"),
-    (28672, 8192, 24, "gemm_slab_staged"), (4096, 4096, 17, "gemm_slab"), (6144, 4096, 21, "gemm_slab"), (6144, 4096, 24, "gemm_slab_staged"), (4096, 4096, 24, "gemm_slab"),
+    (28672, 8192, 24, "gemm_slab_staged"), (4096, 4096, 17, "gemm_slab"), (6144, 4096, 21, "gemm_slab_staged"), (6144, 4096, 17, "gemm_slab_staged"), (6144, 4096, 24, "gemm_slab_staged"), (4096, 4096, 24, "gemm_slab"),
     (4096, 4096, 32, "gemm_slab_staged"),
     (4096, 14336, 17, "gemm_slab_staged"),
     (28672, 8192, 33, "gemm_mfma")])
